@@ -1,0 +1,328 @@
+"""CPU oracle of the Book-Keeping (BK) clipping path -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this module.  It shares no code with the HIP library: it is a plain,
+slow, float64 restatement of what the paper defines, written so it can be
+checked against the paper by eye.
+
+Reference: Bu, Wang, Zha, Karypis, "Differentially Private Optimization on
+Large Model at Small Cost" (ICML 2023, arXiv 2210.00038).
+
+What is computed, and where the paper defines it
+------------------------------------------------
+* use_ghost             -- Section 3.2 (layerwise decision / mixed ghost norm):
+                           ghost norm iff 2 T^2 < p d, instantiate otherwise.
+* linear_norm_sq        -- per-sample squared gradient norm ||a_i^T g_i||_F^2,
+                           the left-hand side of eq. (ghost norm) in Section 2.1
+                           and the per-sample gradient of App. B.4.1.  This is
+                           the definition, used for ghost and instantiated
+                           layers alike (both compute the same number).
+* linear_norm_sq_gram   -- the right-hand side of eq. (ghost norm): the inner
+                           product of the two T x T Gram matrices (App. B.4).
+* embed_norm_sq         -- the same definition for an embedding layer, whose
+                           input is the one-hot encoding of the token ids.
+* aggregate             -- Algorithm 1, aggregation across layers.
+* clip_factors          -- eq. (DP optimizers): Abadi min(R/||g||, 1) and
+                           automatic clipping 1/(||g|| + gamma).
+* weighted_grad         -- Algorithm 1, sum of clipped gradients
+                           a^T diag(C) dL/ds (App. B.3 with the clip weights).
+* embed_weighted_grad   -- the same for an embedding layer.
+* philox4x32_10 / noise -- Algorithm 1, Gaussian noise sigma R N(0, I).  The
+                           paper does not fix a generator; the reading used
+                           here is Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
+                           "Parallel random numbers: as easy as 1, 2, 3",
+                           SC'11) with the Box-Muller transform (Box & Muller,
+                           1958); layout in ``noise``.
+
+Readings where the paper is silent or inconsistent
+--------------------------------------------------
+* Gram orientation: the T x T Grams a_i a_i^T and g_i g_i^T of eq. (ghost norm)
+  (the appendix algorithms print d x d / p x p products, which do not match).
+* Ties 2 T^2 == p d instantiate (Section 3.2 wording).
+* Abadi clipping at ||g|| = 0 gives C = 1; automatic clipping with gamma = 0
+  at ||g|| = 0 gives C = 0 (that sample's gradient is zero).
+* Losses are summed (L = sum_i L_i), so the clipped gradient is a sum, not a
+  mean, over the batch.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "use_ghost", "linear_norm_sq", "linear_norm_sq_gram", "linear_norm_sq_bruteforce",
+    "embed_norm_sq", "embed_norm_sq_pairs", "aggregate", "clip_factors", "weighted_grad",
+    "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
+    "box_muller", "noise", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
+    "bk_layer_norm", "bk_stack",
+]
+
+F64 = np.float64
+
+
+def _f64(x) -> np.ndarray:
+    """Exact upcast of float32 / bfloat16 (torch) or numpy input to float64."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            return x.detach().to("cpu", torch.float64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.asarray(x, dtype=F64)
+
+
+def _ids(x) -> np.ndarray:
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            return x.detach().to("cpu", torch.int64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.asarray(x, dtype=np.int64)
+
+
+# --------------------------------------------------------------------------
+# Section 3.2: which way to compute a layer's per-sample norms
+# --------------------------------------------------------------------------
+def use_ghost(T: int, d: int, p: int) -> bool:
+    """Ghost norm iff 2 T^2 < p d (space of the two Grams vs one per-sample
+    gradient, Table "block complexity"); ties instantiate."""
+    return 2 * int(T) * int(T) < int(p) * int(d)
+
+
+# --------------------------------------------------------------------------
+# Per-sample squared gradient norms of a linear layer s = a W, W in R^{d x p}
+# --------------------------------------------------------------------------
+def linear_norm_sq(a, g) -> np.ndarray:
+    """||dL_i/dW||_F^2 with dL_i/dW = a_i^T g_i  (a: [B,T,d], g: [B,T,p]) -> [B]."""
+    a = _f64(a)
+    g = _f64(g)
+    B = a.shape[0]
+    out = np.zeros(B, dtype=F64)
+    for i in range(B):
+        grad_i = a[i].T @ g[i]            # d x p per-sample gradient
+        out[i] = np.sum(grad_i * grad_i)
+    return out
+
+
+def linear_norm_sq_gram(a, g) -> np.ndarray:
+    """vec(g_i g_i^T) . vec(a_i a_i^T), the ghost-norm form of the same number."""
+    a = _f64(a)
+    g = _f64(g)
+    B = a.shape[0]
+    out = np.zeros(B, dtype=F64)
+    for i in range(B):
+        ga = a[i] @ a[i].T                # T x T
+        gg = g[i] @ g[i].T                # T x T
+        out[i] = np.sum(ga * gg)
+    return out
+
+
+def linear_norm_sq_bruteforce(a, g) -> list:
+    """Pure-Python loops over every entry of every per-sample gradient (tiny inputs)."""
+    a = _f64(a).tolist()
+    g = _f64(g).tolist()
+    res = []
+    for ai, gi in zip(a, g):
+        T, d, p = len(ai), len(ai[0]) if ai else 0, len(gi[0]) if gi else 0
+        s = 0.0
+        for j in range(d):
+            for k in range(p):
+                e = 0.0
+                for t in range(T):
+                    e += ai[t][j] * gi[t][k]
+                s += e * e
+        res.append(s)
+    return res
+
+
+# --------------------------------------------------------------------------
+# Embedding layer: a_i is the one-hot encoding of the ids x_i in R^{T x V}
+# --------------------------------------------------------------------------
+def embed_norm_sq(ids, g, V: int) -> np.ndarray:
+    """||one_hot(x_i)^T g_i||_F^2 = sum_v ||sum_{t: x_it = v} g_it||^2 -> [B]."""
+    ids = _ids(ids)
+    g = _f64(g)
+    B, T, p = g.shape
+    out = np.zeros(B, dtype=F64)
+    for i in range(B):
+        rows = np.zeros((V, p), dtype=F64)      # dL_i/dW of the embedding table
+        np.add.at(rows, ids[i], g[i])
+        out[i] = np.sum(rows * rows)
+    return out
+
+
+def embed_norm_sq_pairs(ids, g) -> np.ndarray:
+    """Same number as a double sum over token pairs with equal ids."""
+    ids = _ids(ids)
+    g = _f64(g)
+    B, T, p = g.shape
+    out = np.zeros(B, dtype=F64)
+    for i in range(B):
+        same = (ids[i][:, None] == ids[i][None, :]).astype(F64)   # a_i a_i^T
+        out[i] = np.sum(same * (g[i] @ g[i].T))
+    return out
+
+
+# --------------------------------------------------------------------------
+# Algorithm 1: aggregate over layers, clip factors, clipped gradient
+# --------------------------------------------------------------------------
+def aggregate(norms_sq) -> np.ndarray:
+    """||dL_i/dW||_F^2 = sum_l ||dL_i/dW_(l)||_F^2 ; norms_sq: [L, B] -> [B]."""
+    n = _f64(norms_sq)
+    tot = np.zeros(n.shape[1], dtype=F64)
+    for l in range(n.shape[0]):
+        tot = tot + n[l]
+    return tot
+
+
+def clip_factors(total_sq, mode: str, R: float = 1.0, gamma: float = 0.01) -> np.ndarray:
+    """C_i from the total squared norm: 'abadi' -> min(R/||g_i||, 1),
+    'auto' -> 1 / (||g_i|| + gamma)."""
+    nrm = np.sqrt(_f64(total_sq))
+    C = np.empty_like(nrm)
+    for i, v in enumerate(nrm):
+        if mode == "abadi":
+            if R <= 0:
+                raise ValueError("Abadi clipping needs R > 0")
+            C[i] = 1.0 if v <= R else R / v
+        elif mode == "auto":
+            den = v + gamma
+            C[i] = 0.0 if den == 0.0 else 1.0 / den
+        else:
+            raise ValueError(mode)
+    return C
+
+
+def weighted_grad(a, g, C) -> np.ndarray:
+    """G = a^T diag(C) g = sum_i C_i a_i^T g_i  -> [d, p]."""
+    a = _f64(a)
+    g = _f64(g)
+    C = _f64(C)
+    B, T, d = a.shape
+    p = g.shape[2]
+    c_row = np.repeat(C, T)                          # weight of every token row
+    return a.reshape(B * T, d).T @ (c_row[:, None] * g.reshape(B * T, p))
+
+
+def embed_weighted_grad(ids, g, C, V: int) -> np.ndarray:
+    """G[v, :] = sum_i C_i sum_{t: x_it = v} g_it  -> [V, p] (every row present)."""
+    ids = _ids(ids)
+    g = _f64(g)
+    C = _f64(C)
+    B, T, p = g.shape
+    G = np.zeros((V, p), dtype=F64)
+    np.add.at(G, ids.reshape(-1), np.repeat(C, T)[:, None] * g.reshape(B * T, p))
+    return G
+
+
+# --------------------------------------------------------------------------
+# Gaussian noise: Philox4x32-10 + Box-Muller
+# --------------------------------------------------------------------------
+# Round multipliers and key increments of Philox4x32 (Salmon et al., SC'11).
+PHILOX_M0 = 0xD2511F53
+PHILOX_M1 = 0xCD9E8D57
+PHILOX_W0 = 0x9E3779B9
+PHILOX_W1 = 0xBB67AE85
+_MASK32 = np.uint64(0xFFFFFFFF)
+
+
+def philox4x32_10(counter, key):
+    """Philox4x32 with 10 rounds on arrays of counters.
+
+    counter: (c0, c1, c2, c3), key: (k0, k1); each entry a scalar or an array
+    of uint32 values.  A round multiplies c0 and c2 by the two multipliers,
+    keeps both 32-bit halves of each product, and mixes:
+        (c0, c1, c2, c3) <- (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0));
+    the key is advanced by the two Weyl constants between rounds.
+    Returns four uint32 arrays."""
+    c0, c1, c2, c3 = (np.asarray(c, dtype=np.uint64) & _MASK32 for c in counter)
+    k0 = np.asarray(key[0], dtype=np.uint64) & _MASK32
+    k1 = np.asarray(key[1], dtype=np.uint64) & _MASK32
+    m0 = np.uint64(PHILOX_M0)
+    m1 = np.uint64(PHILOX_M1)
+    for rnd in range(10):
+        if rnd > 0:
+            k0 = (k0 + np.uint64(PHILOX_W0)) & _MASK32
+            k1 = (k1 + np.uint64(PHILOX_W1)) & _MASK32
+        p0 = m0 * c0                              # < 2^64, exact in uint64
+        p1 = m1 * c2
+        hi0, lo0 = p0 >> np.uint64(32), p0 & _MASK32
+        hi1, lo1 = p1 >> np.uint64(32), p1 & _MASK32
+        c0, c1, c2, c3 = hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0
+    return tuple(x.astype(np.uint32) for x in (c0, c1, c2, c3))
+
+
+def philox_words(seed: int, tensor_id: int, step: int, q0: int, nq: int) -> np.ndarray:
+    """Raw words of counter blocks q0 .. q0+nq-1 -> uint32 [nq, 4].
+
+    Counter block q of tensor `tensor_id` at step `step` is
+    (q mod 2^32, q div 2^32, tensor_id, step) under key (seed mod 2^32, seed div 2^32)."""
+    q = np.arange(q0, q0 + nq, dtype=np.uint64)
+    key = (np.uint64(seed & 0xFFFFFFFF), np.uint64((seed >> 32) & 0xFFFFFFFF))
+    w = philox4x32_10((q & _MASK32, q >> np.uint64(32),
+                       np.full_like(q, tensor_id & 0xFFFFFFFF), np.full_like(q, step & 0xFFFFFFFF)), key)
+    return np.stack(w, axis=1)
+
+
+def uniforms_from_words(x) -> np.ndarray:
+    """u = (2 * (x >> 9) + 1) / 2^24: odd multiples of 2^-24, strictly inside (0, 1)."""
+    x = np.asarray(x, dtype=np.uint64)
+    return ((x >> np.uint64(9)).astype(F64) * 2.0 + 1.0) / float(1 << 24)
+
+
+def box_muller(u_r, u_theta):
+    """(r cos 2 pi u_theta, r sin 2 pi u_theta) with r = sqrt(-2 ln u_r)."""
+    r = np.sqrt(-2.0 * np.log(u_r))
+    th = 2.0 * np.pi * u_theta
+    return r * np.cos(th), r * np.sin(th)
+
+
+def noise(n: int, seed: int, tensor_id: int, step: int) -> np.ndarray:
+    """n standard normal draws for elements 0..n-1 of one tensor (float64).
+
+    Element e uses word e mod 4 of counter block q = e div 4; words (0, 1) give
+    elements 4q and 4q+1 via Box-Muller (word 0 -> radius, word 1 -> angle),
+    words (2, 3) give elements 4q+2 and 4q+3 the same way."""
+    nq = (n + 3) // 4
+    w = philox_words(seed, tensor_id, step, 0, nq)
+    u = uniforms_from_words(w)
+    z = np.empty((nq, 4), dtype=F64)
+    z[:, 0], z[:, 1] = box_muller(u[:, 0], u[:, 1])
+    z[:, 2], z[:, 3] = box_muller(u[:, 2], u[:, 3])
+    return z.reshape(-1)[:n]
+
+
+def add_noise(G, std: float, seed: int, tensor_id: int, step: int) -> np.ndarray:
+    """G_hat = G + std * N(0, I), std = sigma * R (Algorithm 1, noise step)."""
+    G = _f64(G)
+    return G + std * noise(G.size, seed, tensor_id, step).reshape(G.shape)
+
+
+# --------------------------------------------------------------------------
+# Whole path (Algorithm 1 from "norms" to "noise", BK-MixGhostClip choice of
+# norm per layer from Algorithm "BKAL-mixed")
+# --------------------------------------------------------------------------
+def bk_layer_norm(layer_kind: str, x, g, V: int = 0) -> np.ndarray:
+    if layer_kind == "embed":
+        return embed_norm_sq(x, g, V)
+    return linear_norm_sq(x, g)
+
+
+def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed: int,
+             step: int = 0, with_noise: bool = True):
+    """layers: objects with .kind, .T, .d, .p; inputs: list of (a or ids, g).
+
+    Returns dict with per-layer norms [L, B], totals [B], C [B], the clipped
+    gradients G_l (before noise) and, if with_noise, G_hat_l with tensor_id = l."""
+    norms = np.stack([bk_layer_norm(L.kind, x, g, L.d) for L, (x, g) in zip(layers, inputs)])
+    total = aggregate(norms)
+    C = clip_factors(total, mode, R, gamma)
+    G, Ghat = [], []
+    for l, (L, (x, g)) in enumerate(zip(layers, inputs)):
+        Gl = embed_weighted_grad(x, g, C, L.d) if L.kind == "embed" else weighted_grad(x, g, C)
+        G.append(Gl)
+        if with_noise:
+            Ghat.append(add_noise(Gl, std, seed, l, step))
+    return {"norms": norms, "total": total, "C": C, "G": G, "Ghat": Ghat,
+            "paths": [("embed" if L.kind == "embed" else ("ghost" if use_ghost(L.T, L.d, L.p) else "inst"))
+                      for L in layers]}
