@@ -1,0 +1,223 @@
+/*
+ * bk.h -- C ABI of the Book-Keeping (BK) differentially private gradient path
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Bu, Wang, Zha, Karypis, "Differentially Private Optimization on
+ * Large Model at Small Cost" (ICML 2023, arXiv 2210.00038).  Starting from the
+ * activations a and output gradients dL/ds that one back-propagation keeps
+ * ("book-keeping", Section 2.1), the library computes, for every generalized
+ * linear layer s = a W with W in R^{d x p} (App. B, eq. "linear layer mat
+ * multi"):
+ *
+ *   1. per-sample squared gradient norms ||a_i^T g_i||_F^2, by the ghost-norm
+ *      trick (eq. "ghost norm", App. B.4) or by instantiating the per-sample
+ *      gradient (App. B.4.1), whichever the layerwise rule of Section 3.2
+ *      picks;
+ *   2. their sum over layers and the per-sample clip factors C_i
+ *      (Algorithm 1, aggregation and clipping; clip functions of eq. "DP
+ *      optimizers");
+ *   3. the sum of clipped gradients G = a^T diag(C) dL/ds (Algorithm 1, sum of
+ *      clipped gradients; App. B.3);
+ *   4. G_hat = G + sigma R N(0, I) (Algorithm 1, noise step).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the library never
+ *    allocates, frees or keeps them.  Workspaces are caller-provided device
+ *    buffers of at least the size the matching *_workspace_size call returns
+ *    (a NULL workspace is accepted when that size is 0).
+ *  - Layout: row-major, contiguous.  a is [B, T, d], g = dL/ds is [B, T, p]
+ *    (sample-major, then token, then feature), both of the dtype `dt`; token
+ *    ids are int64 [B, T].  Outputs are float32 and are OVERWRITTEN.  Outputs
+ *    must not alias inputs.
+ *  - Sums over the batch, not means: the loss is L = sum_i L_i (Section 2.1).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call is
+ *    asynchronous and ordered on that stream; buffers must stay alive until
+ *    the stream has finished the work.
+ *  - Errors: every call returns a bk_status.  Argument checks (NULL pointers,
+ *    sizes >= 0, products overflowing int64, dtype, workspace size) run on the
+ *    host before any HIP call, so a rejected call does no work at all.  A
+ *    failed kernel launch returns BK_ERR_LAUNCH.  bk_last_error() gives a
+ *    human-readable detail of the calling thread's last failure.  Device
+ *    faults surface at the caller's next synchronisation, as for any kernel.
+ *  - Empty inputs (B == 0 or T == 0) are valid: norms are 0, C is not touched
+ *    beyond its B entries, G is all zeros (plus noise where noise is asked for).
+ *  - Results are deterministic: the same inputs on the same device give the
+ *    same bits (no floating-point atomics).
+ *  - Thread safety: every call is re-entrant; calls that share a workspace
+ *    must be ordered on one stream.
+ */
+#ifndef BK_H
+#define BK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BK_OK = 0,
+    BK_ERR_INVALID_VALUE = 1,   /* bad pointer, size, enum or scalar */
+    BK_ERR_NOT_SUPPORTED = 2,   /* valid request beyond what this build handles */
+    BK_ERR_WORKSPACE = 3,       /* workspace smaller than *_workspace_size */
+    BK_ERR_LAUNCH = 4           /* a HIP call failed; see bk_last_error() */
+} bk_status;
+
+typedef enum { BK_F32 = 0, BK_BF16 = 1 } bk_dtype;
+
+/* Clip functions of eq. "DP optimizers":
+ *   BK_CLIP_ABADI: C_i = min(R / ||g_i||, 1)       (C_i = 1 when ||g_i|| = 0)
+ *   BK_CLIP_AUTO : C_i = 1 / (||g_i|| + gamma)     (automatic clipping; gamma = 0
+ *                  is pure normalisation, and C_i = 0 when ||g_i|| = 0 there) */
+typedef enum { BK_CLIP_ABADI = 0, BK_CLIP_AUTO = 1 } bk_clip;
+
+typedef enum { BK_LINEAR = 0, BK_EMBEDDING = 1 } bk_layer_kind;
+
+/* One generalized linear layer of a stack (used by the grouped calls).
+ *   kind == BK_LINEAR   : x = a [B, T, d] of dtype dt, g [B, T, p], G [d, p]
+ *   kind == BK_EMBEDDING: x = token ids int64 [B, T] (values in [0, d)),
+ *                         d = vocabulary size V, g [B, T, p], G [V, p]
+ * G may be NULL in calls that only compute norms. */
+typedef struct bk_layer {
+    int32_t kind;
+    int32_t reserved;        /* must be 0 */
+    int64_t T, d, p;
+    const void* x;
+    const void* g;
+    float* G;
+} bk_layer;
+
+/* Operation ids for bk_workspace_size. */
+typedef enum {
+    BK_OP_GHOST_NORM = 0,
+    BK_OP_INST_NORM = 1,
+    BK_OP_EMBED_GHOST_NORM = 2,
+    BK_OP_WEIGHTED_GRAD = 3,
+    BK_OP_EMBED_WEIGHTED_GRAD = 4
+} bk_op;
+
+/* ---------------------------------------------------------------------------
+ * Layerwise decision, Section 3.2 (mixed ghost norm): the ghost norm is used on
+ * a layer iff 2 T^2 < p d (the space of the two T x T Grams against that of one
+ * per-sample gradient, Table "block complexity"); otherwise the per-sample
+ * gradient is instantiated.  Ties instantiate.  Pure host function: returns 1
+ * for ghost, 0 for instantiation, -1 for negative sizes.
+ * ------------------------------------------------------------------------- */
+int bk_use_ghost(int64_t T, int64_t d, int64_t p);
+
+/* Workspace bytes `op` needs for one layer of these sizes (d = V for the
+ * embedding ops).  Returns 0 for an invalid request. */
+size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d, int64_t p);
+
+/* ---------------------------------------------------------------------------
+ * Ghost norm, eq. "ghost norm" (Section 2.1) and App. B.4:
+ *   norm_sq[i] = vec(g_i g_i^T) . vec(a_i a_i^T) = ||a_i^T g_i||_F^2
+ * from the two T x T Gram matrices of sample i, which are formed tile by tile
+ * on chip and never written to memory.
+ *   a [B,T,d], g [B,T,p] (dtype dt), norm_sq [B] float32 out.
+ * ------------------------------------------------------------------------- */
+bk_status bk_ghost_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T,
+                        int64_t d, int64_t p, float* norm_sq, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/* Per-sample gradient instantiation, App. B.4.1: the d x p gradient a_i^T g_i
+ * of every sample, reduced on chip to norm_sq[i] = ||a_i^T g_i||_F^2 (the
+ * per-sample gradients themselves are never stored).  Same arguments as
+ * bk_ghost_norm. */
+bk_status bk_inst_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T,
+                       int64_t d, int64_t p, float* norm_sq, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* Ghost norm of an embedding layer (Section 2.1 names the embedding among the
+ * generalized linear layers; App. D.1 lists it as ghost-norm only).  Its input
+ * a_i is the one-hot encoding of the ids x_i, so a_i a_i^T is the token-id
+ * equality matrix and
+ *   norm_sq[i] = sum_{t,t'} [x_it == x_it'] <g_it, g_it'>.
+ *   ids [B,T] int64 in [0, V), g [B,T,p] (dtype dt), norm_sq [B] out. */
+bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B,
+                              int64_t T, int64_t p, int64_t V, float* norm_sq, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Algorithm 1, aggregation and clipping:
+ *   total_sq[i] = sum_l norm_sq[l*B + i]   (l ascending, float64 accumulation)
+ *   C[i]        = clip(sqrt(total_sq[i]))  (bk_clip above)
+ *   norm_sq [L,B] float32 in; C [B] out; total_sq [B] out (may be NULL).
+ * R > 0 is required for BK_CLIP_ABADI, gamma >= 0 for BK_CLIP_AUTO. */
+bk_status bk_clip_factors(const float* norm_sq, int64_t L, int64_t B, bk_clip mode, float R,
+                          float gamma, float* C, float* total_sq, void* stream);
+
+/* Algorithm 1, sum of clipped gradients (App. B.3 with the clip weights):
+ *   G = a^T diag(C) g = sum_i C_i a_i^T g_i,   G [d,p] float32 out,
+ * one GEMM over the flattened B*T rows, C_i applied to the rows of g as they
+ * are loaded (for bf16 the product C_i g is rounded to bf16 before the MFMA). */
+bk_status bk_weighted_grad(const void* a, const void* g, const float* C, bk_dtype dt,
+                           int64_t B, int64_t T, int64_t d, int64_t p, float* G, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* The same for an embedding layer (a = one_hot(ids)):
+ *   G[v,:] = sum_i C_i sum_{t : x_it = v} g_it   for every v in [0, V),
+ * rows of ids that do not occur are zero.  Each row sums its tokens in
+ * ascending (i, t) order.  G [V,p] float32 out.  B*T <= 8192 in this build
+ * (BK_ERR_NOT_SUPPORTED above that). */
+bk_status bk_embed_weighted_grad(const int64_t* ids, const void* g, const float* C,
+                                 bk_dtype dt, int64_t B, int64_t T, int64_t p, int64_t V,
+                                 float* G, void* ws, size_t ws_bytes, void* stream);
+
+/* Algorithm 1, noise step: G[e] += std * z_e for e in [0, n), std = sigma R
+ * (App. A.1: the noise magnitude is sigma times the sensitivity R).
+ * z_e comes from Philox4x32-10 (Salmon et al., SC'11): counter block
+ * q = e / 4 is (q mod 2^32, q div 2^32, tensor_id, step) under the key
+ * (seed mod 2^32, seed div 2^32); its words (w0, w1, w2, w3) become uniforms
+ * u = (2 (w >> 9) + 1) / 2^24, and Box-Muller maps (u0, u1) to elements 4q,
+ * 4q+1 as (r cos 2 pi u1, r sin 2 pi u1), r = sqrt(-2 ln u0), and (u2, u3) to
+ * 4q+2, 4q+3 the same way.  std == 0 leaves G bit-identical. */
+bk_status bk_add_noise(float* G, int64_t n, float std, uint64_t seed, uint32_t tensor_id,
+                       uint32_t step, void* stream);
+
+/* Raw Philox4x32-10 words of counter blocks q0 .. q0+nq-1 of (seed, tensor_id,
+ * step), as used by bk_add_noise: out [nq, 4] uint32 (device). */
+bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64_t q0,
+                        int64_t nq, uint32_t* out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Grouped forms: the same computations for n layers in as few launches as
+ * possible.  Results are bit-identical to calling the per-layer form on each
+ * layer.  The bk_layer array is read on the host during the call only.
+ * ------------------------------------------------------------------------- */
+
+/* Norms of every layer: ghost or instantiated per bk_use_ghost for linear
+ * layers, the embedding ghost norm for embedding layers.  norm_sq [n,B] out,
+ * row l for layer l. */
+size_t bk_layer_norms_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B);
+bk_status bk_layer_norms(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
+                         float* norm_sq, void* ws, size_t ws_bytes, void* stream);
+
+/* Clipped gradients of every layer into layers[l].G. */
+size_t bk_weighted_grads_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
+                                        int64_t B);
+bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, bk_dtype dt,
+                            int64_t B, void* ws, size_t ws_bytes, void* stream);
+
+/* The whole path of Algorithm 1 from the per-layer norms to the noise, with
+ * the layerwise norm choice of Algorithm "BKAL-mixed" (BK-MixGhostClip):
+ * bk_layer_norms -> bk_clip_factors -> bk_weighted_grads -> bk_add_noise on
+ * every layers[l].G with tensor_id = l.  norm_sq [n,B], C [B] out, total_sq [B]
+ * out (may be NULL).  noise_std = sigma R; 0 skips the noise. */
+size_t bk_private_grad_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
+                                      int64_t B);
+bk_status bk_private_grad(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
+                          bk_clip mode, float R, float gamma, float noise_std, uint64_t seed,
+                          uint32_t step, float* norm_sq, float* C, float* total_sq, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/* Diagnostics. */
+const char* bk_status_string(bk_status s);
+const char* bk_last_error(void);
+const char* bk_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BK_H */

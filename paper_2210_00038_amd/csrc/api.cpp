@@ -1,0 +1,655 @@
+// Host side of the C ABI declared in include/bk.h: argument validation (before
+// any HIP call), the layerwise path choice of Section 3.2, workspace layout and
+// the grouping of layers into launches.
+#include "bk.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "bk_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+bk_status fail(bk_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+bk_status hip_fail(hipError_t e, const char* what) {
+    g_err = std::string(what) + ": " + hipGetErrorString(e);
+    return BK_ERR_LAUNCH;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool mul3_ok(int64_t a, int64_t b, int64_t c) {
+    int64_t ab, abc;
+    return !__builtin_mul_overflow(a, b, &ab) && !__builtin_mul_overflow(ab, c, &abc);
+}
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+size_t elem_bytes(bk_dtype dt) { return dt == BK_BF16 ? 2 : 4; }
+
+enum class Path { Ghost, Inst, Embed };
+
+// Everything the kernels index with 32-bit integers stays below 2^31.
+bk_status check_dims(const char* fn, int64_t B, int64_t T, int64_t d, int64_t p) {
+    if (B < 0 || T < 0 || d < 0 || p < 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: negative size (B=%lld T=%lld d=%lld p=%lld)", fn,
+                    (long long)B, (long long)T, (long long)d, (long long)p);
+    if (!mul3_ok(B, T, d) || !mul3_ok(B, T, p) || !mul3_ok(d, p, 1))
+        return fail(BK_ERR_INVALID_VALUE, "%s: size product overflows int64", fn);
+    if (B * T > INT32_MAX || d > INT32_MAX || p > INT32_MAX || T > INT32_MAX)
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: B*T, d and p must each stay below 2^31", fn);
+    return BK_OK;
+}
+
+bk_status check_dtype(const char* fn, bk_dtype dt) {
+    if (dt != BK_F32 && dt != BK_BF16)
+        return fail(BK_ERR_INVALID_VALUE, "%s: unknown dtype %d", fn, (int)dt);
+    return BK_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------------------
+// Per-layer plans
+// ---------------------------------------------------------------------------
+struct NormPlan {
+    Path path;
+    int64_t nwg;        // workgroups of the norm kernel
+    int64_t npart;      // partials per sample
+    bool vec;           // 16-byte vector loads allowed
+};
+
+NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
+    NormPlan np{};
+    const size_t es = elem_bytes(dt);
+    if (L.kind == BK_EMBEDDING) {
+        np.path = Path::Embed;
+    } else {
+        np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
+    }
+    if (np.path == Path::Inst) {
+        np.npart = cdiv(L.d, bk::kTile) * cdiv(L.p, bk::kTile);
+        np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
+    } else {
+        const int64_t nsb = cdiv(L.T, bk::kSuper);
+        np.npart = nsb * (nsb + 1) / 2;
+        const bool xv = np.path == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
+        np.vec = xv && aligned16(L.g) && (L.p * es) % 16 == 0;
+    }
+    np.nwg = B * np.npart;
+    return np;
+}
+
+size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
+    return align_up((size_t)(B * np.npart) * sizeof(float));
+}
+
+size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t V) {
+    return align_up((size_t)(B * T) * sizeof(uint64_t)) + align_up((size_t)V * sizeof(int32_t));
+}
+
+bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, bool need_G) {
+    if (L.kind != BK_LINEAR && L.kind != BK_EMBEDDING)
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld has unknown kind %d", fn, (long long)l, L.kind);
+    if (L.reserved != 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: reserved field must be 0", fn, (long long)l);
+    bk_status s = check_dims(fn, B, L.T, L.d, L.p);
+    if (s != BK_OK) return s;
+    const bool has_tokens = B > 0 && L.T > 0;
+    if (has_tokens && (!L.x || (!L.g && L.p > 0)))
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: NULL input pointer", fn, (long long)l);
+    if (need_G && !L.G && L.d * L.p > 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: NULL gradient output", fn, (long long)l);
+    if (L.kind == BK_EMBEDDING && need_G && B * L.T > 8192)
+        return fail(BK_ERR_NOT_SUPPORTED,
+                    "%s: layer %lld: embedding gradient supports at most 8192 tokens per call (B*T=%lld)",
+                    fn, (long long)l, (long long)(B * L.T));
+    return BK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Grouped execution
+// ---------------------------------------------------------------------------
+size_t layer_norms_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    size_t tot = 0;
+    for (int64_t l = 0; l < n; ++l) tot += norm_ws_bytes(norm_plan(layers[l], dt, B), B);
+    return tot;
+}
+
+bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
+                      float* norm_sq, void* ws, size_t ws_bytes, hipStream_t s) {
+    if (n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative layer count", fn);
+    if (n > 0 && !layers) return fail(BK_ERR_INVALID_VALUE, "%s: NULL layer array", fn);
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if (B < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative batch", fn);
+    for (int64_t l = 0; l < n; ++l)
+        if ((st = check_layer(fn, layers[l], l, B, false)) != BK_OK) return st;
+    if (n * B > 0 && !norm_sq) return fail(BK_ERR_INVALID_VALUE, "%s: NULL norm output", fn);
+    const size_t need = layer_norms_ws(layers, n, dt, B);
+    if (ws_bytes < need || (need > 0 && !ws))
+        return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    if ((size_t)need / sizeof(float) > (size_t)INT32_MAX)
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: too many partial sums", fn);
+    if (n == 0 || B == 0) return BK_OK;
+
+    float* part = static_cast<float*>(ws);
+    const bool bf16 = dt == BK_BF16;
+
+    // Batches of same-kernel layers; each batch is one launch.
+    struct Item { int64_t l; NormPlan np; int64_t part_off; };
+    std::vector<Item> items;
+    items.reserve((size_t)n);
+    int64_t off = 0;
+    for (int64_t l = 0; l < n; ++l) {
+        const NormPlan np = norm_plan(layers[l], dt, B);
+        items.push_back({l, np, off});
+        off += (int64_t)(norm_ws_bytes(np, B) / sizeof(float));
+    }
+
+    auto flush_ghost = [&](std::vector<const Item*>& v, bool embed, bool vec) -> bk_status {
+        if (v.empty()) return BK_OK;
+        bk::GhostArgs a{};
+        a.n = (int32_t)v.size();
+        a.B = (int32_t)B;
+        a.part = part;
+        int64_t wg = 0;
+        for (size_t k = 0; k < v.size(); ++k) {
+            const bk_layer& L = layers[v[k]->l];
+            bk::GhostLayer& g = a.L[k];
+            g.x = L.x;
+            g.g = L.g;
+            g.T = (int32_t)L.T;
+            g.d = (int32_t)L.d;
+            g.p = (int32_t)L.p;
+            g.nsb = (int32_t)cdiv(L.T, bk::kSuper);
+            g.npairs = (int32_t)v[k]->np.npart;
+            g.wg_begin = (int32_t)wg;
+            g.part_off = (int32_t)v[k]->part_off;
+            wg += v[k]->np.nwg;
+        }
+        if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        hipError_t e = bk::launch_ghost(a, (int)wg, bf16, embed, vec, s);
+        v.clear();
+        return e == hipSuccess ? BK_OK : hip_fail(e, "ghost norm launch");
+    };
+    auto flush_inst = [&](std::vector<const Item*>& v, bool vec) -> bk_status {
+        if (v.empty()) return BK_OK;
+        bk::GemmArgs a{};
+        a.n = (int32_t)v.size();
+        a.B = (int32_t)B;
+        a.C = nullptr;
+        a.part = part;
+        int64_t wg = 0;
+        for (size_t k = 0; k < v.size(); ++k) {
+            const bk_layer& L = layers[v[k]->l];
+            bk::GemmLayer& g = a.L[k];
+            g.a = L.x;
+            g.g = L.g;
+            g.G = nullptr;
+            g.T = (int32_t)L.T;
+            g.d = (int32_t)L.d;
+            g.p = (int32_t)L.p;
+            g.tm = (int32_t)cdiv(L.d, bk::kTile);
+            g.tn = (int32_t)cdiv(L.p, bk::kTile);
+            g.wg_begin = (int32_t)wg;
+            g.part_off = (int32_t)v[k]->part_off;
+            wg += v[k]->np.nwg;
+        }
+        if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        hipError_t e = bk::launch_gemm(a, (int)wg, bf16, true, vec, s);
+        v.clear();
+        return e == hipSuccess ? BK_OK : hip_fail(e, "instantiated norm launch");
+    };
+
+    // Group by (path, vec), preserving layer order inside a group.
+    for (int kind = 0; kind < 3; ++kind)
+        for (int vec = 0; vec < 2; ++vec) {
+            std::vector<const Item*> batch;
+            for (const Item& it : items) {
+                const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
+                if (it.np.path != want || it.np.vec != (vec == 1) || it.np.nwg == 0) continue;
+                batch.push_back(&it);
+                const size_t cap = kind == 2 ? bk::kMaxGemm : bk::kMaxGhost;
+                if (batch.size() == cap) {
+                    st = kind == 2 ? flush_inst(batch, vec) : flush_ghost(batch, kind == 1, vec);
+                    if (st != BK_OK) return st;
+                }
+            }
+            st = kind == 2 ? flush_inst(batch, vec) : flush_ghost(batch, kind == 1, vec);
+            if (st != BK_OK) return st;
+        }
+
+    // Finish every layer's norms with the fixed-order reduction.
+    for (int64_t l0 = 0; l0 < n; l0 += bk::kMaxReduce) {
+        const int64_t cnt = std::min<int64_t>(bk::kMaxReduce, n - l0);
+        bk::ReduceArgs r{};
+        r.n = (int32_t)cnt;
+        r.B = (int32_t)B;
+        r.part = part;
+        for (int64_t k = 0; k < cnt; ++k) {
+            const Item& it = items[(size_t)(l0 + k)];
+            r.L[k].out = norm_sq + (l0 + k) * B;
+            r.L[k].part_off = (int32_t)it.part_off;
+            r.L[k].npart = (int32_t)it.np.npart;
+        }
+        hipError_t e = bk::launch_reduce(r, (int)(cnt * B), s);
+        if (e != hipSuccess) return hip_fail(e, "norm reduction launch");
+    }
+    return BK_OK;
+}
+
+size_t weighted_grads_ws(const bk_layer* layers, int64_t n, int64_t B) {
+    size_t tot = 0;
+    for (int64_t l = 0; l < n; ++l)
+        if (layers[l].kind == BK_EMBEDDING)
+            tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T, layers[l].d));
+    return tot;
+}
+
+bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, const float* C,
+                         bk_dtype dt, int64_t B, void* ws, size_t ws_bytes, hipStream_t s) {
+    if (n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative layer count", fn);
+    if (n > 0 && !layers) return fail(BK_ERR_INVALID_VALUE, "%s: NULL layer array", fn);
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if (B < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative batch", fn);
+    for (int64_t l = 0; l < n; ++l)
+        if ((st = check_layer(fn, layers[l], l, B, true)) != BK_OK) return st;
+    if (B > 0 && !C) return fail(BK_ERR_INVALID_VALUE, "%s: NULL clip factors", fn);
+    const size_t need = weighted_grads_ws(layers, n, B);
+    if (ws_bytes < need || (need > 0 && !ws))
+        return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    const bool bf16 = dt == BK_BF16;
+    const size_t es = elem_bytes(dt);
+
+    for (int vec = 0; vec < 2; ++vec) {
+        bk::GemmArgs a{};
+        a.B = (int32_t)B;
+        a.C = C;
+        a.part = nullptr;
+        int64_t wg = 0;
+        auto flush = [&]() -> bk_status {
+            if (a.n == 0) return BK_OK;
+            if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+            hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, vec == 1, s);
+            a.n = 0;
+            wg = 0;
+            return e == hipSuccess ? BK_OK : hip_fail(e, "clipped gradient launch");
+        };
+        for (int64_t l = 0; l < n; ++l) {
+            const bk_layer& L = layers[l];
+            if (L.kind != BK_LINEAR || L.d * L.p == 0) continue;
+            const bool v = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 &&
+                           (L.p * es) % 16 == 0;
+            if (v != (vec == 1)) continue;
+            bk::GemmLayer& g = a.L[a.n++];
+            g.a = L.x;
+            g.g = L.g;
+            g.G = L.G;
+            // With no tokens (B*T == 0) the tiles still run, writing zeros.
+            g.T = (int32_t)L.T;
+            g.d = (int32_t)L.d;
+            g.p = (int32_t)L.p;
+            g.tm = (int32_t)cdiv(L.d, bk::kTile);
+            g.tn = (int32_t)cdiv(L.p, bk::kTile);
+            g.wg_begin = (int32_t)wg;
+            g.part_off = 0;
+            wg += (int64_t)g.tm * g.tn;
+            if (a.n == bk::kMaxGemm && (st = flush()) != BK_OK) return st;
+        }
+        if ((st = flush()) != BK_OK) return st;
+    }
+    for (int64_t l = 0; l < n; ++l) {
+        const bk_layer& L = layers[l];
+        if (L.kind != BK_EMBEDDING || L.d * L.p == 0) continue;
+        char* w = static_cast<char*>(ws);
+        uint64_t* keys = reinterpret_cast<uint64_t*>(w);
+        int32_t* first = reinterpret_cast<int32_t*>(w + align_up((size_t)(B * L.T) * sizeof(uint64_t)));
+        hipError_t e = bk::launch_embed_grad(static_cast<const int64_t*>(L.x), L.g, C, bf16, B, L.T,
+                                             L.p, L.d, L.G, keys, first, s);
+        if (e != hipSuccess) return hip_fail(e, "embedding gradient launch");
+    }
+    return BK_OK;
+}
+
+bk_status add_noise_layers(const char* fn, float* const* G, const int64_t* nel,
+                           const uint32_t* tensor_id, int64_t n, float std, uint64_t seed,
+                           uint32_t step, hipStream_t s) {
+    bk::NoiseArgs a{};
+    a.std = std;
+    a.seed = seed;
+    a.step = step;
+    int64_t wg = 0;
+    auto flush = [&]() -> bk_status {
+        if (a.n == 0) return BK_OK;
+        if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        hipError_t e = bk::launch_noise(a, (int)wg, s);
+        a.n = 0;
+        wg = 0;
+        return e == hipSuccess ? BK_OK : hip_fail(e, "noise launch");
+    };
+    for (int64_t l = 0; l < n; ++l) {
+        if (nel[l] == 0) continue;
+        bk::NoiseLayer& L = a.L[a.n++];
+        L.G = G[l];
+        L.n = nel[l];
+        L.tensor_id = tensor_id[l];
+        L.wg_begin = (uint32_t)wg;
+        wg += cdiv(cdiv(nel[l], 4), bk::kNoiseBlocksPerWG);
+        if (a.n == bk::kMaxNoise) {
+            bk_status st = flush();
+            if (st != BK_OK) return st;
+        }
+    }
+    return flush();
+}
+
+bk_layer linear_layer(const void* a, const void* g, int64_t T, int64_t d, int64_t p, float* G) {
+    bk_layer L{};
+    L.kind = BK_LINEAR;
+    L.T = T;
+    L.d = d;
+    L.p = p;
+    L.x = a;
+    L.g = g;
+    L.G = G;
+    return L;
+}
+
+bk_layer embed_layer(const int64_t* ids, const void* g, int64_t T, int64_t V, int64_t p, float* G) {
+    bk_layer L{};
+    L.kind = BK_EMBEDDING;
+    L.T = T;
+    L.d = V;
+    L.p = p;
+    L.x = ids;
+    L.g = g;
+    L.G = G;
+    return L;
+}
+
+// Single-layer norm with a forced path (the grouped call picks it by rule).
+bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt, int64_t B,
+                      float* norm_sq, void* ws, size_t ws_bytes, hipStream_t s) {
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if ((st = check_layer(fn, L, 0, B, false)) != BK_OK) return st;
+    if (B > 0 && !norm_sq) return fail(BK_ERR_INVALID_VALUE, "%s: NULL norm output", fn);
+    NormPlan np = norm_plan(L, dt, B);
+    np.path = want;
+    if (want == Path::Inst) {
+        np.npart = cdiv(L.d, bk::kTile) * cdiv(L.p, bk::kTile);
+        const size_t es = elem_bytes(dt);
+        np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
+    } else {
+        const int64_t nsb = cdiv(L.T, bk::kSuper);
+        np.npart = nsb * (nsb + 1) / 2;
+        const size_t es = elem_bytes(dt);
+        const bool xv = want == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
+        np.vec = xv && aligned16(L.g) && (L.p * es) % 16 == 0;
+    }
+    np.nwg = B * np.npart;
+    const size_t need = norm_ws_bytes(np, B);
+    if (ws_bytes < need || (need > 0 && !ws))
+        return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    if (B == 0) return BK_OK;
+    float* part = static_cast<float*>(ws);
+    hipError_t e = hipSuccess;
+    if (np.nwg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+    if (want == Path::Inst) {
+        bk::GemmArgs a{};
+        a.n = 1;
+        a.B = (int32_t)B;
+        a.part = part;
+        bk::GemmLayer& g = a.L[0];
+        g.a = L.x;
+        g.g = L.g;
+        g.T = (int32_t)L.T;
+        g.d = (int32_t)L.d;
+        g.p = (int32_t)L.p;
+        g.tm = (int32_t)cdiv(L.d, bk::kTile);
+        g.tn = (int32_t)cdiv(L.p, bk::kTile);
+        e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, np.vec, s);
+    } else {
+        bk::GhostArgs a{};
+        a.n = 1;
+        a.B = (int32_t)B;
+        a.part = part;
+        bk::GhostLayer& g = a.L[0];
+        g.x = L.x;
+        g.g = L.g;
+        g.T = (int32_t)L.T;
+        g.d = (int32_t)L.d;
+        g.p = (int32_t)L.p;
+        g.nsb = (int32_t)cdiv(L.T, bk::kSuper);
+        g.npairs = (int32_t)np.npart;
+        e = bk::launch_ghost(a, (int)np.nwg, dt == BK_BF16, want == Path::Embed, np.vec, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "norm launch");
+    bk::ReduceArgs r{};
+    r.n = 1;
+    r.B = (int32_t)B;
+    r.part = part;
+    r.L[0].out = norm_sq;
+    r.L[0].part_off = 0;
+    r.L[0].npart = (int32_t)np.npart;
+    e = bk::launch_reduce(r, (int)B, s);
+    return e == hipSuccess ? BK_OK : hip_fail(e, "norm reduction launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+int bk_use_ghost(int64_t T, int64_t d, int64_t p) {
+    if (T < 0 || d < 0 || p < 0) return -1;
+    // 2 T^2 < p d, evaluated without overflow (128-bit products).
+    const __int128 lhs = (__int128)2 * T * T;
+    const __int128 rhs = (__int128)p * d;
+    return lhs < rhs ? 1 : 0;
+}
+
+size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d, int64_t p) {
+    if (check_dtype("bk_workspace_size", dt) != BK_OK) return 0;
+    if (check_dims("bk_workspace_size", B, T, d, p) != BK_OK) return 0;
+    bk_layer L{};
+    L.T = T;
+    L.d = d;
+    L.p = p;
+    switch (op) {
+        case BK_OP_GHOST_NORM:
+        case BK_OP_EMBED_GHOST_NORM: {
+            const int64_t nsb = cdiv(T, bk::kSuper);
+            return align_up((size_t)(B * (nsb * (nsb + 1) / 2)) * sizeof(float));
+        }
+        case BK_OP_INST_NORM:
+            return align_up((size_t)(B * cdiv(d, bk::kTile) * cdiv(p, bk::kTile)) * sizeof(float));
+        case BK_OP_WEIGHTED_GRAD:
+            return 0;
+        case BK_OP_EMBED_WEIGHTED_GRAD:
+            return embed_grad_ws_bytes(B, T, d);
+        default:
+            return 0;
+    }
+}
+
+bk_status bk_ghost_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T, int64_t d,
+                        int64_t p, float* norm_sq, void* ws, size_t ws_bytes, void* stream) {
+    return single_norm("bk_ghost_norm", Path::Ghost, linear_layer(a, g, T, d, p, nullptr), dt, B,
+                       norm_sq, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_inst_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T, int64_t d,
+                       int64_t p, float* norm_sq, void* ws, size_t ws_bytes, void* stream) {
+    return single_norm("bk_inst_norm", Path::Inst, linear_layer(a, g, T, d, p, nullptr), dt, B,
+                       norm_sq, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B, int64_t T,
+                              int64_t p, int64_t V, float* norm_sq, void* ws, size_t ws_bytes,
+                              void* stream) {
+    return single_norm("bk_embed_ghost_norm", Path::Embed, embed_layer(ids, g, T, V, p, nullptr), dt,
+                       B, norm_sq, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_clip_factors(const float* norm_sq, int64_t L, int64_t B, bk_clip mode, float R,
+                          float gamma, float* C, float* total_sq, void* stream) {
+    const char* fn = "bk_clip_factors";
+    if (L < 0 || B < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (mode != BK_CLIP_ABADI && mode != BK_CLIP_AUTO)
+        return fail(BK_ERR_INVALID_VALUE, "%s: unknown clip mode %d", fn, (int)mode);
+    if (mode == BK_CLIP_ABADI && !(R > 0.f))
+        return fail(BK_ERR_INVALID_VALUE, "%s: Abadi clipping needs R > 0", fn);
+    if (mode == BK_CLIP_AUTO && !(gamma >= 0.f))
+        return fail(BK_ERR_INVALID_VALUE, "%s: automatic clipping needs gamma >= 0", fn);
+    if (!mul3_ok(L, B, 1)) return fail(BK_ERR_INVALID_VALUE, "%s: L*B overflows", fn);
+    if (B > 0 && (!C || (L > 0 && !norm_sq)))
+        return fail(BK_ERR_INVALID_VALUE, "%s: NULL pointer", fn);
+    hipError_t e = bk::launch_clip(norm_sq, L, B, (int)mode, R, gamma, C, total_sq,
+                                   static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "clip launch");
+}
+
+bk_status bk_weighted_grad(const void* a, const void* g, const float* C, bk_dtype dt, int64_t B,
+                           int64_t T, int64_t d, int64_t p, float* G, void* ws, size_t ws_bytes,
+                           void* stream) {
+    const bk_layer L = linear_layer(a, g, T, d, p, G);
+    return weighted_grads("bk_weighted_grad", &L, 1, C, dt, B, ws, ws_bytes,
+                          static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_embed_weighted_grad(const int64_t* ids, const void* g, const float* C, bk_dtype dt,
+                                 int64_t B, int64_t T, int64_t p, int64_t V, float* G, void* ws,
+                                 size_t ws_bytes, void* stream) {
+    const bk_layer L = embed_layer(ids, g, T, V, p, G);
+    return weighted_grads("bk_embed_weighted_grad", &L, 1, C, dt, B, ws, ws_bytes,
+                          static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_add_noise(float* G, int64_t n, float std, uint64_t seed, uint32_t tensor_id,
+                       uint32_t step, void* stream) {
+    const char* fn = "bk_add_noise";
+    if (n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (n > 0 && !G) return fail(BK_ERR_INVALID_VALUE, "%s: NULL tensor", fn);
+    if (!(std >= 0.f) || std == INFINITY) return fail(BK_ERR_INVALID_VALUE, "%s: std must be finite and >= 0", fn);
+    if (n == 0 || std == 0.f) return BK_OK;
+    return add_noise_layers(fn, &G, &n, &tensor_id, 1, std, seed, step, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64_t q0, int64_t nq,
+                        uint32_t* out, void* stream) {
+    const char* fn = "bk_philox_raw";
+    if (nq < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative count", fn);
+    if (nq > 0 && !out) return fail(BK_ERR_INVALID_VALUE, "%s: NULL output", fn);
+    if (nq > ((int64_t)1 << 40)) return fail(BK_ERR_NOT_SUPPORTED, "%s: count too large", fn);
+    hipError_t e = bk::launch_philox_raw(seed, tensor_id, step, q0, nq, out, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "philox launch");
+}
+
+size_t bk_layer_norms_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    if (n < 0 || (n > 0 && !layers) || B < 0 || check_dtype("", dt) != BK_OK) return 0;
+    for (int64_t l = 0; l < n; ++l)
+        if (check_dims("", B, layers[l].T, layers[l].d, layers[l].p) != BK_OK) return 0;
+    return layer_norms_ws(layers, n, dt, B);
+}
+
+bk_status bk_layer_norms(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B, float* norm_sq,
+                         void* ws, size_t ws_bytes, void* stream) {
+    return layer_norms("bk_layer_norms", layers, n, dt, B, norm_sq, ws, ws_bytes,
+                       static_cast<hipStream_t>(stream));
+}
+
+size_t bk_weighted_grads_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    if (n < 0 || (n > 0 && !layers) || B < 0 || check_dtype("", dt) != BK_OK) return 0;
+    for (int64_t l = 0; l < n; ++l)
+        if (check_dims("", B, layers[l].T, layers[l].d, layers[l].p) != BK_OK) return 0;
+    return weighted_grads_ws(layers, n, B);
+}
+
+bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, bk_dtype dt,
+                            int64_t B, void* ws, size_t ws_bytes, void* stream) {
+    return weighted_grads("bk_weighted_grads", layers, n, C, dt, B, ws, ws_bytes,
+                          static_cast<hipStream_t>(stream));
+}
+
+size_t bk_private_grad_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    return std::max(bk_layer_norms_workspace_size(layers, n, dt, B),
+                    bk_weighted_grads_workspace_size(layers, n, dt, B));
+}
+
+bk_status bk_private_grad(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B, bk_clip mode,
+                          float R, float gamma, float noise_std, uint64_t seed, uint32_t step,
+                          float* norm_sq, float* C, float* total_sq, void* ws, size_t ws_bytes,
+                          void* stream) {
+    const char* fn = "bk_private_grad";
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!(noise_std >= 0.f) || noise_std == INFINITY)
+        return fail(BK_ERR_INVALID_VALUE, "%s: noise_std must be finite and >= 0", fn);
+    if (mode != BK_CLIP_ABADI && mode != BK_CLIP_AUTO)
+        return fail(BK_ERR_INVALID_VALUE, "%s: unknown clip mode %d", fn, (int)mode);
+    if (mode == BK_CLIP_ABADI && !(R > 0.f))
+        return fail(BK_ERR_INVALID_VALUE, "%s: Abadi clipping needs R > 0", fn);
+    if (mode == BK_CLIP_AUTO && !(gamma >= 0.f))
+        return fail(BK_ERR_INVALID_VALUE, "%s: automatic clipping needs gamma >= 0", fn);
+    if (n < 0 || (n > 0 && !layers)) return fail(BK_ERR_INVALID_VALUE, "%s: bad layer array", fn);
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    for (int64_t l = 0; l < n; ++l)
+        if ((st = check_layer(fn, layers[l], l, B, true)) != BK_OK) return st;
+    if (B > 0 && !C) return fail(BK_ERR_INVALID_VALUE, "%s: NULL clip factor output", fn);
+    if (n > UINT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many layers", fn);
+    const size_t need = bk_private_grad_workspace_size(layers, n, dt, B);
+    if (ws_bytes < need || (need > 0 && !ws))
+        return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+
+    if ((st = layer_norms(fn, layers, n, dt, B, norm_sq, ws, ws_bytes, s)) != BK_OK) return st;
+    hipError_t e = bk::launch_clip(norm_sq, n, B, (int)mode, R, gamma, C, total_sq, s);
+    if (e != hipSuccess) return hip_fail(e, "clip launch");
+    if ((st = weighted_grads(fn, layers, n, C, dt, B, ws, ws_bytes, s)) != BK_OK) return st;
+    if (noise_std == 0.f) return BK_OK;
+    std::vector<float*> G((size_t)n);
+    std::vector<int64_t> nel((size_t)n);
+    std::vector<uint32_t> tid((size_t)n);
+    for (int64_t l = 0; l < n; ++l) {
+        G[(size_t)l] = layers[l].G;
+        nel[(size_t)l] = layers[l].d * layers[l].p;
+        tid[(size_t)l] = (uint32_t)l;
+    }
+    return add_noise_layers(fn, G.data(), nel.data(), tid.data(), n, noise_std, seed, step, s);
+}
+
+const char* bk_status_string(bk_status s) {
+    switch (s) {
+        case BK_OK: return "BK_OK";
+        case BK_ERR_INVALID_VALUE: return "BK_ERR_INVALID_VALUE";
+        case BK_ERR_NOT_SUPPORTED: return "BK_ERR_NOT_SUPPORTED";
+        case BK_ERR_WORKSPACE: return "BK_ERR_WORKSPACE";
+        case BK_ERR_LAUNCH: return "BK_ERR_LAUNCH";
+        default: return "BK_ERR_UNKNOWN";
+    }
+}
+
+const char* bk_last_error(void) { return g_err.c_str(); }
+
+const char* bk_version(void) { return "bk 0.1 (gfx950)"; }
+
+}  // extern "C"

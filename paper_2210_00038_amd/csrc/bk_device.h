@@ -1,0 +1,139 @@
+// Device-side building blocks shared by the BK kernels (gfx950 / CDNA4 only).
+//
+//  * 16-byte operand fragments and the 32x32 MFMA step that consumes them;
+//  * bf16 <-> fp32 conversion (round to nearest even);
+//  * Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+//    easy as 1, 2, 3", SC'11) and the Box-Muller transform;
+//  * wave / workgroup reductions with a fixed summation order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bk {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+
+// Storage type of a bf16 element.
+struct bf16_t { uint16_t bits; };
+
+template <typename T> struct Elem;
+template <> struct Elem<float> { static constexpr int per16 = 4; static constexpr int bytes = 4; };
+template <> struct Elem<bf16_t> { static constexpr int per16 = 8; static constexpr int bytes = 2; };
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Round-to-nearest-even fp32 -> bf16 (inputs here are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// ---------------------------------------------------------------------------
+// One 32x32 output tile step: acc += A_frag * B_frag^T over the k values that
+// a 16-byte fragment per lane carries.
+//
+// Fragment layout (both operands): lane l holds row (l % 32) of its 32-row
+// block and the 16 bytes of that row at k-offset (l / 32) * 16 bytes within
+// the current 32-byte k slab.  bf16: one v_mfma_f32_32x32x16_bf16 (8 k values
+// per lane, 16 per step).  fp32: four v_mfma_f32_32x32x2_f32, element e of
+// every lane's 4 floats forming the e-th step.  Because A and B use the same
+// lane -> k assignment, the assignment of k values to MFMA slots is irrelevant
+// to the result (a sum over k), which lets rows be read in contiguous 16-byte
+// pieces.
+// ---------------------------------------------------------------------------
+template <typename T> struct Mfma;
+
+template <> struct Mfma<bf16_t> {
+    static __device__ __forceinline__ void step(f32x16_t& acc, const uint4& a, const uint4& b) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), acc,
+                                                       0, 0, 0);
+    }
+};
+
+template <> struct Mfma<float> {
+    static __device__ __forceinline__ void step(f32x16_t& acc, const uint4& a, const uint4& b) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    }
+};
+
+// Row (within the 32x32 tile) of accumulator element i of lane `lane`; the
+// column is lane % 32.  (Output layout of the 32x32 MFMA family.)
+__device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
+
+// ---------------------------------------------------------------------------
+// Reductions in a fixed order (deterministic).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Sum of one float per thread over a 256-thread workgroup; result valid in
+// thread 0.  `red` must hold 4 floats of LDS.
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float s = 0.f;
+    if (threadIdx.x == 0) s = (red[0] + red[1]) + (red[2] + red[3]);
+    return s;
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (SC'11): two 32x32->64 multiplications per round, key bumped
+// by the Weyl constants between rounds.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t hi0 = __umulhi(kPhiloxM0, c.x), lo0 = kPhiloxM0 * c.x;
+        const uint32_t hi1 = __umulhi(kPhiloxM1, c.z), lo1 = kPhiloxM1 * c.z;
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+        k0 += kPhiloxW0;
+        k1 += kPhiloxW1;
+    }
+    return c;
+}
+
+// Counter block q of tensor `tid` at step `step` under `seed`.
+__device__ __forceinline__ uint4 philox_block(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q) {
+    return philox4x32_10(make_uint4((uint32_t)q, (uint32_t)(q >> 32), tid, step), (uint32_t)seed,
+                         (uint32_t)(seed >> 32));
+}
+
+// u = (2 (w >> 9) + 1) 2^-24: an odd multiple of 2^-24, exact in fp32, in (0, 1).
+__device__ __forceinline__ float word_to_uniform(uint32_t w) {
+    return (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-08f;
+}
+
+// Box-Muller: (r cos 2 pi u1, r sin 2 pi u1), r = sqrt(-2 ln u0).
+__device__ __forceinline__ float2 box_muller(uint32_t w0, uint32_t w1) {
+    const float u0 = word_to_uniform(w0), u1 = word_to_uniform(w1);
+    const float r = sqrtf(-2.0f * logf(u0));
+    float s, c;
+    sincospif(2.0f * u1, &s, &c);
+    return make_float2(r * c, r * s);
+}
+
+// The four standard normals of counter block q.
+__device__ __forceinline__ float4 normal4(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q) {
+    const uint4 w = philox_block(seed, tid, step, q);
+    const float2 z01 = box_muller(w.x, w.y), z23 = box_muller(w.z, w.w);
+    return make_float4(z01.x, z01.y, z23.x, z23.y);
+}
+
+}  // namespace bk

@@ -1,0 +1,100 @@
+// Kernel-argument descriptors and launchers of the BK kernels (internal to
+// libbk; the public interface is include/bk.h).
+//
+// Grouped launches: the descriptors of up to kMax* layers travel in the kernel
+// arguments themselves (no device-side table to upload), so one launch covers
+// a whole stack and the call needs no workspace for bookkeeping.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bk {
+
+constexpr int kSuper = 128;   // ghost norm: rows of a super block of the T x T Gram
+constexpr int kTile = 128;    // a^T g GEMMs: output tile is kTile x kTile
+
+// ---- ghost norm (linear and embedding) ----------------------------------
+struct GhostLayer {
+    const void* x;      // a [B,T,d] (linear) or ids int64 [B,T] (embedding)
+    const void* g;      // [B,T,p]
+    int32_t T, d, p;    // d unused for the embedding
+    int32_t nsb;        // super blocks: ceil(T / kSuper)
+    int32_t npairs;     // nsb (nsb + 1) / 2 upper-triangle super-block pairs
+    int32_t wg_begin;   // first workgroup of this layer in the launch
+    int32_t part_off;   // first partial (float) of this layer in the workspace
+    int32_t pad;
+};
+constexpr int kMaxGhost = 64;
+struct GhostArgs {
+    int32_t n, B;
+    float* part;        // partial sums, [layer][sample][pair]
+    GhostLayer L[kMaxGhost];
+};
+
+// ---- a^T diag(w) g GEMMs: instantiated norms and clipped gradients -------
+struct GemmLayer {
+    const void* a;      // [B,T,d]
+    const void* g;      // [B,T,p]
+    float* G;           // [d,p] out (clipped gradient)
+    int32_t T, d, p;
+    int32_t tm, tn;     // output tiles along d and p
+    int32_t wg_begin;
+    int32_t part_off;   // instantiated norm: first partial of this layer
+    int32_t pad;
+};
+constexpr int kMaxGemm = 56;
+struct GemmArgs {
+    int32_t n, B;
+    const float* C;     // [B] clip factors (clipped gradient)
+    float* part;        // partial sums (instantiated norm), [layer][sample][tile]
+    GemmLayer L[kMaxGemm];
+};
+
+// ---- fixed-order reduction of partial sums ---------------------------------
+struct ReduceLayer {
+    float* out;         // [B]
+    int32_t part_off;
+    int32_t npart;      // partials per sample
+};
+constexpr int kMaxReduce = 200;
+struct ReduceArgs {
+    int32_t n, B;
+    const float* part;
+    ReduceLayer L[kMaxReduce];
+};
+
+// ---- noise ------------------------------------------------------------------
+struct NoiseLayer {
+    float* G;
+    int64_t n;          // elements
+    uint32_t tensor_id;
+    uint32_t wg_begin;
+};
+constexpr int kMaxNoise = 150;
+struct NoiseArgs {
+    int32_t n;
+    float std;
+    uint64_t seed;
+    uint32_t step;
+    uint32_t pad;
+    NoiseLayer L[kMaxNoise];
+};
+constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by one workgroup
+
+// ---- launchers (return the launch status) ----------------------------------
+hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
+                        hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, bool vec,
+                       hipStream_t s);
+hipError_t launch_reduce(const ReduceArgs& args, int n_threads, hipStream_t s);
+hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, float R, float gamma,
+                       float* C, float* total_sq, hipStream_t s);
+hipError_t launch_noise(const NoiseArgs& args, int n_wg, hipStream_t s);
+hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q0, int64_t nq,
+                             uint32_t* out, hipStream_t s);
+hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
+                             int64_t B, int64_t T, int64_t p, int64_t V, float* G,
+                             uint64_t* keys, int32_t* first, hipStream_t s);
+
+}  // namespace bk

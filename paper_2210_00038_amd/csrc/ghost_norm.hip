@@ -1,0 +1,219 @@
+// Ghost norm of linear and embedding layers (eq. "ghost norm", Section 2.1;
+// App. B.4):
+//
+//   n_i = vec(g_i g_i^T) . vec(a_i a_i^T) = sum_{t,t'} (a_i a_i^T)_{tt'} (g_i g_i^T)_{tt'}
+//
+// For an embedding a_i = one_hot(x_i), so (a_i a_i^T)_{tt'} = [x_it == x_it'].
+//
+// Work decomposition.  The T x T Grams of sample i are cut into 128 x 128
+// super blocks; only the upper triangle of super-block pairs (R <= C) is
+// visited and off-diagonal pairs count twice (both Grams are symmetric).  One
+// 256-thread workgroup owns one (layer, sample, R, C): it streams rows
+// [128R, 128R+128) and [128C, 128C+128) of a_i through LDS in 128-byte column
+// chunks and accumulates its part of a_i a_i^T with 32x32 MFMA tiles, then does
+// the same for g_i, and finally multiplies the two accumulators elementwise
+// and reduces.  The Grams never leave the registers.  Inside a diagonal super
+// block only the 10 upper 32x32 sub-tiles are formed (diagonal ones weight 1,
+// others 2); sub-tiles made only of padding rows (t >= T) are skipped.  Each
+// workgroup writes one partial sum; a fixed-order reduction finishes the norm.
+#include "bk_device.h"
+#include "bk_kernels.h"
+
+namespace bk {
+namespace {
+
+constexpr int kRowU4 = 9;                    // LDS row: 128 data bytes + 16 pad, in uint4
+constexpr int kBlockU4 = kSuper * kRowU4;    // one staged super block
+
+struct WaveTiles {
+    int r0, c0;   // first 32-row sub-block of the rows (block R) / columns (block C)
+    int w[4];     // weight of sub-tile (r0 + x, c0 + y) at index 2x + y; 0 = skip
+};
+
+__device__ __forceinline__ WaveTiles wave_tiles(int wave, bool diag) {
+    WaveTiles t;
+    if (!diag) {
+        t.r0 = 2 * (wave >> 1);
+        t.c0 = 2 * (wave & 1);
+        t.w[0] = t.w[1] = t.w[2] = t.w[3] = 2;
+        return t;
+    }
+    // Upper triangle of the 4 x 4 sub-tiles of a diagonal super block:
+    // wave 0: (0,0) (0,1) (1,1); wave 1: (2,2) (2,3) (3,3);
+    // wave 2: (0,2) (1,2);       wave 3: (0,3) (1,3).
+    switch (wave) {
+        case 0: t.r0 = 0; t.c0 = 0; t.w[0] = 1; t.w[1] = 2; t.w[2] = 0; t.w[3] = 1; break;
+        case 1: t.r0 = 2; t.c0 = 2; t.w[0] = 1; t.w[1] = 2; t.w[2] = 0; t.w[3] = 1; break;
+        case 2: t.r0 = 0; t.c0 = 2; t.w[0] = 2; t.w[1] = 0; t.w[2] = 2; t.w[3] = 0; break;
+        default: t.r0 = 0; t.c0 = 2; t.w[0] = 0; t.w[1] = 2; t.w[2] = 0; t.w[3] = 2; break;
+    }
+    return t;
+}
+
+// 16 bytes of row r, starting at column k, of a [rows, K] matrix; zero outside.
+template <typename T, bool VEC>
+__device__ __forceinline__ uint4 load16(const T* X, int rows, int K, int r, int k) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r >= rows) return v;
+    const T* p = X + (size_t)r * (size_t)K + k;
+    if constexpr (VEC) {
+        if (k < K) v = *reinterpret_cast<const uint4*>(p);
+    } else {
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        if constexpr (sizeof(T) == 2) {
+            const uint16_t* q = reinterpret_cast<const uint16_t*>(p);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (k + e < K) w[e >> 1] |= (uint32_t)q[e] << (16 * (e & 1));
+        } else {
+            const uint32_t* q = reinterpret_cast<const uint32_t*>(p);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (k + e < K) w[e] = q[e];
+        }
+        v = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    return v;
+}
+
+// Accumulate this wave's sub-tiles of X X^T, X = one sample's [rows, K] matrix,
+// rows of block R starting at rowR and of block C at rowC.
+template <typename T, bool VEC>
+__device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
+                                     bool diag, const WaveTiles& wt, f32x16_t acc[4],
+                                     uint4* __restrict__ lds) {
+    constexpr int EPV = Elem<T>::per16;       // elements per 16 bytes
+    constexpr int EPC = 8 * EPV;              // elements per 128-byte chunk
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[s][i] = 0.f;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int c16 = tid & 7, rq = tid >> 3;
+    const int r = lane & 31, h = lane >> 5;
+    uint4* ldsR = lds;
+    uint4* ldsC = diag ? lds : lds + kBlockU4;
+    const int nch = (K + EPC - 1) / EPC;
+
+    uint4 pr[8];
+    auto fetch = [&](int ch) {
+        const int k = ch * EPC + c16 * EPV;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pr[q] = load16<T, VEC>(X, rows, K, rowR + rq + 32 * q, k);
+            if (!diag) pr[4 + q] = load16<T, VEC>(X, rows, K, rowC + rq + 32 * q, k);
+        }
+    };
+    fetch(0);
+    for (int ch = 0; ch < nch; ++ch) {
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            ldsR[(rq + 32 * q) * kRowU4 + c16] = pr[q];
+            if (!diag) ldsC[(rq + 32 * q) * kRowU4 + c16] = pr[4 + q];
+        }
+        __syncthreads();
+        if (ch + 1 < nch) fetch(ch + 1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = 2 * j + h;
+            const uint4 x0 = ldsR[((wt.r0 + 0) * 32 + r) * kRowU4 + col];
+            const uint4 x1 = ldsR[((wt.r0 + 1) * 32 + r) * kRowU4 + col];
+            const uint4 y0 = ldsC[((wt.c0 + 0) * 32 + r) * kRowU4 + col];
+            const uint4 y1 = ldsC[((wt.c0 + 1) * 32 + r) * kRowU4 + col];
+            if (wt.w[0]) Mfma<T>::step(acc[0], x0, y0);
+            if (wt.w[1]) Mfma<T>::step(acc[1], x0, y1);
+            if (wt.w[2]) Mfma<T>::step(acc[2], x1, y0);
+            if (wt.w[3]) Mfma<T>::step(acc[3], x1, y1);
+        }
+    }
+}
+
+template <typename T, bool EMBED, bool VEC>
+__global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
+    __shared__ uint4 lds[2 * kBlockU4];
+    __shared__ int64_t sid[2 * kSuper];
+    __shared__ float red[4];
+
+    const int wg = blockIdx.x;
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const GhostLayer& L = args.L[l];
+    const int nT = L.T, d = L.d, p = L.p, nsb = L.nsb, npairs = L.npairs;
+    const int local = wg - L.wg_begin;
+    const int sample = local / npairs;
+    int pair = local - sample * npairs;
+    int R = 0;
+    while (pair >= nsb - R) { pair -= nsb - R; ++R; }
+    const int C = R + pair;
+    const bool diag = (R == C);
+    const int rowR = R * kSuper, rowC = C * kSuper;
+
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    WaveTiles wt = wave_tiles(wave, diag);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int rs = rowR + (wt.r0 + (s >> 1)) * 32, cs = rowC + (wt.c0 + (s & 1)) * 32;
+        if (rs >= nT || cs >= nT) wt.w[s] = 0;
+    }
+
+    const size_t off_g = (size_t)sample * (size_t)nT * (size_t)p;
+    f32x16_t accG[4];
+    float part = 0.f;
+    if constexpr (EMBED) {
+        const int64_t* ids = reinterpret_cast<const int64_t*>(L.x) + (size_t)sample * nT;
+        const int t = threadIdx.x;
+        const int row = (t < kSuper) ? rowR + t : rowC + (t - kSuper);
+        sid[t] = (row < nT) ? ids[row] : (int64_t)-1;
+        gram<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, lds);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (!wt.w[s]) continue;
+            const int cl = (wt.c0 + (s & 1)) * 32 + (lane & 31);
+            const int64_t idc = sid[kSuper + cl];
+            const int64_t* idr = sid + (wt.r0 + (s >> 1)) * 32;
+            float v = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v += (idr[acc_row(i, lane)] == idc) ? accG[s][i] : 0.f;
+            part += (float)wt.w[s] * v;
+        }
+        (void)d;
+    } else {
+        f32x16_t accA[4];
+        const size_t off_a = (size_t)sample * (size_t)nT * (size_t)d;
+        gram<T, VEC>(reinterpret_cast<const T*>(L.x) + off_a, nT, d, rowR, rowC, diag, wt, accA, lds);
+        gram<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, lds);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (!wt.w[s]) continue;
+            float v = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v += accA[s][i] * accG[s][i];
+            part += (float)wt.w[s] * v;
+        }
+    }
+    const float tot = block_sum_256(part, red);
+    if (threadIdx.x == 0)
+        args.part[(size_t)L.part_off + (size_t)sample * npairs + (local - sample * npairs)] = tot;
+}
+
+}  // namespace
+
+hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
+                        hipStream_t s) {
+    if (n_wg <= 0) return hipSuccess;
+    const dim3 grid(n_wg), block(256);
+#define BK_GHOST(T, E, V) hipLaunchKernelGGL((ghost_norm_kernel<T, E, V>), grid, block, 0, s, args)
+    if (bf16) {
+        if (embed) { if (vec) BK_GHOST(bf16_t, true, true); else BK_GHOST(bf16_t, true, false); }
+        else       { if (vec) BK_GHOST(bf16_t, false, true); else BK_GHOST(bf16_t, false, false); }
+    } else {
+        if (embed) { if (vec) BK_GHOST(float, true, true); else BK_GHOST(float, true, false); }
+        else       { if (vec) BK_GHOST(float, false, true); else BK_GHOST(float, false, false); }
+    }
+#undef BK_GHOST
+    return hipGetLastError();
+}
+
+}  // namespace bk

@@ -1,0 +1,143 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+symbol include/bk.h declares, and rejects bad arguments with a status code
+before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bk.h")
+
+bk = pytest.importorskip("paper_2210_00038_amd", reason="libbk.so not built")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bk_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(bk.lib, n), n
+    assert set(names) == set(bk.EXPORTS)
+
+
+def test_use_ghost_rule():
+    # Section 3.2: ghost iff 2 T^2 < p d; ties instantiate
+    assert bk.bk_use_ghost(16, 64, 64)
+    assert not bk.bk_use_ghost(1024, 768, 768)
+    assert bk.bk_use_ghost(1024, 768, 3072)
+    assert not bk.bk_use_ghost(32, 32, 64)
+    assert bk.bk_use_ghost(31, 32, 64)
+    assert bk.lib.bk_use_ghost(-1, 2, 3) == -1
+    # no overflow for huge sizes
+    assert not bk.bk_use_ghost(1 << 40, 1 << 20, 1 << 20)
+    assert bk.bk_use_ghost(1, 1 << 40, 1 << 40)
+
+
+def test_workspace_sizes():
+    ws = bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_BF16, 32, 128, 768, 768)
+    assert ws == 256 and ws >= 32 * 4           # one partial per sample, padded to 256 B
+    ws = bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_BF16, 16, 1024, 768, 3072)
+    assert ws >= 16 * 36 * 4                    # 8 super blocks -> 36 pairs
+    ws = bk.bk_workspace_size(bk.BK_OP_INST_NORM, bk.BK_BF16, 16, 1024, 768, 768)
+    assert ws >= 16 * 36 * 4                    # 6 x 6 output tiles
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 768, 768) == 0
+    assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) >= \
+        16 * 256 * 8 + 50257 * 4
+    assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, 7, 1, 1, 1, 1) == 0        # bad dtype
+    assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_F32, -1, 1, 1, 1) == 0
+
+
+FAKE = ctypes.c_void_p(0x10000)     # never dereferenced: every call below fails validation
+
+
+def _st(fn, *args):
+    return getattr(bk.lib, fn)(*args)
+
+
+def test_validation_before_any_device_call():
+    L = bk.lib
+    # NULL inputs
+    assert L.bk_ghost_norm(None, None, bk.BK_BF16, 2, 3, 4, 5, FAKE, FAKE, 1 << 20, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    assert "NULL" in bk.bk_last_error()
+    # negative sizes
+    assert L.bk_ghost_norm(FAKE, FAKE, bk.BK_BF16, -2, 3, 4, 5, FAKE, FAKE, 1 << 20, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    assert L.bk_inst_norm(FAKE, FAKE, bk.BK_BF16, 2, 3, -4, 5, FAKE, FAKE, 1 << 20, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    # int64 overflow of B*T*d
+    assert L.bk_weighted_grad(FAKE, FAKE, FAKE, bk.BK_BF16, 1 << 40, 1 << 20, 1 << 10, 4, FAKE, None, 0,
+                              None) == bk.BK_ERR_INVALID_VALUE
+    # beyond 32-bit indexing
+    assert L.bk_weighted_grad(FAKE, FAKE, FAKE, bk.BK_BF16, 1 << 20, 1 << 12, 4, 4, FAKE, None, 0,
+                              None) == bk.BK_ERR_NOT_SUPPORTED
+    # unknown dtype
+    assert L.bk_ghost_norm(FAKE, FAKE, 9, 2, 3, 4, 5, FAKE, FAKE, 1 << 20, None) == bk.BK_ERR_INVALID_VALUE
+    # workspace too small
+    need = bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_BF16, 2, 300, 4, 5)
+    assert L.bk_ghost_norm(FAKE, FAKE, bk.BK_BF16, 2, 300, 4, 5, FAKE, FAKE, need - 1, None) == \
+        bk.BK_ERR_WORKSPACE
+    assert L.bk_ghost_norm(FAKE, FAKE, bk.BK_BF16, 2, 300, 4, 5, FAKE, None, need, None) == \
+        bk.BK_ERR_WORKSPACE
+    # clip factors: Abadi needs R > 0, automatic gamma >= 0, known mode
+    assert L.bk_clip_factors(FAKE, 3, 4, bk.BK_CLIP_ABADI, 0.0, 0.0, FAKE, None, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    assert L.bk_clip_factors(FAKE, 3, 4, bk.BK_CLIP_AUTO, 1.0, -0.5, FAKE, None, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    assert L.bk_clip_factors(FAKE, 3, 4, 5, 1.0, 0.0, FAKE, None, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_clip_factors(None, 3, 4, bk.BK_CLIP_AUTO, 1.0, 0.0, FAKE, None, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    # noise: negative / non-finite std, NULL tensor
+    assert L.bk_add_noise(FAKE, 10, -1.0, 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_add_noise(FAKE, 10, float("nan"), 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_add_noise(None, 10, 1.0, 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_add_noise(FAKE, -1, 1.0, 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_philox_raw(0, 0, 0, 0, 4, None, None) == bk.BK_ERR_INVALID_VALUE
+    # embedding gradient token limit of this build
+    assert L.bk_embed_weighted_grad(FAKE, FAKE, FAKE, bk.BK_BF16, 64, 256, 16, 100, FAKE, FAKE, 1 << 30,
+                                    None) == bk.BK_ERR_NOT_SUPPORTED
+
+
+def test_empty_inputs_are_noops_without_device():
+    L = bk.lib
+    # B == 0: nothing to compute, nothing launched
+    assert L.bk_ghost_norm(None, None, bk.BK_BF16, 0, 5, 4, 5, None, None, 0, None) == bk.BK_OK
+    assert L.bk_inst_norm(None, None, bk.BK_F32, 0, 5, 4, 5, None, None, 0, None) == bk.BK_OK
+    assert L.bk_clip_factors(None, 0, 0, bk.BK_CLIP_AUTO, 1.0, 0.0, None, None, None) == bk.BK_OK
+    assert L.bk_add_noise(FAKE, 10, 0.0, 0, 0, 0, None) == bk.BK_OK       # std = 0 leaves G untouched
+    assert L.bk_add_noise(None, 0, 1.0, 0, 0, 0, None) == bk.BK_OK
+    assert L.bk_philox_raw(0, 0, 0, 0, 0, None, None) == bk.BK_OK
+
+
+def test_grouped_validation():
+    arr = (bk.bk_layer * 2)()
+    for k in range(2):
+        arr[k].kind, arr[k].T, arr[k].d, arr[k].p = bk.BK_LINEAR, 8, 16, 16
+        arr[k].x = arr[k].g = arr[k].G = 0x10000
+    arr[1].reserved = 1
+    st = bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    assert st == bk.BK_ERR_INVALID_VALUE and "reserved" in bk.bk_last_error()
+    arr[1].reserved = 0
+    arr[1].kind = 5
+    assert bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None) == bk.BK_ERR_INVALID_VALUE
+    arr[1].kind = bk.BK_LINEAR
+    arr[1].G = None
+    assert bk.lib.bk_weighted_grads(arr, 2, FAKE, bk.BK_BF16, 4, None, 0, None) == bk.BK_ERR_INVALID_VALUE
+    need = bk.bk_layer_norms_workspace_size(arr, 2, bk.BK_BF16, 4)
+    assert need > 0
+    assert bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, need - 1, None) == bk.BK_ERR_WORKSPACE
+    assert bk.lib.bk_private_grad(arr, 2, bk.BK_BF16, 4, bk.BK_CLIP_ABADI, 0.0, 0.0, 1.0, 0, 0, FAKE,
+                                  FAKE, None, FAKE, 1 << 20, None) == bk.BK_ERR_INVALID_VALUE
+
+
+def test_status_strings():
+    assert bk.bk_status_string(bk.BK_OK) == "BK_OK"
+    assert bk.bk_status_string(bk.BK_ERR_WORKSPACE) == "BK_ERR_WORKSPACE"
+    assert "gfx950" in bk.bk_version()

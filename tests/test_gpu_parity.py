@@ -1,0 +1,269 @@
+"""Parity of every libbk entry point with the float64 CPU oracle (MI355X).
+
+Inputs are seeded and synthetic (workloads / numpy), drawn on the host and
+copied to the device; the oracle sees the same values upcast exactly to
+float64.  Tolerances: norms, totals and clip factors within 1e-5 relative for
+fp32 inputs and 2e-2 for bf16 inputs; clipped gradients within 1e-4 (fp32) or
+2e-2 (bf16) relative Frobenius error; path choice and Philox words exact.
+Sizes span several tiles with ragged tails.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+NORM_TOL = {torch.float32: 1e-5, torch.bfloat16: 2e-2}
+GRAD_TOL = {torch.float32: 1e-4, torch.bfloat16: 2e-2}
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def bk():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2210_00038_amd as m
+    return m
+
+
+def _pair(B, T, d, p, dtype, seed, g_scale=1.0):
+    gen = torch.Generator().manual_seed(seed)
+    a = torch.randn(B, T, d, generator=gen).to(dtype)
+    g = (torch.randn(B, T, p, generator=gen) * g_scale).to(dtype)
+    return a, g
+
+
+def _rel(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return np.max(np.abs(x - ref) / np.maximum(np.abs(ref), 1e-300)) if ref.size else 0.0
+
+
+def _frob(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    n = np.linalg.norm(ref)
+    return np.linalg.norm(x - ref) / n if n > 0 else np.linalg.norm(x)
+
+
+SHAPES = [
+    # (B, T, d, p, dtype): one tile, several super blocks, ragged T / d / p, unaligned rows
+    (4, 16, 64, 64, torch.float32),
+    (3, 200, 96, 136, torch.bfloat16),
+    (2, 300, 72, 40, torch.float32),
+    (2, 257, 70, 33, torch.float32),          # rows not 16-byte multiples: scalar-load path
+    (2, 129, 100, 60, torch.bfloat16),        # rows not 16-byte multiples: scalar-load path
+    (5, 1, 48, 24, torch.bfloat16),
+    (2, 128, 768, 256, torch.bfloat16),
+]
+
+
+@pytest.mark.parametrize("B,T,d,p,dtype", SHAPES)
+def test_ghost_and_inst_norm_match_oracle(bk, B, T, d, p, dtype):
+    a, g = _pair(B, T, d, p, dtype, seed=B * 1000 + T)
+    ref = oracle.linear_norm_sq(a, g)
+    ghost = bk.bk_ghost_norm(a.to(DEV), g.to(DEV)).cpu().numpy()
+    inst = bk.bk_inst_norm(a.to(DEV), g.to(DEV)).cpu().numpy()
+    print(f"ghost rel err {_rel(ghost, ref):.2e}, inst rel err {_rel(inst, ref):.2e}")
+    assert _rel(ghost, ref) <= NORM_TOL[dtype]
+    assert _rel(inst, ref) <= NORM_TOL[dtype]
+
+
+def test_ghost_norm_ties_and_zero(bk):
+    a, g = _pair(3, 40, 32, 16, torch.float32, seed=5)
+    a[1].zero_()
+    out = bk.bk_ghost_norm(a.to(DEV), g.to(DEV)).cpu().numpy()
+    assert out[1] == 0.0
+    ref = oracle.linear_norm_sq(a, g)
+    assert _rel(out[[0, 2]], ref[[0, 2]]) <= 1e-5
+
+
+def test_empty_batch_and_tokens(bk):
+    a = torch.zeros(3, 0, 8, device=DEV)
+    g = torch.zeros(3, 0, 4, device=DEV)
+    assert bk.bk_ghost_norm(a, g).cpu().tolist() == [0.0, 0.0, 0.0]
+    assert bk.bk_inst_norm(a, g).cpu().tolist() == [0.0, 0.0, 0.0]
+    C = torch.ones(3, device=DEV)
+    G = bk.bk_weighted_grad(a, g, C)
+    assert G.shape == (8, 4) and torch.count_nonzero(G).item() == 0
+
+
+@pytest.mark.parametrize("B,T,V,p,dtype", [
+    (3, 50, 11, 24, torch.float32), (2, 300, 1000, 72, torch.bfloat16), (4, 64, 5, 40, torch.bfloat16)])
+def test_embed_ghost_norm_matches_oracle(bk, B, T, V, p, dtype):
+    gen = torch.Generator().manual_seed(V)
+    ids = torch.randint(0, V, (B, T), generator=gen)
+    g = torch.randn(B, T, p, generator=gen).to(dtype)
+    ref = oracle.embed_norm_sq(ids, g, V)
+    out = bk.bk_embed_ghost_norm(ids.to(DEV), g.to(DEV), V).cpu().numpy()
+    print(f"embed norm rel err {_rel(out, ref):.2e}")
+    assert _rel(out, ref) <= NORM_TOL[dtype]
+
+
+def test_embed_norm_zipf_ids(bk):
+    ids = torch.from_numpy(wl.zipf_ids(8 * 256, 50257, 1.1, 7)).view(8, 256)
+    g = (torch.randn(8, 256, 128, generator=torch.Generator().manual_seed(3)) * 1e-2).to(torch.bfloat16)
+    ref = oracle.embed_norm_sq(ids, g, 50257)
+    out = bk.bk_embed_ghost_norm(ids.to(DEV), g.to(DEV), 50257).cpu().numpy()
+    assert _rel(out, ref) <= 2e-2
+
+
+@pytest.mark.parametrize("mode,R,gamma", [(0, 1.0, 0.0), (0, 3.5, 0.0), (1, 1.0, 0.01), (1, 1.0, 0.0)])
+def test_clip_factors_match_oracle(bk, mode, R, gamma):
+    rng = np.random.default_rng(11)
+    n = (np.abs(rng.standard_normal((7, 37))) * 3).astype(np.float32)
+    n[:, 5] = 0.0                                     # a zero-gradient sample
+    C, tot = bk.bk_clip_factors(torch.from_numpy(n).to(DEV), mode, R, gamma)
+    ref_tot = oracle.aggregate(n)
+    ref_C = oracle.clip_factors(ref_tot, "abadi" if mode == 0 else "auto", R, gamma)
+    assert _rel(tot.cpu().numpy(), ref_tot) <= 1e-6
+    got = C.cpu().numpy()
+    assert np.all(np.abs(got - ref_C) <= 1e-6 * np.maximum(np.abs(ref_C), 1e-30))
+
+
+WSHAPES = [
+    (4, 16, 64, 64, torch.float32),
+    (3, 50, 200, 136, torch.bfloat16),
+    (2, 77, 70, 33, torch.float32),
+    (5, 33, 256, 384, torch.bfloat16),
+    (2, 129, 100, 60, torch.bfloat16),
+]
+
+
+@pytest.mark.parametrize("B,T,d,p,dtype", WSHAPES)
+def test_weighted_grad_matches_oracle(bk, B, T, d, p, dtype):
+    a, g = _pair(B, T, d, p, dtype, seed=77 + T)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(T)) + 0.1
+    ref = oracle.weighted_grad(a, g, C)
+    G = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), C.to(DEV)).cpu().numpy()
+    err = _frob(G, ref)
+    print(f"weighted grad frob err {err:.2e}")
+    assert err <= GRAD_TOL[dtype]
+    # C == 1 is the standard (non-private) gradient a^T g
+    G1 = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), torch.ones(B, device=DEV)).cpu().numpy()
+    assert _frob(G1, oracle.weighted_grad(a, g, np.ones(B))) <= GRAD_TOL[dtype]
+
+
+@pytest.mark.parametrize("B,T,V,p,dtype", [(3, 40, 17, 24, torch.float32), (16, 256, 50257, 64, torch.bfloat16)])
+def test_embed_weighted_grad_matches_oracle(bk, B, T, V, p, dtype):
+    ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.1, 99)).view(B, T)
+    g = torch.randn(B, T, p, generator=torch.Generator().manual_seed(5)).to(dtype)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(6)) + 0.1
+    ref = oracle.embed_weighted_grad(ids, g, C, V)
+    G = bk.bk_embed_weighted_grad(ids.to(DEV), g.to(DEV), C.to(DEV), V).cpu().numpy()
+    assert _frob(G, ref) <= GRAD_TOL[dtype]
+    absent = np.setdiff1d(np.arange(V), ids.numpy().ravel())
+    assert np.all(G[absent] == 0.0)
+
+
+@pytest.mark.parametrize("seed,tid,step,q0,nq", [
+    (0, 0, 0, 0, 1000), (0xFFFFFFFFFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, 0, 64),
+    (0x0123456789ABCDEF, 3, 11, (1 << 32) - 5, 300), (5, 144, 0, 123456789012, 77)])
+def test_philox_words_exact(bk, seed, tid, step, q0, nq):
+    got = bk.bk_philox_raw(seed, tid, step, q0, nq).cpu().numpy().view(np.uint32)
+    ref = oracle.philox_words(seed, tid, step, q0, nq)
+    np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("n,std,seed,tid,step", [(1001, 1.0, 2, 0, 0), (4096, 0.8, 5, 7, 3), (3, 2.0, 1, 1, 1)])
+def test_noise_matches_oracle(bk, n, std, seed, tid, step):
+    G0 = torch.randn(n, generator=torch.Generator().manual_seed(n))
+    G = bk.bk_add_noise(G0.clone().to(DEV), std, seed, tid, step).cpu().numpy()
+    ref = oracle.add_noise(G0, std, seed, tid, step)
+    assert np.max(np.abs(G - ref)) <= 2e-5 * std * 8
+    # std = 0 leaves the tensor bit-identical
+    Gz = bk.bk_add_noise(G0.clone().to(DEV), 0.0, seed, tid, step).cpu()
+    assert torch.equal(Gz, G0)
+
+
+def test_noise_statistics(bk):
+    z = bk.bk_add_noise(torch.zeros(1 << 22, device=DEV), 1.0, 2024, 3, 0).double()
+    m, v = z.mean().item(), z.var().item()
+    n = z.numel()
+    assert abs(m) < 5 / np.sqrt(n) and abs(v - 1) < 5 * np.sqrt(2 / n)
+
+
+def _stack_inputs(layers, B, dtype, seed):
+    ins = []
+    gen = torch.Generator().manual_seed(seed)
+    for L in layers:
+        if L.kind == "embed":
+            ids = torch.randint(0, L.d, (B, L.T), generator=gen)
+            g = (torch.randn(B, L.T, L.p, generator=gen) * 1e-2).to(dtype)
+            ins.append((ids, g))
+        else:
+            a = torch.randn(B, L.T, L.d, generator=gen).to(dtype)
+            g = (torch.randn(B, L.T, L.p, generator=gen) * 1e-2).to(dtype)
+            ins.append((a, g))
+    return ins
+
+
+def _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, std, seed):
+    dev_ins = [(x.to(DEV), g.to(DEV)) for x, g in ins]
+    Gs = [torch.empty(L.d, L.p, device=DEV) for L in layers]
+    specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
+              "V": L.d} for L, (x, g), G in zip(layers, dev_ins, Gs)]
+    arr = bk.make_layers(specs)
+    n = len(layers)
+    norm_sq = torch.empty(n, B, device=DEV)
+    C = torch.empty(B, device=DEV)
+    tot = torch.empty(B, device=DEV)
+    dt = bk.BK_BF16 if dtype == torch.bfloat16 else bk.BK_F32
+    bk.bk_private_grad(arr, n, dt, B, mode, R, gamma, std, seed, 0, norm_sq, C, tot)
+    torch.cuda.synchronize()
+    return norm_sq.cpu().numpy(), C.cpu().numpy(), tot.cpu().numpy(), [G.cpu().numpy() for G in Gs]
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_private_grad_stack_matches_oracle(bk, dtype):
+    """Whole path on a small mixed stack: ghost, instantiated and embedding layers."""
+    Lr = wl.Layer
+    layers = [Lr("linear", 40, 64, 96),       # ghost (3200 < 6144)
+              Lr("linear", 150, 96, 130),     # instantiate (45000 > 12480)
+              Lr("linear", 150, 200, 260),    # ghost (45000 < 52000)
+              Lr("embed", 40, 500, 64)]
+    B = 6
+    ins = _stack_inputs(layers, B, dtype, seed=42)
+    for mode, R, gamma, std in [(0, 1e-2, 0.0, 0.0), (1, 1.0, 0.01, 0.0), (0, 1e-2, 0.0, 0.7)]:
+        norms, C, tot, G = _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, std, seed=9)
+        ref = oracle.bk_stack(layers, ins, "abadi" if mode == 0 else "auto", R, gamma, std, seed=9,
+                              with_noise=std > 0)
+        assert ref["paths"] == ["ghost", "inst", "ghost", "embed"]
+        assert _rel(norms, ref["norms"]) <= NORM_TOL[dtype]
+        assert _rel(tot, ref["total"]) <= NORM_TOL[dtype]
+        assert _rel(C, ref["C"]) <= NORM_TOL[dtype]
+        for l in range(len(layers)):
+            want = ref["Ghat"][l] if std > 0 else ref["G"][l]
+            if std > 0:
+                # compare the clipped gradient and the noise separately
+                noise_ref = ref["Ghat"][l] - ref["G"][l]
+                got_noise = G[l] - ref["G"][l]
+                assert np.max(np.abs(got_noise - noise_ref)) <= 1e-4 * std * 8 + 1e-3 * np.abs(ref["G"][l]).max()
+            else:
+                assert _frob(G[l], want) <= GRAD_TOL[dtype], l
+
+
+def test_config1_single_layer(bk):
+    """Single fp32 linear layer, B=4, T=16, d=p=64, Abadi R=1, sigma=1: the
+    ghost path against brute-force per-sample gradients."""
+    w = wl.get(1)
+    a, g = wl.draw_linear(w, 0)
+    ref = oracle.linear_norm_sq_bruteforce(a, g)
+    out = bk.bk_ghost_norm(a.to(DEV), g.to(DEV)).cpu().numpy()
+    assert _rel(out, ref) <= 1e-5
+    assert bk.bk_use_ghost(16, 64, 64)
+    norms, C, tot, G = _run_stack(bk, list(w.layers), [(a, g)], w.B, torch.float32, 0, 1.0, 0.0, 0.0, seed=1)
+    refs = oracle.bk_stack(list(w.layers), [(a, g)], "abadi", 1.0, 0.0, 1.0, seed=1)
+    assert _rel(C, refs["C"]) <= 1e-5
+    assert _frob(G[0], refs["G"][0]) <= 1e-4
+
+
+def test_determinism(bk):
+    a, g = _pair(4, 200, 256, 384, torch.bfloat16, seed=3)
+    a, g = a.to(DEV), g.to(DEV)
+    C = torch.rand(4, device=DEV)
+    n1, n2 = bk.bk_ghost_norm(a, g), bk.bk_ghost_norm(a, g)
+    G1, G2 = bk.bk_weighted_grad(a, g, C), bk.bk_weighted_grad(a, g, C)
+    assert torch.equal(n1, n2) and torch.equal(G1, G2)
