@@ -1,0 +1,217 @@
+"""Benchmark of the BK private-gradient path on one MI355X.
+
+One step = the whole path of Algorithm 1 after book-keeping, over one batch of
+a synthetic layer stack whose inputs already sit in HBM:
+
+    per-layer per-sample norms (ghost / instantiated / embedding)  -> [L, B]
+    clip factors                                                   -> [B]
+    clip-weighted gradients of every layer                         -> G_l
+    Gaussian noise on every G_l
+
+Default workload: the GPT-2-small-shaped stack (12 blocks of 768->2304,
+768->768, 768->3072, 3072->768; B=32, T=128, bf16, automatic clipping
+gamma=0.01, sigma=1).  Prints one JSON line: samples/s, the roofline of the
+dominant kernel measured with HIP events on the launch stream over the timed
+steps, and the float64 CPU oracle timed on a bounded sample of the same
+workload on the host.
+
+    python bench.py [--steps K] [--warmup W] [--workload N] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+METRIC = "BK clipped-grad samples/s on layer stack; ghost-norm+weighted-GEMM % MFMA peak"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense MFMA
+
+
+def algorithmic_work(w: wl.Workload):
+    """Per-step algorithmic flops / bytes of each phase (paper's per-module costs)."""
+    es = 2 if w.dtype == "bf16" else 4
+    B = w.B
+    out = {"norm_flops": 0.0, "norm_bytes": 0.0, "gemm_flops": 0.0, "gemm_bytes": 0.0,
+           "noise_elems": 0.0, "ghost_layers": 0, "inst_layers": 0, "embed_layers": 0}
+    for L in w.layers:
+        if L.kind == "embed":
+            out["embed_layers"] += 1
+            out["norm_bytes"] += B * L.T * (L.p * es + 8)
+            out["gemm_bytes"] += B * L.T * (L.p * es + 8) + 4.0 * L.d * L.p
+        else:
+            ghost = 2 * L.T * L.T < L.p * L.d
+            if ghost:
+                out["ghost_layers"] += 1
+                out["norm_flops"] += 2.0 * B * L.T * L.T * (L.p + L.d)       # ghost norm, App. B.4
+            else:
+                out["inst_layers"] += 1
+                out["norm_flops"] += 2.0 * B * L.T * L.p * L.d               # instantiation, App. B.4.1
+            out["norm_bytes"] += B * L.T * (L.d + L.p) * es
+            out["gemm_flops"] += 2.0 * B * L.T * L.p * L.d                   # a^T diag(C) g, App. B.3
+            out["gemm_bytes"] += B * L.T * (L.d + L.p) * es + 4.0 * L.d * L.p
+        out["noise_elems"] += float(L.d) * L.p
+    return out
+
+
+def make_inputs(w: wl.Workload, dev):
+    ins = [wl.draw_layer(w, l, device=dev) for l in range(len(w.layers))]
+    Gs = [torch.empty(L.d, L.p, device=dev) for L in w.layers]
+    return ins, Gs
+
+
+def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
+    """The float64 oracle on the host: whole path on the first layers of the
+    stack (all B samples), until ~budget_s of work; scaled to the whole stack
+    by the fraction of its gradient flops done."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    total = algorithmic_work(w)["gemm_flops"] + 1e-9
+    done, t_used, nl = 0.0, 0.0, 0
+    for l, L in enumerate(w.layers):
+        x, g = wl.draw_layer(w, l)
+        t0 = time.perf_counter()
+        n = oracle.bk_layer_norm(L.kind, x, g, L.d)
+        C = oracle.clip_factors(n, w.clip, w.R, w.gamma)
+        G = (oracle.embed_weighted_grad(x, g, C, L.d) if L.kind == "embed" else oracle.weighted_grad(x, g, C))
+        oracle.add_noise(G, w.noise_std, w.wid, l, 0)
+        t_used += time.perf_counter() - t0
+        done += 2.0 * w.B * L.T * L.p * L.d
+        nl += 1
+        if t_used >= budget_s:
+            break
+    t_full = t_used * total / done
+    return {"value": w.B / t_full, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {nl} of {len(w.layers)} layers, all {w.B} samples, full path in float64 "
+                      f"({t_used:.1f} s), scaled by gradient flops to the whole stack"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-5)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path shards by samples "
+              "with one all-reduce of each G_l, which this single-GPU build does not run.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2210_00038_amd as bk
+
+    w = wl.get(args.workload)
+    dev = torch.device("cuda:0")
+    dt = bk.BK_BF16 if w.dtype == "bf16" else bk.BK_F32
+    mode = bk.BK_CLIP_ABADI if w.clip == "abadi" else bk.BK_CLIP_AUTO
+    n, B = len(w.layers), w.B
+
+    ins, Gs = make_inputs(w, dev)
+    specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
+              "V": L.d} for L, (x, g), G in zip(w.layers, ins, Gs)]
+    arr = bk.make_layers(specs)
+    norm_sq = torch.empty(n, B, device=dev)
+    C = torch.empty(B, device=dev)
+    tot = torch.empty(B, device=dev)
+    ws_n = torch.empty(max(1, bk.bk_layer_norms_workspace_size(arr, n, dt, B)), dtype=torch.uint8, device=dev)
+    ws_g = torch.empty(max(1, bk.bk_weighted_grads_workspace_size(arr, n, dt, B)), dtype=torch.uint8,
+                       device=dev)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    import ctypes
+    g_ptrs = (ctypes.c_void_p * n)(*[G.data_ptr() for G in Gs])
+    g_nel = (ctypes.c_int64 * n)(*[G.numel() for G in Gs])
+    g_tid = (ctypes.c_uint32 * n)(*range(n))
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        bk._check(bk.lib.bk_layer_norms(arr, n, dt, B, norm_sq.data_ptr(), ws_n.data_ptr(),
+                                        ws_n.numel(), sp), "bk_layer_norms")
+        if ev: ev[1].record(stream)
+        bk._check(bk.lib.bk_clip_factors(norm_sq.data_ptr(), n, B, mode, w.R, w.gamma, C.data_ptr(),
+                                         tot.data_ptr(), sp), "bk_clip_factors")
+        if ev: ev[2].record(stream)
+        bk._check(bk.lib.bk_weighted_grads(arr, n, C.data_ptr(), dt, B, ws_g.data_ptr(), ws_g.numel(), sp),
+                  "bk_weighted_grads")
+        if ev: ev[3].record(stream)
+        bk._check(bk.lib.bk_add_noise_grouped(g_ptrs, g_nel, g_tid, n, w.noise_std, w.wid, 0, sp),
+                  "bk_add_noise_grouped")
+        if ev: ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert torch.isfinite(C).all().item(), "non-finite clip factors"
+
+    ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs])   # ms
+    ph_ms = ph.mean(axis=0)
+    work = algorithmic_work(w)
+    ms_step = elapsed * 1e3 / args.steps
+    peak_mfma = PEAK_MFMA_TFLOPS[w.dtype]
+    phases = {
+        "norms": {"ms": ph_ms[0], "tflops": work["norm_flops"] / ph_ms[0] / 1e9,
+                  "gbs": work["norm_bytes"] / ph_ms[0] / 1e6},
+        "clip": {"ms": ph_ms[1]},
+        "weighted_grads": {"ms": ph_ms[2], "tflops": work["gemm_flops"] / ph_ms[2] / 1e9,
+                           "gbs": work["gemm_bytes"] / ph_ms[2] / 1e6},
+        "noise": {"ms": ph_ms[3], "gbs": 8.0 * work["noise_elems"] / ph_ms[3] / 1e6},
+    }
+    # Dominant kernel: the phase with the most time among the two big ones.
+    if phases["weighted_grads"]["ms"] >= phases["norms"]["ms"]:
+        ach = phases["weighted_grads"]["tflops"]
+        roof = {"kernel": "agemm_kernel (clip-weighted gradient, all layers in one launch)",
+                "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
+                "frac": ach / peak_mfma, "traffic": None,
+                "per_launch": f"{work['gemm_flops'] / 1e9:.1f} GFLOP (sum over layers of 2 B T d p)"}
+    else:
+        ach = phases["norms"]["gbs"]
+        roof = {"kernel": "ghost_norm_kernel + reduce (all layers)", "bound": "hbm", "achieved": ach,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None,
+                "per_launch": f"{work['norm_bytes'] / 1e9:.3f} GB (a and g read once)"}
+    for v in phases.values():
+        for k in list(v):
+            v[k] = round(float(v[k]), 4)
+    res = {
+        "metric": METRIC, "value": B / (ms_step / 1e3), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
+                   "clip": w.clip, "sigma": w.sigma, "paths": {"ghost": work["ghost_layers"],
+                   "inst": work["inst_layers"], "embed": work["embed_layers"]}},
+        "roofline": roof,
+        "phases": phases,
+        "mfma_frac": {"ghost_norm_paper_flops": phases["norms"].get("tflops", 0) / peak_mfma,
+                      "weighted_gemm": phases["weighted_grads"]["tflops"] / peak_mfma},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -176,6 +176,12 @@ bk_status bk_embed_weighted_grad(const int64_t* ids, const void* g, const float*
 bk_status bk_add_noise(float* G, int64_t n, float std, uint64_t seed, uint32_t tensor_id,
                        uint32_t step, void* stream);
 
+/* bk_add_noise on n tensors in one launch: tensor k (G[k], nel[k] elements)
+ * gets the stream of tensor_id[k]; the values are those of bk_add_noise on
+ * each tensor.  G, nel and tensor_id are host arrays of n entries. */
+bk_status bk_add_noise_grouped(float* const* G, const int64_t* nel, const uint32_t* tensor_id,
+                               int64_t n, float std, uint64_t seed, uint32_t step, void* stream);
+
 /* Raw Philox4x32-10 words of counter blocks q0 .. q0+nq-1 of (seed, tensor_id,
  * step), as used by bk_add_noise: out [nq, 4] uint32 (device). */
 bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64_t q0,
@@ -202,8 +208,8 @@ bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, b
 
 /* The whole path of Algorithm 1 from the per-layer norms to the noise, with
  * the layerwise norm choice of Algorithm "BKAL-mixed" (BK-MixGhostClip):
- * bk_layer_norms -> bk_clip_factors -> bk_weighted_grads -> bk_add_noise on
- * every layers[l].G with tensor_id = l.  norm_sq [n,B], C [B] out, total_sq [B]
+ * bk_layer_norms -> bk_clip_factors -> bk_weighted_grads -> bk_add_noise_grouped
+ * on every layers[l].G with tensor_id = l.  norm_sq [n,B], C [B] out, total_sq [B]
  * out (may be NULL).  noise_std = sigma R; 0 skips the noise. */
 size_t bk_private_grad_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
                                       int64_t B);

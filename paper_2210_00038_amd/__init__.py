@@ -26,7 +26,7 @@ __all__ = [
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
-    "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
+    "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
     "bk_layer_norms_workspace_size", "bk_weighted_grads_workspace_size",
     "bk_private_grad_workspace_size", "bk_status_string", "bk_last_error", "bk_version",
 ]
@@ -43,8 +43,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbk.so")
 # Every symbol include/bk.h declares.
 EXPORTS = (
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
-    "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
+    "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
+    "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
     "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_status_string",
     "bk_last_error", "bk_version",
 )
@@ -64,7 +64,7 @@ class bk_layer(ctypes.Structure):
 
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2210_00038_amd.build` "
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2210_00038_amd/build.py` "
                       "(the BK path has no fallback)")
 lib = ctypes.CDLL(LIB_PATH)
 
@@ -83,6 +83,7 @@ _SIG = {
     "bk_embed_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp,
                                      _sz, _vp]),
     "bk_add_noise": (_st, [_vp, _i64, _f32, _u64, _u32, _u32, _vp]),
+    "bk_add_noise_grouped": (_st, [_vp, _vp, _vp, _i64, _f32, _u64, _u32, _vp]),
     "bk_philox_raw": (_st, [_u64, _u32, _u32, _u64, _i64, _vp, _vp]),
     "bk_layer_norms_workspace_size": (_sz, [_P, _i64, ctypes.c_int, _i64]),
     "bk_layer_norms": (_st, [_P, _i64, ctypes.c_int, _i64, _vp, _vp, _sz, _vp]),
@@ -275,6 +276,22 @@ def bk_add_noise(G, std: float, seed: int, tensor_id: int, step: int = 0, stream
     _check(lib.bk_add_noise(_ptr(G), G.numel(), std, seed, tensor_id, step, _stream(stream)),
            "bk_add_noise")
     return G
+
+
+def bk_add_noise_grouped(Gs: Sequence[torch.Tensor], std: float, seed: int, tensor_ids=None, step: int = 0,
+                         stream=None):
+    """bk_add_noise on every tensor of Gs in one launch (tensor k uses tensor_ids[k], default k)."""
+    n = len(Gs)
+    for G in Gs:
+        _dev(G, "G")
+        if G.dtype != torch.float32:
+            raise ValueError("G must be float32")
+    ptrs = (ctypes.c_void_p * max(1, n))(*[_ptr(G) for G in Gs])
+    nel = (ctypes.c_int64 * max(1, n))(*[G.numel() for G in Gs])
+    tids = (ctypes.c_uint32 * max(1, n))(*(range(n) if tensor_ids is None else tensor_ids))
+    _check(lib.bk_add_noise_grouped(ptrs, nel, tids, n, std, seed, step, _stream(stream)),
+           "bk_add_noise_grouped")
+    return Gs
 
 
 def bk_philox_raw(seed: int, tensor_id: int, step: int, q0: int, nq: int, out=None, device="cuda",

@@ -1,6 +1,6 @@
 """Build libbk.so (the HIP kernels and the C ABI of include/bk.h) for gfx950.
 
-    python -m paper_2210_00038_amd.build
+    python paper_2210_00038_amd/build.py
 
 Every source is compiled by hipcc into an object in ``_build/`` (in parallel),
 then linked into ``paper_2210_00038_amd/libbk.so``.  Packed-fp32 instruction

@@ -230,12 +230,188 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernel for 16-byte aligned rows.  Tiles are staged in LDS exactly as
+// they sit in memory ([k][m] with m contiguous: plain 16-byte copies) and the
+// MFMA fragments are gathered with the gfx950 LDS transpose read
+// ds_read_b64_tr_b16: in each 16-lane group, lanes 4q..4q+3 point at 16
+// consecutive columns of row q, and lane j receives column j of the 4 rows.
+// Two such reads give a lane the 8 k values of its column.
+//
+// Workgroup tile 256 (m) x 128 (n), k stage 64; wave (wm, wn) owns
+// rows [128 wm, 128 wm + 128) x columns [64 wn, 64 wn + 64) as 4 x 2 MFMA
+// 32x32x16 accumulators.  LDS rows are padded to 576 / 320 bytes so that the
+// four rows a 16-lane group reads fall on distinct banks.
+// ---------------------------------------------------------------------------
+constexpr int kBM = 256, kBN = 128, kBK = 64;
+constexpr int kSA = kBM * 2 + 64;     // bytes per staged k-row of a
+constexpr int kSB = kBN * 2 + 64;     // bytes per staged k-row of g
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint2 lds_tr16(const char* p) {
+    const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)(p));
+    return __builtin_bit_cast(uint2, v);
+}
+
+// Fragment of columns [cb, cb + 32) for k rows [kb, kb + 16) of a [k][col]
+// tile with row stride S bytes: lane l ends with 8 k values of column
+// cb + 16 ((l >> 4) & 1) + (l & 15), k = kb + 8 (l >> 5) + 0..7.
+template <int S>
+__device__ __forceinline__ uint4 frag_tr(const char* lds, int kb, int cb, int lane) {
+    const int grp = lane >> 4, i = lane & 15;
+    const int row = kb + 8 * (grp >> 1) + (i >> 2);
+    const int col = cb + 16 * (grp & 1) + 4 * (i & 3);
+    const char* p = lds + row * S + col * 2;
+    const uint2 lo = lds_tr16(p), hi = lds_tr16(p + 4 * S);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+// Two bf16 in one word, each multiplied by c, rounded to nearest even.
+__device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float c) {
+    const f32x2_t f = {__uint_as_float(w << 16) * c, __uint_as_float(w & 0xFFFF0000u) * c};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+// Logical tile of workgroup `wg` of `n` such that consecutive logical tiles
+// run on the same XCD (workgroups are dealt round-robin to the 8 XCDs).
+__device__ __forceinline__ int xcd_remap(int wg, int n) {
+    const int x = wg & 7, idx = wg >> 3, per = n >> 3, rem = n & 7;
+    return x * per + min(x, rem) + idx;
+}
+
+template <bool INST>
+__global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args, int n_wg) {
+    __shared__ __attribute__((aligned(16))) char ldsA[kBK * kSA];
+    __shared__ __attribute__((aligned(16))) char ldsB[kBK * kSB];
+    __shared__ float red[4];
+
+    const int wg = xcd_remap(blockIdx.x, n_wg);
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const GemmLayer& L = args.L[l];
+    const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
+    const int tiles = L.tm * tn;
+    const int local = wg - L.wg_begin;
+    const int sample = INST ? local / tiles : 0;
+    const int tile = local - sample * tiles;
+    const int mt = tile / tn, nt = tile - mt * tn;
+    const int m0 = mt * kBM, n0 = nt * kBN;
+
+    const int64_t row0 = INST ? (int64_t)sample * nT : 0;
+    const int64_t nrows = INST ? (int64_t)nT : (int64_t)args.B * nT;
+    const bf16_t* A = reinterpret_cast<const bf16_t*>(L.a) + row0 * d;
+    const bf16_t* Bm = reinterpret_cast<const bf16_t*>(L.g) + row0 * p;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    // Staging: a tile is 64 rows x 32 chunks of 16 B (8 chunks per thread),
+    // g tile 64 rows x 16 chunks (4 per thread).
+    const int ca = (tid & 31) * 8, ka = tid >> 5;      // + 8 j rows
+    const int cb = (tid & 15) * 8, kb = tid >> 4;      // + 16 j rows
+    const bool a_col = m0 + ca < d, b_col = n0 + cb < p;
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
+
+    uint4 va[8], vb[4];
+    float cw[4];
+    auto fetch = [&](int64_t k0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int64_t k = k0 + ka + 8 * j;
+            va[j] = (k < nrows && a_col) ? *reinterpret_cast<const uint4*>(A + k * d + m0 + ca)
+                                         : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t k = k0 + kb + 16 * j;
+            const bool ok = k < nrows;
+            vb[j] = (ok && b_col) ? *reinterpret_cast<const uint4*>(Bm + k * p + n0 + cb)
+                                  : make_uint4(0u, 0u, 0u, 0u);
+            if constexpr (!INST) cw[j] = ok ? args.C[(uint32_t)k / (uint32_t)nT] : 0.f;
+        }
+    };
+
+    const int64_t nst = (nrows + kBK - 1) / kBK;
+    fetch(0);
+    for (int64_t st = 0; st < nst; ++st) {
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            *reinterpret_cast<uint4*>(ldsA + (ka + 8 * j) * kSA + ca * 2) = va[j];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint4 v = vb[j];
+            if constexpr (!INST)
+                v = make_uint4(scale_bf16x2(v.x, cw[j]), scale_bf16x2(v.y, cw[j]), scale_bf16x2(v.z, cw[j]),
+                               scale_bf16x2(v.w, cw[j]));
+            *reinterpret_cast<uint4*>(ldsB + (kb + 16 * j) * kSB + cb * 2) = v;
+        }
+        __syncthreads();
+        if (st + 1 < nst) fetch((st + 1) * kBK);
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            uint4 fa[4], fb[2];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) fa[x] = frag_tr<kSA>(ldsA, 16 * kk, 128 * wm + 32 * x, lane);
+#pragma unroll
+            for (int y = 0; y < 2; ++y) fb[y] = frag_tr<kSB>(ldsB, 16 * kk, 64 * wn + 32 * y, lane);
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) Mfma<bf16_t>::step(acc[x][y], fa[x], fb[y]);
+        }
+    }
+
+    if constexpr (INST) {
+        float s = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) s += acc[x][y][i] * acc[x][y][i];
+        const float tot = block_sum_256(s, red);
+        if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
+    } else {
+        float* G = L.G;
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int n = n0 + 64 * wn + 32 * y + (lane & 31);
+                if (n >= p) continue;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
+                    if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
+                }
+            }
+    }
+}
+
 }  // namespace
+
+bool gemm_uses_wide_tile(bool bf16, bool vec) { return bf16 && vec; }
 
 hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, bool vec,
                        hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
     const dim3 grid(n_wg), block(256);
+    if (gemm_uses_wide_tile(bf16, vec)) {
+        if (inst_norm) hipLaunchKernelGGL(agemm_bf16_kernel<true>, grid, block, 0, s, args, n_wg);
+        else hipLaunchKernelGGL(agemm_bf16_kernel<false>, grid, block, 0, s, args, n_wg);
+        return hipGetLastError();
+    }
 #define BK_GEMM(T, I, V) hipLaunchKernelGGL((agemm_kernel<T, I, V>), grid, block, 0, s, args)
     if (bf16) {
         if (inst_norm) { if (vec) BK_GEMM(bf16_t, true, true); else BK_GEMM(bf16_t, true, false); }

@@ -86,8 +86,9 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
         np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
     }
     if (np.path == Path::Inst) {
-        np.npart = cdiv(L.d, bk::kTile) * cdiv(L.p, bk::kTile);
         np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
+        const bool bf16 = dt == BK_BF16;
+        np.npart = cdiv(L.d, bk::gemm_tile_m(bf16, np.vec)) * cdiv(L.p, bk::gemm_tile_n(bf16, np.vec));
     } else {
         const int64_t nsb = cdiv(L.T, bk::kSuper);
         np.npart = nsb * (nsb + 1) / 2;
@@ -208,8 +209,8 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::kTile);
-            g.tn = (int32_t)cdiv(L.p, bk::kTile);
+            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bf16, vec));
+            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bf16, vec));
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
             wg += v[k]->np.nwg;
@@ -309,8 +310,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::kTile);
-            g.tn = (int32_t)cdiv(L.p, bk::kTile);
+            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bf16, vec == 1));
+            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bf16, vec == 1));
             g.wg_begin = (int32_t)wg;
             g.part_off = 0;
             wg += (int64_t)g.tm * g.tn;
@@ -397,9 +398,10 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
     NormPlan np = norm_plan(L, dt, B);
     np.path = want;
     if (want == Path::Inst) {
-        np.npart = cdiv(L.d, bk::kTile) * cdiv(L.p, bk::kTile);
         const size_t es = elem_bytes(dt);
         np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
+        np.npart = cdiv(L.d, bk::gemm_tile_m(dt == BK_BF16, np.vec)) *
+                   cdiv(L.p, bk::gemm_tile_n(dt == BK_BF16, np.vec));
     } else {
         const int64_t nsb = cdiv(L.T, bk::kSuper);
         np.npart = nsb * (nsb + 1) / 2;
@@ -426,8 +428,8 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.T = (int32_t)L.T;
         g.d = (int32_t)L.d;
         g.p = (int32_t)L.p;
-        g.tm = (int32_t)cdiv(L.d, bk::kTile);
-        g.tn = (int32_t)cdiv(L.p, bk::kTile);
+        g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(dt == BK_BF16, np.vec));
+        g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(dt == BK_BF16, np.vec));
         e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, np.vec, s);
     } else {
         bk::GhostArgs a{};
@@ -481,7 +483,7 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
             const int64_t nsb = cdiv(T, bk::kSuper);
             return align_up((size_t)(B * (nsb * (nsb + 1) / 2)) * sizeof(float));
         }
-        case BK_OP_INST_NORM:
+        case BK_OP_INST_NORM:   // upper bound over the tile shapes (alignment is not known here)
             return align_up((size_t)(B * cdiv(d, bk::kTile) * cdiv(p, bk::kTile)) * sizeof(float));
         case BK_OP_WEIGHTED_GRAD:
             return 0;
@@ -553,6 +555,20 @@ bk_status bk_add_noise(float* G, int64_t n, float std, uint64_t seed, uint32_t t
     if (!(std >= 0.f) || std == INFINITY) return fail(BK_ERR_INVALID_VALUE, "%s: std must be finite and >= 0", fn);
     if (n == 0 || std == 0.f) return BK_OK;
     return add_noise_layers(fn, &G, &n, &tensor_id, 1, std, seed, step, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_add_noise_grouped(float* const* G, const int64_t* nel, const uint32_t* tensor_id,
+                               int64_t n, float std, uint64_t seed, uint32_t step, void* stream) {
+    const char* fn = "bk_add_noise_grouped";
+    if (n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative tensor count", fn);
+    if (n > 0 && (!G || !nel || !tensor_id)) return fail(BK_ERR_INVALID_VALUE, "%s: NULL array", fn);
+    if (!(std >= 0.f) || std == INFINITY) return fail(BK_ERR_INVALID_VALUE, "%s: std must be finite and >= 0", fn);
+    for (int64_t k = 0; k < n; ++k) {
+        if (nel[k] < 0) return fail(BK_ERR_INVALID_VALUE, "%s: tensor %lld: negative size", fn, (long long)k);
+        if (nel[k] > 0 && !G[k]) return fail(BK_ERR_INVALID_VALUE, "%s: tensor %lld: NULL", fn, (long long)k);
+    }
+    if (n == 0 || std == 0.f) return BK_OK;
+    return add_noise_layers(fn, G, nel, tensor_id, n, std, seed, step, static_cast<hipStream_t>(stream));
 }
 
 bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64_t q0, int64_t nq,

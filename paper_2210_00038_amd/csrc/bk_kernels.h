@@ -82,6 +82,12 @@ struct NoiseArgs {
 };
 constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by one workgroup
 
+// Output tile of the a^T g GEMMs: 256 x 128 for the bf16 kernel on 16-byte
+// aligned rows, kTile x kTile otherwise.
+bool gemm_uses_wide_tile(bool bf16, bool vec);
+inline int gemm_tile_m(bool bf16, bool vec) { return gemm_uses_wide_tile(bf16, vec) ? 256 : kTile; }
+inline int gemm_tile_n(bool, bool) { return kTile; }
+
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);

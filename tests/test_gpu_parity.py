@@ -57,6 +57,7 @@ SHAPES = [
     (2, 129, 100, 60, torch.bfloat16),        # rows not 16-byte multiples: scalar-load path
     (5, 1, 48, 24, torch.bfloat16),
     (2, 128, 768, 256, torch.bfloat16),
+    (2, 70, 520, 264, torch.bfloat16),        # ragged 256 x 128 tiles of the instantiated norm
 ]
 
 
@@ -129,6 +130,8 @@ WSHAPES = [
     (2, 77, 70, 33, torch.float32),
     (5, 33, 256, 384, torch.bfloat16),
     (2, 129, 100, 60, torch.bfloat16),
+    (3, 130, 1280, 384, torch.bfloat16),      # several 256 x 128 tiles, ragged k stages
+    (2, 64, 520, 264, torch.bfloat16),        # ragged tiles in both output dimensions
 ]
 
 
@@ -267,3 +270,11 @@ def test_determinism(bk):
     n1, n2 = bk.bk_ghost_norm(a, g), bk.bk_ghost_norm(a, g)
     G1, G2 = bk.bk_weighted_grad(a, g, C), bk.bk_weighted_grad(a, g, C)
     assert torch.equal(n1, n2) and torch.equal(G1, G2)
+
+
+def test_grouped_noise_equals_per_tensor_noise(bk):
+    Gs = [torch.randn(n, generator=torch.Generator().manual_seed(n)).to(DEV) for n in (5, 4096, 1, 777)]
+    ref = [bk.bk_add_noise(G.clone(), 0.6, 31, 10 + k, 2) for k, G in enumerate(Gs)]
+    got = bk.bk_add_noise_grouped([G.clone() for G in Gs], 0.6, 31, tensor_ids=[10, 11, 12, 13], step=2)
+    for r, o in zip(ref, got):
+        assert torch.equal(r, o)
