@@ -20,6 +20,8 @@
 #include "bk_device.h"
 #include "bk_kernels.h"
 
+#include <algorithm>
+
 namespace bk {
 namespace {
 
@@ -184,10 +186,10 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
     const int64_t nst = (nrows + BK - 1) / BK;
     fetch(0);
     for (int64_t st = 0; st < nst; ++st) {
-        __syncthreads();
+        lds_barrier();
         store_transposed<T, false>(ldsA, kg, mg * EPV, va, cw);
         store_transposed<T, !INST>(ldsB, kg, mg * EPV, vb, cw);
-        __syncthreads();
+        lds_barrier();
         if (st + 1 < nst) fetch((st + 1) * BK);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -238,14 +240,18 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
 // consecutive columns of row q, and lane j receives column j of the 4 rows.
 // Two such reads give a lane the 8 k values of its column.
 //
-// Workgroup tile 256 (m) x 128 (n), k stage 64; wave (wm, wn) owns
-// rows [128 wm, 128 wm + 128) x columns [64 wn, 64 wn + 64) as 4 x 2 MFMA
-// 32x32x16 accumulators.  LDS rows are padded to 576 / 320 bytes so that the
-// four rows a 16-lane group reads fall on distinct banks.
+// Workgroup tile 256 (m) x 128 (n), k stage 64, two workgroups per CU; wave
+// (wm, wn) owns rows [128 wm, 128 wm + 128) x columns [64 wn, 64 wn + 64) as
+// 4 x 2 MFMA 32x32x16 accumulators.  One LDS buffer per stage: the next
+// stage's global loads are issued right after the tile is written and land
+// in registers while the waves multiply.  LDS rows are padded to 576 / 320
+// bytes so that the four rows a 16-lane group reads fall on distinct banks.
+// The other workgroup on the CU covers this one's barriers.
 // ---------------------------------------------------------------------------
+constexpr uint32_t kOut = 0xFFFFFFF0u;           // buffer offset that loads zeros
 constexpr int kBM = 256, kBN = 128, kBK = 64;
-constexpr int kSA = kBM * 2 + 64;     // bytes per staged k-row of a
-constexpr int kSB = kBN * 2 + 64;     // bytes per staged k-row of g
+constexpr int kSA = kBM * 2 + 64;                // bytes per staged k-row of a
+constexpr int kSB = kBN * 2 + 64;                // bytes per staged k-row of g
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -301,18 +307,24 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kBM, n0 = nt * kBN;
 
+    // Contraction rows: one sample's T rows (instantiation) or all B*T rows.
+    // The host guarantees (nrows + 2 kBK) * row bytes < 2^31 for this kernel.
     const int64_t row0 = INST ? (int64_t)sample * nT : 0;
-    const int64_t nrows = INST ? (int64_t)nT : (int64_t)args.B * nT;
-    const bf16_t* A = reinterpret_cast<const bf16_t*>(L.a) + row0 * d;
-    const bf16_t* Bm = reinterpret_cast<const bf16_t*>(L.g) + row0 * p;
+    const uint32_t nrows = INST ? (uint32_t)nT : (uint32_t)args.B * (uint32_t)nT;
+    const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(reinterpret_cast<const bf16_t*>(L.a) + row0 * d, nrows * rowA);
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(reinterpret_cast<const bf16_t*>(L.g) + row0 * p, nrows * rowB);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    // Staging: a tile is 64 rows x 32 chunks of 16 B (8 chunks per thread),
-    // g tile 64 rows x 16 chunks (4 per thread).
+    // Staging: the a tile is 64 rows x 32 chunks of 16 B (8 chunks per
+    // thread), the g tile 64 rows x 16 chunks (4 per thread).  Rows past the
+    // last one fall outside the buffer resource and load as zeros; chunks past
+    // the last column get an out-of-range offset and load as zeros too.
     const int ca = (tid & 31) * 8, ka = tid >> 5;      // + 8 j rows
     const int cb = (tid & 15) * 8, kb = tid >> 4;      // + 16 j rows
-    const bool a_col = m0 + ca < d, b_col = n0 + cb < p;
+    const uint32_t offA = (m0 + ca < d) ? (uint32_t)ka * rowA + (uint32_t)(m0 + ca) * 2u : kOut;
+    const uint32_t offB = (n0 + cb < p) ? (uint32_t)kb * rowB + (uint32_t)(n0 + cb) * 2u : kOut;
 
     f32x16_t acc[4][2];
 #pragma unroll
@@ -324,27 +336,37 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 
     uint4 va[8], vb[4];
     float cw[4];
-    auto fetch = [&](int64_t k0) {
+    auto fetch = [&](uint32_t k0) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int64_t k = k0 + ka + 8 * j;
-            va[j] = (k < nrows && a_col) ? *reinterpret_cast<const uint4*>(A + k * d + m0 + ca)
-                                         : make_uint4(0u, 0u, 0u, 0u);
-        }
+        for (int j = 0; j < 8; ++j)
+            va[j] = buffer_load16(rA, offA == kOut ? kOut : offA + (k0 + 8u * j) * rowA);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t k = k0 + kb + 16 * j;
-            const bool ok = k < nrows;
-            vb[j] = (ok && b_col) ? *reinterpret_cast<const uint4*>(Bm + k * p + n0 + cb)
-                                  : make_uint4(0u, 0u, 0u, 0u);
-            if constexpr (!INST) cw[j] = ok ? args.C[(uint32_t)k / (uint32_t)nT] : 0.f;
+        for (int j = 0; j < 4; ++j)
+            vb[j] = buffer_load16(rB, offB == kOut ? kOut : offB + (k0 + 16u * j) * rowB);
+        if constexpr (!INST) {
+            // Clip weight of each staged g row: C[k / T].  When T >= 64 the 64
+            // rows of a stage span at most two samples (scalar split point).
+            const uint32_t q0 = k0 / (uint32_t)nT;
+            if (nT >= kBK) {
+                const uint32_t split = (q0 + 1u) * (uint32_t)nT - k0;
+                const float c0 = args.C[min(q0, (uint32_t)args.B - 1u)];
+                const float c1 = args.C[min(q0 + 1u, (uint32_t)args.B - 1u)];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) cw[j] = ((uint32_t)(kb + 16 * j) < split) ? c0 : c1;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t k = min(k0 + (uint32_t)(kb + 16 * j), nrows - 1u);
+                    cw[j] = args.C[k / (uint32_t)nT];
+                }
+            }
         }
     };
 
-    const int64_t nst = (nrows + kBK - 1) / kBK;
-    fetch(0);
-    for (int64_t st = 0; st < nst; ++st) {
-        __syncthreads();
+    const uint32_t nst = (nrows + kBK - 1) / kBK;
+    if (nst > 0) fetch(0);
+    for (uint32_t st = 0; st < nst; ++st) {
+        lds_barrier();
 #pragma unroll
         for (int j = 0; j < 8; ++j)
             *reinterpret_cast<uint4*>(ldsA + (ka + 8 * j) * kSA + ca * 2) = va[j];
@@ -356,19 +378,27 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
                                scale_bf16x2(v.w, cw[j]));
             *reinterpret_cast<uint4*>(ldsB + (kb + 16 * j) * kSB + cb * 2) = v;
         }
-        __syncthreads();
+        lds_barrier();
         if (st + 1 < nst) fetch((st + 1) * kBK);
+        // Fragments of step kk + 1 are read while the MFMAs of step kk run.
+        uint4 fa[2][4], fb[2][2];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) fa[0][x] = frag_tr<kSA>(ldsA, 0, 128 * wm + 32 * x, lane);
+#pragma unroll
+        for (int y = 0; y < 2; ++y) fb[0][y] = frag_tr<kSB>(ldsB, 0, 64 * wn + 32 * y, lane);
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
-            uint4 fa[4], fb[2];
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk + 1 < kBK / 16) {
 #pragma unroll
-            for (int x = 0; x < 4; ++x) fa[x] = frag_tr<kSA>(ldsA, 16 * kk, 128 * wm + 32 * x, lane);
+                for (int x = 0; x < 4; ++x) fa[nxt][x] = frag_tr<kSA>(ldsA, 16 * (kk + 1), 128 * wm + 32 * x, lane);
 #pragma unroll
-            for (int y = 0; y < 2; ++y) fb[y] = frag_tr<kSB>(ldsB, 16 * kk, 64 * wn + 32 * y, lane);
+                for (int y = 0; y < 2; ++y) fb[nxt][y] = frag_tr<kSB>(ldsB, 16 * (kk + 1), 64 * wn + 32 * y, lane);
+            }
 #pragma unroll
             for (int x = 0; x < 4; ++x)
 #pragma unroll
-                for (int y = 0; y < 2; ++y) Mfma<bf16_t>::step(acc[x][y], fa[x], fb[y]);
+                for (int y = 0; y < 2; ++y) Mfma<bf16_t>::step(acc[x][y], fa[cur][x], fb[cur][y]);
         }
     }
 
@@ -377,9 +407,14 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 #pragma unroll
         for (int x = 0; x < 4; ++x)
 #pragma unroll
-            for (int y = 0; y < 2; ++y)
+            for (int y = 0; y < 2; ++y) {
+                const bool col_ok = n0 + 64 * wn + 32 * y + (lane & 31) < p;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) s += acc[x][y][i] * acc[x][y][i];
+                for (int i = 0; i < 16; ++i) {
+                    const bool ok = col_ok && (m0 + 128 * wm + 32 * x + acc_row(i, lane) < d);
+                    s += ok ? acc[x][y][i] * acc[x][y][i] : 0.f;
+                }
+            }
         const float tot = block_sum_256(s, red);
         if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
     } else {
@@ -401,13 +436,25 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 
 }  // namespace
 
-bool gemm_uses_wide_tile(bool bf16, bool vec) { return bf16 && vec; }
+int gemm_tile_m(GemmVariant v) { return v == GemmVariant::Wide ? kBM : kTile; }
+int gemm_tile_n(GemmVariant v) { return v == GemmVariant::Wide ? kBN : kTile; }
 
-hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, bool vec,
+GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned) {
+    const int64_t es = bf16 ? 2 : 4;
+    const bool vec = aligned && (d * es) % 16 == 0 && (p * es) % 16 == 0;
+    if (!vec) return GemmVariant::Scalar;
+    // The wide kernel addresses a layer's rows (plus two stages of overrun)
+    // with 32-bit buffer offsets.
+    if (bf16 && (rows + 2 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) return GemmVariant::Wide;
+    return GemmVariant::Vec;
+}
+
+hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,
                        hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
     const dim3 grid(n_wg), block(256);
-    if (gemm_uses_wide_tile(bf16, vec)) {
+    const bool vec = v != GemmVariant::Scalar;
+    if (v == GemmVariant::Wide) {
         if (inst_norm) hipLaunchKernelGGL(agemm_bf16_kernel<true>, grid, block, 0, s, args, n_wg);
         else hipLaunchKernelGGL(agemm_bf16_kernel<false>, grid, block, 0, s, args, n_wg);
         return hipGetLastError();

@@ -74,27 +74,32 @@ struct NormPlan {
     Path path;
     int64_t nwg;        // workgroups of the norm kernel
     int64_t npart;      // partials per sample
-    bool vec;           // 16-byte vector loads allowed
+    int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads;
+                        // instantiation: bk::GemmVariant
 };
+
+void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
+    const size_t es = elem_bytes(dt);
+    if (np.path == Path::Inst) {
+        const auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
+        np.var = (int)v;
+        np.npart = cdiv(L.d, bk::gemm_tile_m(v)) * cdiv(L.p, bk::gemm_tile_n(v));
+    } else {
+        const int64_t nsb = cdiv(L.T, bk::kSuper);
+        np.npart = nsb * (nsb + 1) / 2;
+        const bool xv = np.path == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
+        np.var = (xv && aligned16(L.g) && (L.p * es) % 16 == 0) ? 1 : 0;
+    }
+}
 
 NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
-    const size_t es = elem_bytes(dt);
     if (L.kind == BK_EMBEDDING) {
         np.path = Path::Embed;
     } else {
         np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
     }
-    if (np.path == Path::Inst) {
-        np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
-        const bool bf16 = dt == BK_BF16;
-        np.npart = cdiv(L.d, bk::gemm_tile_m(bf16, np.vec)) * cdiv(L.p, bk::gemm_tile_n(bf16, np.vec));
-    } else {
-        const int64_t nsb = cdiv(L.T, bk::kSuper);
-        np.npart = nsb * (nsb + 1) / 2;
-        const bool xv = np.path == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
-        np.vec = xv && aligned16(L.g) && (L.p * es) % 16 == 0;
-    }
+    set_norm_variant(np, L, dt);
     np.nwg = B * np.npart;
     return np;
 }
@@ -192,7 +197,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
         v.clear();
         return e == hipSuccess ? BK_OK : hip_fail(e, "ghost norm launch");
     };
-    auto flush_inst = [&](std::vector<const Item*>& v, bool vec) -> bk_status {
+    auto flush_inst = [&](std::vector<const Item*>& v, int var) -> bk_status {
         if (v.empty()) return BK_OK;
         bk::GemmArgs a{};
         a.n = (int32_t)v.size();
@@ -209,33 +214,33 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bf16, vec));
-            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bf16, vec));
+            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bk::GemmVariant(var)));
+            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(var)));
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
             wg += v[k]->np.nwg;
         }
         if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
-        hipError_t e = bk::launch_gemm(a, (int)wg, bf16, true, vec, s);
+        hipError_t e = bk::launch_gemm(a, (int)wg, bf16, true, bk::GemmVariant(var), s);
         v.clear();
         return e == hipSuccess ? BK_OK : hip_fail(e, "instantiated norm launch");
     };
 
-    // Group by (path, vec), preserving layer order inside a group.
+    // Group by (path, kernel variant), preserving layer order inside a group.
     for (int kind = 0; kind < 3; ++kind)
-        for (int vec = 0; vec < 2; ++vec) {
+        for (int var = 0; var < 3; ++var) {
             std::vector<const Item*> batch;
             for (const Item& it : items) {
                 const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
-                if (it.np.path != want || it.np.vec != (vec == 1) || it.np.nwg == 0) continue;
+                if (it.np.path != want || it.np.var != var || it.np.nwg == 0) continue;
                 batch.push_back(&it);
                 const size_t cap = kind == 2 ? bk::kMaxGemm : bk::kMaxGhost;
                 if (batch.size() == cap) {
-                    st = kind == 2 ? flush_inst(batch, vec) : flush_ghost(batch, kind == 1, vec);
+                    st = kind == 2 ? flush_inst(batch, var) : flush_ghost(batch, kind == 1, var == 1);
                     if (st != BK_OK) return st;
                 }
             }
-            st = kind == 2 ? flush_inst(batch, vec) : flush_ghost(batch, kind == 1, vec);
+            st = kind == 2 ? flush_inst(batch, var) : flush_ghost(batch, kind == 1, var == 1);
             if (st != BK_OK) return st;
         }
 
@@ -280,9 +285,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     if (ws_bytes < need || (need > 0 && !ws))
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
     const bool bf16 = dt == BK_BF16;
-    const size_t es = elem_bytes(dt);
 
-    for (int vec = 0; vec < 2; ++vec) {
+    for (int var = 0; var < 3; ++var) {
         bk::GemmArgs a{};
         a.B = (int32_t)B;
         a.C = C;
@@ -291,7 +295,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         auto flush = [&]() -> bk_status {
             if (a.n == 0) return BK_OK;
             if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
-            hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, vec == 1, s);
+            hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, bk::GemmVariant(var), s);
             a.n = 0;
             wg = 0;
             return e == hipSuccess ? BK_OK : hip_fail(e, "clipped gradient launch");
@@ -299,9 +303,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         for (int64_t l = 0; l < n; ++l) {
             const bk_layer& L = layers[l];
             if (L.kind != BK_LINEAR || L.d * L.p == 0) continue;
-            const bool v = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 &&
-                           (L.p * es) % 16 == 0;
-            if (v != (vec == 1)) continue;
+            const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
+            if ((int)v != var) continue;
             bk::GemmLayer& g = a.L[a.n++];
             g.a = L.x;
             g.g = L.g;
@@ -310,8 +313,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bf16, vec == 1));
-            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bf16, vec == 1));
+            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(v));
+            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(v));
             g.wg_begin = (int32_t)wg;
             g.part_off = 0;
             wg += (int64_t)g.tm * g.tn;
@@ -395,20 +398,9 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
     if (st != BK_OK) return st;
     if ((st = check_layer(fn, L, 0, B, false)) != BK_OK) return st;
     if (B > 0 && !norm_sq) return fail(BK_ERR_INVALID_VALUE, "%s: NULL norm output", fn);
-    NormPlan np = norm_plan(L, dt, B);
+    NormPlan np{};
     np.path = want;
-    if (want == Path::Inst) {
-        const size_t es = elem_bytes(dt);
-        np.vec = aligned16(L.x) && aligned16(L.g) && (L.d * es) % 16 == 0 && (L.p * es) % 16 == 0;
-        np.npart = cdiv(L.d, bk::gemm_tile_m(dt == BK_BF16, np.vec)) *
-                   cdiv(L.p, bk::gemm_tile_n(dt == BK_BF16, np.vec));
-    } else {
-        const int64_t nsb = cdiv(L.T, bk::kSuper);
-        np.npart = nsb * (nsb + 1) / 2;
-        const size_t es = elem_bytes(dt);
-        const bool xv = want == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
-        np.vec = xv && aligned16(L.g) && (L.p * es) % 16 == 0;
-    }
+    set_norm_variant(np, L, dt);
     np.nwg = B * np.npart;
     const size_t need = norm_ws_bytes(np, B);
     if (ws_bytes < need || (need > 0 && !ws))
@@ -428,9 +420,9 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.T = (int32_t)L.T;
         g.d = (int32_t)L.d;
         g.p = (int32_t)L.p;
-        g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(dt == BK_BF16, np.vec));
-        g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(dt == BK_BF16, np.vec));
-        e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, np.vec, s);
+        g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bk::GemmVariant(np.var)));
+        g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(np.var)));
+        e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, bk::GemmVariant(np.var), s);
     } else {
         bk::GhostArgs a{};
         a.n = 1;
@@ -444,7 +436,7 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.p = (int32_t)L.p;
         g.nsb = (int32_t)cdiv(L.T, bk::kSuper);
         g.npairs = (int32_t)np.npart;
-        e = bk::launch_ghost(a, (int)np.nwg, dt == BK_BF16, want == Path::Embed, np.vec, s);
+        e = bk::launch_ghost(a, (int)np.nwg, dt == BK_BF16, want == Path::Embed, np.var == 1, s);
     }
     if (e != hipSuccess) return hip_fail(e, "norm launch");
     bk::ReduceArgs r{};

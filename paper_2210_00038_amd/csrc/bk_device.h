@@ -68,6 +68,31 @@ template <> struct Mfma<float> {
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
 // ---------------------------------------------------------------------------
+// Raw buffer loads.  The resource covers [base, base + bytes); a load whose
+// offset lies outside returns zeros instead of touching memory, which replaces
+// per-load bounds branches.  All of the offset goes in the VGPR operand (the
+// range check applies to it).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup barrier for LDS producer/consumer hand-offs.  It waits for this
+// wave's LDS (and scalar) operations only, not for its global loads still in
+// flight: those write the wave's own registers, so prefetches issued before
+// the barrier stay in flight across it (__syncthreads() would drain them).
+// The "memory" clobber keeps the compiler from moving memory accesses across.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// ---------------------------------------------------------------------------
 // Reductions in a fixed order (deterministic).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {

@@ -82,16 +82,19 @@ struct NoiseArgs {
 };
 constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by one workgroup
 
-// Output tile of the a^T g GEMMs: 256 x 128 for the bf16 kernel on 16-byte
-// aligned rows, kTile x kTile otherwise.
-bool gemm_uses_wide_tile(bool bf16, bool vec);
-inline int gemm_tile_m(bool bf16, bool vec) { return gemm_uses_wide_tile(bf16, vec) ? 256 : kTile; }
-inline int gemm_tile_n(bool, bool) { return kTile; }
+// Kernel variant of the a^T g GEMMs for one layer:
+//  Scalar: element loads (rows not 16-byte multiples / unaligned), 128 x 128;
+//  Vec   : 16-byte loads, register transpose, 128 x 128 (fp32, or huge bf16);
+//  Wide  : bf16, LDS transpose reads, larger tiles.
+enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2 };
+GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
+int gemm_tile_m(GemmVariant v);
+int gemm_tile_n(GemmVariant v);
 
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
-hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, bool vec,
+hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,
                        hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& args, int n_threads, hipStream_t s);
 hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, float R, float gamma,

@@ -107,13 +107,13 @@ __device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, i
     };
     fetch(0);
     for (int ch = 0; ch < nch; ++ch) {
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             ldsR[(rq + 32 * q) * kRowU4 + c16] = pr[q];
             if (!diag) ldsC[(rq + 32 * q) * kRowU4 + c16] = pr[4 + q];
         }
-        __syncthreads();
+        lds_barrier();
         if (ch + 1 < nch) fetch(ch + 1);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
