@@ -52,7 +52,7 @@ __all__ = [
     "use_ghost", "linear_norm_sq", "linear_norm_sq_gram", "linear_norm_sq_bruteforce",
     "embed_norm_sq", "embed_norm_sq_pairs", "aggregate", "clip_factors", "weighted_grad",
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
-    "box_muller", "noise", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
+    "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
     "bk_layer_norm", "bk_stack",
 ]
 
@@ -290,6 +290,22 @@ def noise(n: int, seed: int, tensor_id: int, step: int) -> np.ndarray:
     z[:, 0], z[:, 1] = box_muller(u[:, 0], u[:, 1])
     z[:, 2], z[:, 3] = box_muller(u[:, 2], u[:, 3])
     return z.reshape(-1)[:n]
+
+
+def noise_at(elements, seed: int, tensor_id: int, step: int) -> np.ndarray:
+    """The draws of ``noise`` for the given element indices only (same layout:
+    element e uses counter block e div 4, word pair (0, 1) or (2, 3))."""
+    e = np.asarray(elements, dtype=np.uint64).ravel()
+    q = e >> np.uint64(2)
+    key = (np.uint64(seed & 0xFFFFFFFF), np.uint64((seed >> 32) & 0xFFFFFFFF))
+    w = philox4x32_10((q & _MASK32, q >> np.uint64(32), np.full_like(q, tensor_id & 0xFFFFFFFF),
+                       np.full_like(q, step & 0xFFFFFFFF)), key)
+    u = [uniforms_from_words(x) for x in w]
+    z01 = box_muller(u[0], u[1])
+    z23 = box_muller(u[2], u[3])
+    j = (e & np.uint64(3)).astype(np.int64)
+    out = np.where(j == 0, z01[0], np.where(j == 1, z01[1], np.where(j == 2, z23[0], z23[1])))
+    return out.reshape(np.shape(elements))
 
 
 def add_noise(G, std: float, seed: int, tensor_id: int, step: int) -> np.ndarray:

@@ -94,3 +94,13 @@ def test_add_noise_scale_and_zero_std():
     np.testing.assert_array_equal(oracle.add_noise(G, 0.0, 1, 0, 0), G)
     z = oracle.noise(12, 1, 0, 0).reshape(3, 4)
     np.testing.assert_allclose(oracle.add_noise(G, 0.8, 1, 0, 0), G + 0.8 * z, rtol=1e-15)
+
+
+def test_noise_at_selects_from_noise():
+    z = oracle.noise(1003, seed=77, tensor_id=5, step=2)
+    idx = np.array([[0, 1, 2, 3], [4, 999, 1002, 17]])
+    np.testing.assert_array_equal(oracle.noise_at(idx, 77, 5, 2), z[idx])
+    big = np.array([(1 << 33) + 5, 7])                   # counter blocks beyond 2^32 elements
+    w = oracle.philox_words(77, 5, 2, ((1 << 33) + 5) // 4, 1)
+    u = oracle.uniforms_from_words(w)
+    assert oracle.noise_at(big, 77, 5, 2)[0] == oracle.box_muller(u[0, 0], u[0, 1])[1]
