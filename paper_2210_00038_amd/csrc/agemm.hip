@@ -21,6 +21,7 @@
 #include "bk_kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace bk {
 namespace {
@@ -276,6 +277,15 @@ __device__ __forceinline__ uint4 frag_tr(const char* lds, int kb, int cb, int la
     return make_uint4(lo.x, lo.y, hi.x, hi.y);
 }
 
+// Half h of frag_tr: rows kb + 4 h + 8 (l >> 5) + 0..3 of the same column.
+template <int S>
+__device__ __forceinline__ uint2 frag_tr_half(const char* lds, int kb, int cb, int lane, int h) {
+    const int grp = lane >> 4, i = lane & 15;
+    const int row = kb + 8 * (grp >> 1) + (i >> 2) + 4 * h;
+    const int col = cb + 16 * (grp & 1) + 4 * (i & 3);
+    return lds_tr16(lds + row * S + col * 2);
+}
+
 // Two bf16 in one word, each multiplied by c, rounded to nearest even.
 __device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float c) {
     const f32x2_t f = {__uint_as_float(w << 16) * c, __uint_as_float(w & 0xFFFF0000u) * c};
@@ -308,7 +318,7 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     const int m0 = mt * kBM, n0 = nt * kBN;
 
     // Contraction rows: one sample's T rows (instantiation) or all B*T rows.
-    // The host guarantees (nrows + 2 kBK) * row bytes < 2^31 for this kernel.
+    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
     const int64_t row0 = INST ? (int64_t)sample * nT : 0;
     const uint32_t nrows = INST ? (uint32_t)nT : (uint32_t)args.B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
@@ -434,18 +444,206 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Clipped-gradient kernel for 16-byte aligned bf16 rows: one 256 x 256 output
+// tile per 512-thread workgroup, one workgroup per CU.  Compared with two
+// 256 x 128 workgroups on a CU, a stage moves a third fewer bytes from L2 per
+// MFMA.  Waves (wm, wn), wm in 0..1, wn in 0..3, own 128 x 64 sub-tiles (4 x 2
+// MFMA 32x32x16 accumulators), read with the same LDS transpose reads.
+//
+// Two LDS buffers: while the waves multiply stage s out of one buffer, the
+// registers holding stage s + 1 (loaded during stage s - 1) are written to the
+// other one, and the loads of stage s + 2 are issued.  One barrier per stage.
+// ---------------------------------------------------------------------------
+constexpr int kGM = 256, kGN = 256;
+constexpr int kSG = 256 * 2 + 64;                // bytes per staged k-row (both operands)
+constexpr int kGOp = kBK * kSG;                  // one operand of one stage
+constexpr int kGStage = 2 * kGOp;
+
+__global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args, int n_wg) {
+    __shared__ __attribute__((aligned(16))) char lds[2 * kGStage];
+
+    const int wg = xcd_remap(blockIdx.x, n_wg);
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const GemmLayer& L = args.L[l];
+    const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
+    const int tile = wg - L.wg_begin;
+    const int mt = tile / tn, nt = tile - mt * tn;
+    const int m0 = mt * kGM, n0 = nt * kGN;
+
+    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    const uint32_t nrows = (uint32_t)args.B * (uint32_t)nT;
+    const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(L.a, nrows * rowA);
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(L.g, nrows * rowB);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;
+    // Staging: each operand tile is 64 rows x 32 chunks of 16 B; thread t
+    // moves chunk t % 32 of rows t / 32 + 16 j, j = 0..3.  Rows past the last
+    // one fall outside the buffer resource and load as zeros, and so do
+    // chunks past the last column (out-of-range offset).
+    const int cc = (tid & 31) * 8, kr = tid >> 5;
+    const uint32_t offA = (m0 + cc < d) ? (uint32_t)kr * rowA + (uint32_t)(m0 + cc) * 2u : kOut;
+    const uint32_t offB = (n0 + cc < p) ? (uint32_t)kr * rowB + (uint32_t)(n0 + cc) * 2u : kOut;
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
+
+    // Register staging of one stage (rows [k0, k0 + 64)): chunk j of a (va)
+    // and of g (vb) for rows kr + 16 j.  Rows at or past nrows load zeros, so
+    // the stages after the last one need no branch.  The host launches this
+    // kernel only for T >= 64, so the 64 rows span at most two samples: the
+    // first `split` rows belong to sample fq, the rest to fq + 1, with clip
+    // weights c0 and c1 (loaded through the vector memory path: a scalar load
+    // would make the waits for it drain the LDS reads as well).
+    const __amdgpu_buffer_rsrc_t rC = make_rsrc(args.C, (uint32_t)args.B * 4u);
+    uint4 va[4], vb[4];
+    float c0 = 0.f, c1 = 0.f;
+    uint32_t split = 0;
+    uint32_t fk0 = 0, fq = 0, frem = 0;   // next fetch: first row, its sample, row in sample
+    auto load_a = [&](int j) { va[j] = buffer_load16(rA, offA == kOut ? kOut : offA + (fk0 + 16u * j) * rowA); };
+    auto load_b = [&](int j) { vb[j] = buffer_load16(rB, offB == kOut ? kOut : offB + (fk0 + 16u * j) * rowB); };
+    auto load_c = [&]() {
+        // Samples past B read zeros (their rows are zero too).
+        c0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rC, fq * 4u, 0, 0));
+        c1 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rC, fq * 4u + 4u, 0, 0));
+        split = (uint32_t)nT - frem;
+        fk0 += kBK;
+        frem += kBK;
+        if (frem >= (uint32_t)nT) {
+            frem -= (uint32_t)nT;
+            ++fq;
+        }
+    };
+    auto store_a = [&](char* A, int j) {
+        *reinterpret_cast<uint4*>(A + (kr + 16 * j) * kSG + cc * 2) = va[j];
+    };
+    auto store_b = [&](char* Bt, int j) {
+        const float cw = ((uint32_t)(kr + 16 * j) < split) ? c0 : c1;
+        const uint4 v = vb[j];
+        *reinterpret_cast<uint4*>(Bt + (kr + 16 * j) * kSG + cc * 2) =
+            make_uint4(scale_bf16x2(v.x, cw), scale_bf16x2(v.y, cw), scale_bf16x2(v.z, cw),
+                       scale_bf16x2(v.w, cw));
+    };
+
+    // One stage out of buffer BUF (a compile-time constant).  The issue order
+    // is laid out by hand, one slot per MFMA, each slot fenced off from the
+    // next: slot i of step kk issues MFMA (i / 2, i % 2) of step kk and its
+    // share of the 12 transpose reads of step kk + 1 (two per slot for the
+    // four a fragments, one for the halves of the two g fragments).  In step
+    // 0 slot i also writes register chunk i of stage st + 1 to the other
+    // buffer and reloads that register with stage st + 2.  The other buffer
+    // was last read in stage st - 1, which every wave finished before the
+    // barrier that ended it; after the last stage these writes go to a buffer
+    // that is never read again.
+    auto stage = [&](auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const char* A = lds + BUF * kGStage;
+        const char* Bt = A + kGOp;
+        char* An = lds + (BUF ^ 1) * kGStage;
+        char* Bn = An + kGOp;
+        uint2 fa[2][4][2], fb[2][2][2];
+        auto read = [&](int kk, int r) {          // transpose read r (0..11) of step kk
+            const int f = r >> 1, h = r & 1;
+            if (f < 4) fa[kk & 1][f][h] = frag_tr_half<kSG>(A, 16 * kk, 128 * wm + 32 * f, lane, h);
+            else fb[kk & 1][f - 4][h] = frag_tr_half<kSG>(Bt, 16 * kk, 64 * wn + 32 * (f - 4), lane, h);
+        };
+#pragma unroll
+        for (int r = 0; r < 12; ++r) read(0, r);
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            const int cur = kk & 1;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int x = i >> 1, y = i & 1;
+                const uint2 al = fa[cur][x][0], ah = fa[cur][x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
+                Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
+                if (kk + 1 < kBK / 16) {
+                    if (i < 4) {
+                        read(kk + 1, 2 * i);
+                        read(kk + 1, 2 * i + 1);
+                    } else {
+                        read(kk + 1, 4 + i);
+                    }
+                }
+                if (kk == 0) {
+                    if (i < 4) {
+                        store_a(An, i);
+                        load_a(i);
+                    } else {
+                        store_b(Bn, i - 4);
+                        load_b(i - 4);
+                        if (i == 7) load_c();
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        lds_barrier();
+    };
+
+    const uint32_t nst = (nrows + kBK - 1) / kBK;
+    if (nst > 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            load_a(j);
+            load_b(j);
+        }
+        load_c();
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            store_a(lds, j);
+            store_b(lds + kGOp, j);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            load_a(j);
+            load_b(j);
+        }
+        load_c();
+    }
+    lds_barrier();
+    uint32_t st = 0;
+    for (; st + 1 < nst; st += 2) {
+        stage(std::integral_constant<int, 0>{});
+        stage(std::integral_constant<int, 1>{});
+    }
+    if (st < nst) stage(std::integral_constant<int, 0>{});
+
+    float* G = L.G;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int n = n0 + 64 * wn + 32 * y + (lane & 31);
+            if (n >= p) continue;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
+                if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
+            }
+        }
+}
+
 }  // namespace
 
-int gemm_tile_m(GemmVariant v) { return v == GemmVariant::Wide ? kBM : kTile; }
-int gemm_tile_n(GemmVariant v) { return v == GemmVariant::Wide ? kBN : kTile; }
+int gemm_tile_m(GemmVariant v) { return v == GemmVariant::Grad ? kGM : v == GemmVariant::Wide ? kBM : kTile; }
+int gemm_tile_n(GemmVariant v) { return v == GemmVariant::Grad ? kGN : v == GemmVariant::Wide ? kBN : kTile; }
 
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned) {
     const int64_t es = bf16 ? 2 : 4;
     const bool vec = aligned && (d * es) % 16 == 0 && (p * es) % 16 == 0;
     if (!vec) return GemmVariant::Scalar;
-    // The wide kernel addresses a layer's rows (plus two stages of overrun)
+    // The wide kernels address a layer's rows (plus three stages of overrun)
     // with 32-bit buffer offsets.
-    if (bf16 && (rows + 2 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) return GemmVariant::Wide;
+    if (bf16 && (rows + 3 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) return GemmVariant::Wide;
     return GemmVariant::Vec;
 }
 
@@ -454,6 +652,11 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
     if (n_wg <= 0) return hipSuccess;
     const dim3 grid(n_wg), block(256);
     const bool vec = v != GemmVariant::Scalar;
+    if (v == GemmVariant::Grad) {
+        if (inst_norm) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(agrad_bf16_kernel, grid, dim3(512), 0, s, args, n_wg);
+        return hipGetLastError();
+    }
     if (v == GemmVariant::Wide) {
         if (inst_norm) hipLaunchKernelGGL(agemm_bf16_kernel<true>, grid, block, 0, s, args, n_wg);
         else hipLaunchKernelGGL(agemm_bf16_kernel<false>, grid, block, 0, s, args, n_wg);

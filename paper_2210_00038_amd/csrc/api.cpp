@@ -286,7 +286,13 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
     const bool bf16 = dt == BK_BF16;
 
-    for (int var = 0; var < 3; ++var) {
+    // The clipped gradient runs the Wide layers with T >= 64 on the 256 x 256
+    // kernel.
+    auto grad_variant = [&](const bk_layer& L) {
+        const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
+        return v == bk::GemmVariant::Wide && L.T >= 64 ? bk::GemmVariant::Grad : v;
+    };
+    for (int var = 0; var < 4; ++var) {
         bk::GemmArgs a{};
         a.B = (int32_t)B;
         a.C = C;
@@ -303,7 +309,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         for (int64_t l = 0; l < n; ++l) {
             const bk_layer& L = layers[l];
             if (L.kind != BK_LINEAR || L.d * L.p == 0) continue;
-            const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
+            const auto v = grad_variant(L);
             if ((int)v != var) continue;
             bk::GemmLayer& g = a.L[a.n++];
             g.a = L.x;

@@ -85,8 +85,9 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by
 // Kernel variant of the a^T g GEMMs for one layer:
 //  Scalar: element loads (rows not 16-byte multiples / unaligned), 128 x 128;
 //  Vec   : 16-byte loads, register transpose, 128 x 128 (fp32, or huge bf16);
-//  Wide  : bf16, LDS transpose reads, larger tiles.
-enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2 };
+//  Wide  : bf16, LDS transpose reads, larger tiles;
+//  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads.
+enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3 };
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
 int gemm_tile_m(GemmVariant v);
 int gemm_tile_n(GemmVariant v);
