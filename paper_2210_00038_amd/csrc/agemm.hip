@@ -454,6 +454,10 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 // Two LDS buffers: while the waves multiply stage s out of one buffer, the
 // registers holding stage s + 1 (loaded during stage s - 1) are written to the
 // other one, and the loads of stage s + 2 are issued.  One barrier per stage.
+// The instruction order inside a stage is fixed by hand (sched_barrier
+// fences): left to itself the compiler clusters the 48 transpose reads, the
+// LDS stores and the global loads into blocks, and the in-order issue of each
+// wave then leaves the MFMA pipe idle.  Only launched for T >= 64.
 // ---------------------------------------------------------------------------
 constexpr int kGM = 256, kGN = 256;
 constexpr int kSG = 256 * 2 + 64;                // bytes per staged k-row (both operands)
@@ -535,43 +539,52 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
 
     // One stage out of buffer BUF (a compile-time constant).  The issue order
     // is laid out by hand, one slot per MFMA, each slot fenced off from the
-    // next: slot i of step kk issues MFMA (i / 2, i % 2) of step kk and its
-    // share of the 12 transpose reads of step kk + 1 (two per slot for the
-    // four a fragments, one for the halves of the two g fragments).  In step
-    // 0 slot i also writes register chunk i of stage st + 1 to the other
-    // buffer and reloads that register with stage st + 2.  The other buffer
-    // was last read in stage st - 1, which every wave finished before the
-    // barrier that ended it; after the last stage these writes go to a buffer
-    // that is never read again.
+    // next: slot i of step kk issues MFMA (x, y) = (i / 2, i % 2) of step kk
+    // and its share of the 12 transpose reads of the next step: an even slot
+    // one half of a g fragment (double-buffered), an odd slot both halves of
+    // a fragment x, whose two MFMAs of this step have then been issued (one
+    // buffer).  In step 0, slot i also writes register chunk i of stage
+    // st + 1 to the other LDS buffer and reloads that register with stage
+    // st + 2.
+    //
+    // The barrier sits between steps 2 and 3: the reads of step 3 were issued
+    // (and are waited for) before it, so every read of this buffer is done
+    // before the next stage overwrites it, and the stage st + 1 data written
+    // in step 0 is complete after it, so step 3 reads the first fragments of
+    // stage st + 1 and the next stage starts with MFMAs.  (After the last
+    // stage the writes and reads go to a buffer nobody uses.)
+    uint2 fa[4][2], fb[2][2][2];
+    auto read_a = [&](const char* A, int kk, int x, int h) {
+        fa[x][h] = frag_tr_half<kSG>(A, 16 * kk, 128 * wm + 32 * x, lane, h);
+    };
+    auto read_b = [&](const char* Bt, int kk, int y, int h) {
+        fb[kk & 1][y][h] = frag_tr_half<kSG>(Bt, 16 * kk, 64 * wn + 32 * y, lane, h);
+    };
     auto stage = [&](auto buf_c) {
         constexpr int BUF = decltype(buf_c)::value;
         const char* A = lds + BUF * kGStage;
         const char* Bt = A + kGOp;
         char* An = lds + (BUF ^ 1) * kGStage;
         char* Bn = An + kGOp;
-        uint2 fa[2][4][2], fb[2][2][2];
-        auto read = [&](int kk, int r) {          // transpose read r (0..11) of step kk
-            const int f = r >> 1, h = r & 1;
-            if (f < 4) fa[kk & 1][f][h] = frag_tr_half<kSG>(A, 16 * kk, 128 * wm + 32 * f, lane, h);
-            else fb[kk & 1][f - 4][h] = frag_tr_half<kSG>(Bt, 16 * kk, 64 * wn + 32 * (f - 4), lane, h);
-        };
-#pragma unroll
-        for (int r = 0; r < 12; ++r) read(0, r);
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
             const int cur = kk & 1;
+            // Source of the reads in this step: step kk + 1 of this stage, or
+            // step 0 of the next one.
+            const char* RA = kk + 1 < kBK / 16 ? A : An;
+            const char* RB = kk + 1 < kBK / 16 ? Bt : Bn;
+            const int rk = (kk + 1) & 3;
+            if (kk == kBK / 16 - 1) lds_barrier();
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int x = i >> 1, y = i & 1;
-                const uint2 al = fa[cur][x][0], ah = fa[cur][x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
+                const uint2 al = fa[x][0], ah = fa[x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
                 Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
-                if (kk + 1 < kBK / 16) {
-                    if (i < 4) {
-                        read(kk + 1, 2 * i);
-                        read(kk + 1, 2 * i + 1);
-                    } else {
-                        read(kk + 1, 4 + i);
-                    }
+                if (i & 1) {
+                    read_a(RA, rk, x, 0);
+                    read_a(RA, rk, x, 1);
+                } else {
+                    read_b(RB, rk, i >> 2, (i >> 1) & 1);
                 }
                 if (kk == 0) {
                     if (i < 4) {
@@ -586,7 +599,6 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-        lds_barrier();
     };
 
     const uint32_t nst = (nrows + kBK - 1) / kBK;
@@ -610,6 +622,16 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
         load_c();
     }
     lds_barrier();
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        read_a(lds, 0, x, 0);
+        read_a(lds, 0, x, 1);
+    }
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+        read_b(lds + kGOp, 0, y, 0);
+        read_b(lds + kGOp, 0, y, 1);
+    }
     uint32_t st = 0;
     for (; st + 1 < nst; st += 2) {
         stage(std::integral_constant<int, 0>{});
