@@ -88,7 +88,11 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
         const int64_t nsb = cdiv(L.T, bk::kSuper);
         np.npart = nsb * (nsb + 1) / 2;
         const bool xv = np.path == Path::Embed || (aligned16(L.x) && (L.d * es) % 16 == 0);
-        np.var = (xv && aligned16(L.g) && (L.p * es) % 16 == 0) ? 1 : 0;
+        // The 16-byte path addresses one sample's rows (plus a super block of
+        // padding) with 32-bit buffer offsets.
+        const int64_t K = np.path == Path::Embed ? L.p : std::max(L.d, L.p);
+        const bool fits = (L.T + bk::kSuper) * K * (int64_t)es < ((int64_t)1 << 31);
+        np.var = (xv && fits && aligned16(L.g) && (L.p * es) % 16 == 0) ? 1 : 0;
     }
 }
 

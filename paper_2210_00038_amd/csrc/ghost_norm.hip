@@ -13,9 +13,12 @@
 // chunks and accumulates its part of a_i a_i^T with 32x32 MFMA tiles, then does
 // the same for g_i, and finally multiplies the two accumulators elementwise
 // and reduces.  The Grams never leave the registers.  Inside a diagonal super
-// block only the 10 upper 32x32 sub-tiles are formed (diagonal ones weight 1,
-// others 2); sub-tiles made only of padding rows (t >= T) are skipped.  Each
-// workgroup writes one partial sum; a fixed-order reduction finishes the norm.
+// block only the 10 upper 32x32 sub-tiles count (diagonal ones weight 1,
+// others 2); sub-tiles made only of padding rows (t >= T) get weight 0.  A
+// wave multiplies all four of its sub-tiles whatever their weights (a branch
+// around each MFMA costs more than the MFMA), except that a wave with no
+// weighted sub-tile skips its MFMAs.  Each workgroup writes one partial sum;
+// a fixed-order reduction finishes the norm.
 #include "bk_device.h"
 #include "bk_kernels.h"
 
@@ -23,6 +26,7 @@ namespace bk {
 namespace {
 
 constexpr int kRowU4 = 9;                    // LDS row: 128 data bytes + 16 pad, in uint4
+constexpr uint32_t kGhostOut = 0xFFFFFFF0u;  // buffer offset that loads zeros
 constexpr int kBlockU4 = kSuper * kRowU4;    // one staged super block
 
 struct WaveTiles {
@@ -40,12 +44,12 @@ __device__ __forceinline__ WaveTiles wave_tiles(int wave, bool diag) {
     }
     // Upper triangle of the 4 x 4 sub-tiles of a diagonal super block:
     // wave 0: (0,0) (0,1) (1,1); wave 1: (2,2) (2,3) (3,3);
-    // wave 2: (0,2) (1,2);       wave 3: (0,3) (1,3).
+    // wave 2: (0,2) (0,3) (1,2) (1,3); wave 3: none.
     switch (wave) {
         case 0: t.r0 = 0; t.c0 = 0; t.w[0] = 1; t.w[1] = 2; t.w[2] = 0; t.w[3] = 1; break;
         case 1: t.r0 = 2; t.c0 = 2; t.w[0] = 1; t.w[1] = 2; t.w[2] = 0; t.w[3] = 1; break;
-        case 2: t.r0 = 0; t.c0 = 2; t.w[0] = 2; t.w[1] = 0; t.w[2] = 2; t.w[3] = 0; break;
-        default: t.r0 = 0; t.c0 = 2; t.w[0] = 0; t.w[1] = 2; t.w[2] = 0; t.w[3] = 2; break;
+        case 2: t.r0 = 0; t.c0 = 2; t.w[0] = 2; t.w[1] = 2; t.w[2] = 2; t.w[3] = 2; break;
+        default: t.r0 = 0; t.c0 = 2; t.w[0] = 0; t.w[1] = 0; t.w[2] = 0; t.w[3] = 0; break;
     }
     return t;
 }
@@ -115,6 +119,7 @@ __device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, i
         }
         lds_barrier();
         if (ch + 1 < nch) fetch(ch + 1);
+        if ((wt.w[0] | wt.w[1] | wt.w[2] | wt.w[3]) == 0) continue;   // wave-uniform
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int col = 2 * j + h;
@@ -122,17 +127,144 @@ __device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, i
             const uint4 x1 = ldsR[((wt.r0 + 1) * 32 + r) * kRowU4 + col];
             const uint4 y0 = ldsC[((wt.c0 + 0) * 32 + r) * kRowU4 + col];
             const uint4 y1 = ldsC[((wt.c0 + 1) * 32 + r) * kRowU4 + col];
-            if (wt.w[0]) Mfma<T>::step(acc[0], x0, y0);
-            if (wt.w[1]) Mfma<T>::step(acc[1], x0, y1);
-            if (wt.w[2]) Mfma<T>::step(acc[2], x1, y0);
-            if (wt.w[3]) Mfma<T>::step(acc[3], x1, y1);
+            // All four sub-tiles, also those of weight 0 (their rows are real
+            // or zero padding, so the product is finite and gets weight 0):
+            // a branch per MFMA costs more than the MFMA.
+            Mfma<T>::step(acc[0], x0, y0);
+            Mfma<T>::step(acc[1], x0, y1);
+            Mfma<T>::step(acc[2], x1, y0);
+            Mfma<T>::step(acc[3], x1, y1);
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Direct-to-LDS variant of gram() for 16-byte aligned rows (VEC).  The chunks
+// go from global memory straight into a ring of four 16 KB LDS slots (one
+// 128-row x 128-byte block each; a diagonal pair needs one slot per chunk, an
+// off-diagonal pair two), with no staging registers, so up to three chunks per
+// workgroup are in flight.  A 1 KB load instruction fills 8 consecutive
+// 128-byte rows, so rows cannot be padded; instead the 16-byte column c of row
+// r is stored at column c ^ ((r >> 1) & 7), which spreads the 16 rows read by
+// 16 lanes of a fragment load over all 64 banks.
+// ---------------------------------------------------------------------------
+constexpr int kRing = 4;                     // LDS slots
+constexpr int kSlotBytes = kSuper * 128;     // one 128-row x 128-byte block
+
+__device__ __forceinline__ int swz(int row, int col16) { return col16 ^ ((row >> 1) & 7); }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 16, "vmcnt immediate");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <typename T, bool DIAG>
+__device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
+                                        const WaveTiles& wt, f32x16_t acc[4], char* __restrict__ lds) {
+    constexpr int EPV = Elem<T>::per16;       // elements per 16 bytes
+    constexpr int EPC = 8 * EPV;              // elements per 128-byte chunk
+    constexpr int SPC = DIAG ? 1 : 2;         // slots per chunk
+    constexpr int NCH = kRing / SPC;          // chunks held by the ring
+    constexpr int LPW = 4 * SPC;              // 1 KB loads per wave per chunk
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[s][i] = 0.f;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 31, h = lane >> 5;
+    const int nch = (K + EPC - 1) / EPC;
+    const uint32_t rowbytes = (uint32_t)K * (uint32_t)sizeof(T);
+    // The host guarantees rows * rowbytes < 2^31 for this path.
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(X, (uint32_t)rows * rowbytes);
+
+    // Load i (0..3) of this wave for one block fills rows 8 (4 i + wave) + 0..7
+    // of the slot; lane l writes 16-byte column l % 8 of row l / 8, which
+    // holds column swz(row, l % 8) of the chunk.
+    uint32_t roff[4];
+    int lcol[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rl = 8 * (4 * i + wave) + (lane >> 3);
+        lcol[i] = swz(rl, lane & 7);
+        roff[i] = (uint32_t)rl * rowbytes + (uint32_t)(lcol[i] * EPV) * (uint32_t)sizeof(T);
+    }
+    // Chunks at or past nch load zeros (all offsets out of range), so every
+    // iteration issues the same number of loads.
+    auto issue = [&](int ch) {
+        char* slot = lds + ((ch % NCH) * SPC) * kSlotBytes;
+#pragma unroll
+        for (int b = 0; b < SPC; ++b) {
+            const uint32_t base = (uint32_t)(b == 0 ? rowR : rowC) * rowbytes +
+                                  (uint32_t)(ch * EPC) * (uint32_t)sizeof(T);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bool ok = ch * EPC + lcol[i] * EPV < K;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rs, (__attribute__((address_space(3))) void*)(slot + b * kSlotBytes + (4 * i + wave) * 1024),
+                    16, ok ? base + roff[i] : kGhostOut, 0, 0, 0);
+            }
+        }
+    };
+    const bool active = (wt.w[0] | wt.w[1] | wt.w[2] | wt.w[3]) != 0;   // wave-uniform
+    auto compute = [&](int ch) {
+        if (!active) return;
+        const char* sR = lds + ((ch % NCH) * SPC) * kSlotBytes;
+        const char* sC = DIAG ? sR : sR + kSlotBytes;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = 2 * j + h;
+            const int ra0 = (wt.r0 + 0) * 32 + r, ra1 = (wt.r0 + 1) * 32 + r;
+            const int rc0 = (wt.c0 + 0) * 32 + r, rc1 = (wt.c0 + 1) * 32 + r;
+            const uint4 x0 = *reinterpret_cast<const uint4*>(sR + ra0 * 128 + swz(ra0, col) * 16);
+            const uint4 x1 = *reinterpret_cast<const uint4*>(sR + ra1 * 128 + swz(ra1, col) * 16);
+            const uint4 y0 = *reinterpret_cast<const uint4*>(sC + rc0 * 128 + swz(rc0, col) * 16);
+            const uint4 y1 = *reinterpret_cast<const uint4*>(sC + rc1 * 128 + swz(rc1, col) * 16);
+            // All four sub-tiles, also those of weight 0 (their rows are real
+            // or zero padding, so the product is finite and gets weight 0):
+            // a branch per MFMA costs more than the MFMA.
+            Mfma<T>::step(acc[0], x0, y0);
+            Mfma<T>::step(acc[1], x0, y1);
+            Mfma<T>::step(acc[2], x1, y0);
+            Mfma<T>::step(acc[3], x1, y1);
+        }
+    };
+
+    // Chunk ch: wait for this wave's loads of it (the NCH - 2 later chunks may
+    // stay in flight), barrier (everyone's loads of it have landed, and every
+    // wave is done with chunk ch - 1), refill chunk ch - 1's slot with chunk
+    // ch + NCH - 1, multiply chunk ch.
+#pragma unroll
+    for (int c = 0; c < NCH - 1; ++c) issue(c);
+    for (int ch = 0; ch < nch; ++ch) {
+        wait_vmcnt<LPW * (NCH - 2)>();
+        lds_barrier();
+        issue(ch + NCH - 1);
+        compute(ch);
+    }
+    // Drain the loads past the end and let every wave finish reading before
+    // the ring is reused.
+    wait_vmcnt<0>();
+    lds_barrier();
+}
+
+template <typename T, bool VEC>
+__device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
+                                         bool diag, const WaveTiles& wt, f32x16_t acc[4], char* smem) {
+    if constexpr (VEC) {
+        if (diag) gram_dl<T, true>(X, rows, K, rowR, rowC, wt, acc, smem);
+        else gram_dl<T, false>(X, rows, K, rowR, rowC, wt, acc, smem);
+    } else {
+        gram<T, VEC>(X, rows, K, rowR, rowC, diag, wt, acc, reinterpret_cast<uint4*>(smem));
     }
 }
 
 template <typename T, bool EMBED, bool VEC>
 __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
-    __shared__ uint4 lds[2 * kBlockU4];
+    // VEC: the ring of gram_dl; otherwise two padded blocks for gram.
+    __shared__ __attribute__((aligned(16))) char smem[VEC ? kRing * kSlotBytes : 2 * kBlockU4 * 16];
+    uint4* lds = reinterpret_cast<uint4*>(smem);
     __shared__ int64_t sid[2 * kSuper];
     __shared__ float red[4];
 
@@ -150,7 +282,7 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     const bool diag = (R == C);
     const int rowR = R * kSuper, rowC = C * kSuper;
 
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     WaveTiles wt = wave_tiles(wave, diag);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -166,7 +298,7 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
         const int t = threadIdx.x;
         const int row = (t < kSuper) ? rowR + t : rowC + (t - kSuper);
         sid[t] = (row < nT) ? ids[row] : (int64_t)-1;
-        gram<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, lds);
+        gram_any<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, smem);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             if (!wt.w[s]) continue;
@@ -182,8 +314,8 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     } else {
         f32x16_t accA[4];
         const size_t off_a = (size_t)sample * (size_t)nT * (size_t)d;
-        gram<T, VEC>(reinterpret_cast<const T*>(L.x) + off_a, nT, d, rowR, rowC, diag, wt, accA, lds);
-        gram<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, lds);
+        gram_any<T, VEC>(reinterpret_cast<const T*>(L.x) + off_a, nT, d, rowR, rowC, diag, wt, accA, smem);
+        gram_any<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, smem);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             if (!wt.w[s]) continue;
