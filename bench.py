@@ -101,7 +101,7 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = {"agemm_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+KERNEL_SOURCES = {"agrad_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip"}
 
 
@@ -228,9 +228,9 @@ def main():
     # Dominant kernel: the phase with the most time among the two big ones.
     if phases["weighted_grads"]["ms"] >= phases["norms"]["ms"]:
         ach = phases["weighted_grads"]["tflops"]
-        roof = {"kernel": "agemm_bf16_kernel (clip-weighted gradient, all layers in one launch)",
+        roof = {"kernel": "agrad_bf16_kernel (clip-weighted gradient, all layers in one launch)",
                 "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                "frac": ach / peak_mfma, "traffic": measured_traffic("agemm_bf16_kernel", w.name),
+                "frac": ach / peak_mfma, "traffic": measured_traffic("agrad_bf16_kernel", w.name),
                 "per_launch": f"{work['gemm_flops'] / 1e9:.1f} GFLOP (sum over layers of 2 B T d p)"}
     elif work["norm_flops"] / max(work["norm_bytes"], 1.0) > peak_mfma * 1e3 / PEAK_HBM_GBS:
         # above the ridge point (long sequences): the norm kernels are MFMA-bound

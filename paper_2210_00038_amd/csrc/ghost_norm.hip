@@ -148,10 +148,10 @@ __device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, i
 // r is stored at column c ^ ((r >> 1) & 7), which spreads the 16 rows read by
 // 16 lanes of a fragment load over all 64 banks.
 // ---------------------------------------------------------------------------
-constexpr int kRing = 4;                     // LDS slots
-constexpr int kSlotBytes = kSuper * 128;     // one 128-row x 128-byte block
-
-__device__ __forceinline__ int swz(int row, int col16) { return col16 ^ ((row >> 1) & 7); }
+constexpr int kRingBytes = 64 * 1024;        // LDS ring of gram_dl
+#ifndef BK_GHOST_DIAG_CW
+#define BK_GHOST_DIAG_CW 256
+#endif
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -159,14 +159,27 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <typename T, bool DIAG>
+// CW: bytes of each row per chunk (128 or 256).  A slot holds one 128-row
+// block of a chunk; the ring holds kRingBytes / (128 CW) slots.  Column c of
+// row r sits at column c ^ (r / 2 mod 8) (CW = 128: a 256-byte bank line
+// holds two rows) or c ^ (r mod 16) (CW = 256), so that the 16 rows read by
+// 16 lanes land on distinct 16-byte bank groups.
+template <typename T, bool DIAG, int CW>
 __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
                                         const WaveTiles& wt, f32x16_t acc[4], char* __restrict__ lds) {
+    static_assert(CW == 128 || CW == 256, "chunk width");
     constexpr int EPV = Elem<T>::per16;       // elements per 16 bytes
-    constexpr int EPC = 8 * EPV;              // elements per 128-byte chunk
+    constexpr int C16 = CW / 16;              // 16-byte columns per row and chunk
+    constexpr int EPC = C16 * EPV;            // elements per row and chunk
+    constexpr int SLOT = kSuper * CW;         // bytes of one block of one chunk
+    constexpr int NSLOT = kRingBytes / SLOT;
     constexpr int SPC = DIAG ? 1 : 2;         // slots per chunk
-    constexpr int NCH = kRing / SPC;          // chunks held by the ring
-    constexpr int LPW = 4 * SPC;              // 1 KB loads per wave per chunk
+    constexpr int NCH = NSLOT / SPC;          // chunks held by the ring
+    static_assert(NCH >= 2, "ring too small");
+    constexpr int RPL = 64 / C16;             // rows filled by one 1 KB load
+    constexpr int LPB = kSuper / RPL / 4;     // loads per wave per block
+    constexpr int LPW = LPB * SPC;            // loads per wave per chunk
+    auto swz = [](int row, int c) { return C16 == 8 ? c ^ ((row >> 1) & 7) : c ^ (row & 15); };
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -176,33 +189,33 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
     const int r = lane & 31, h = lane >> 5;
     const int nch = (K + EPC - 1) / EPC;
     const uint32_t rowbytes = (uint32_t)K * (uint32_t)sizeof(T);
-    // The host guarantees rows * rowbytes < 2^31 for this path.
+    // The host guarantees (rows + 128) * rowbytes < 2^31 for this path.
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(X, (uint32_t)rows * rowbytes);
 
-    // Load i (0..3) of this wave for one block fills rows 8 (4 i + wave) + 0..7
-    // of the slot; lane l writes 16-byte column l % 8 of row l / 8, which
-    // holds column swz(row, l % 8) of the chunk.
-    uint32_t roff[4];
-    int lcol[4];
+    // Load i of this wave for one block fills rows RPL (4 i + wave) + 0..RPL-1
+    // of the slot; lane l writes 16-byte column l % C16 of row l / C16, which
+    // holds column swz(row, l % C16) of the chunk.
+    uint32_t roff[LPB];
+    int lcol[LPB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int rl = 8 * (4 * i + wave) + (lane >> 3);
-        lcol[i] = swz(rl, lane & 7);
+    for (int i = 0; i < LPB; ++i) {
+        const int rl = RPL * (4 * i + wave) + lane / C16;
+        lcol[i] = swz(rl, lane % C16);
         roff[i] = (uint32_t)rl * rowbytes + (uint32_t)(lcol[i] * EPV) * (uint32_t)sizeof(T);
     }
     // Chunks at or past nch load zeros (all offsets out of range), so every
     // iteration issues the same number of loads.
     auto issue = [&](int ch) {
-        char* slot = lds + ((ch % NCH) * SPC) * kSlotBytes;
+        char* slot = lds + ((ch % NCH) * SPC) * SLOT;
 #pragma unroll
         for (int b = 0; b < SPC; ++b) {
             const uint32_t base = (uint32_t)(b == 0 ? rowR : rowC) * rowbytes +
                                   (uint32_t)(ch * EPC) * (uint32_t)sizeof(T);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < LPB; ++i) {
                 const bool ok = ch * EPC + lcol[i] * EPV < K;
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rs, (__attribute__((address_space(3))) void*)(slot + b * kSlotBytes + (4 * i + wave) * 1024),
+                    rs, (__attribute__((address_space(3))) void*)(slot + b * SLOT + (4 * i + wave) * 1024),
                     16, ok ? base + roff[i] : kGhostOut, 0, 0, 0);
             }
         }
@@ -210,17 +223,17 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
     const bool active = (wt.w[0] | wt.w[1] | wt.w[2] | wt.w[3]) != 0;   // wave-uniform
     auto compute = [&](int ch) {
         if (!active) return;
-        const char* sR = lds + ((ch % NCH) * SPC) * kSlotBytes;
-        const char* sC = DIAG ? sR : sR + kSlotBytes;
+        const char* sR = lds + ((ch % NCH) * SPC) * SLOT;
+        const char* sC = DIAG ? sR : sR + SLOT;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < C16 / 2; ++j) {
             const int col = 2 * j + h;
             const int ra0 = (wt.r0 + 0) * 32 + r, ra1 = (wt.r0 + 1) * 32 + r;
             const int rc0 = (wt.c0 + 0) * 32 + r, rc1 = (wt.c0 + 1) * 32 + r;
-            const uint4 x0 = *reinterpret_cast<const uint4*>(sR + ra0 * 128 + swz(ra0, col) * 16);
-            const uint4 x1 = *reinterpret_cast<const uint4*>(sR + ra1 * 128 + swz(ra1, col) * 16);
-            const uint4 y0 = *reinterpret_cast<const uint4*>(sC + rc0 * 128 + swz(rc0, col) * 16);
-            const uint4 y1 = *reinterpret_cast<const uint4*>(sC + rc1 * 128 + swz(rc1, col) * 16);
+            const uint4 x0 = *reinterpret_cast<const uint4*>(sR + ra0 * CW + swz(ra0, col) * 16);
+            const uint4 x1 = *reinterpret_cast<const uint4*>(sR + ra1 * CW + swz(ra1, col) * 16);
+            const uint4 y0 = *reinterpret_cast<const uint4*>(sC + rc0 * CW + swz(rc0, col) * 16);
+            const uint4 y1 = *reinterpret_cast<const uint4*>(sC + rc1 * CW + swz(rc1, col) * 16);
             // All four sub-tiles, also those of weight 0 (their rows are real
             // or zero padding, so the product is finite and gets weight 0):
             // a branch per MFMA costs more than the MFMA.
@@ -253,8 +266,8 @@ template <typename T, bool VEC>
 __device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
                                          bool diag, const WaveTiles& wt, f32x16_t acc[4], char* smem) {
     if constexpr (VEC) {
-        if (diag) gram_dl<T, true>(X, rows, K, rowR, rowC, wt, acc, smem);
-        else gram_dl<T, false>(X, rows, K, rowR, rowC, wt, acc, smem);
+        if (diag) gram_dl<T, true, BK_GHOST_DIAG_CW>(X, rows, K, rowR, rowC, wt, acc, smem);
+        else gram_dl<T, false, 128>(X, rows, K, rowR, rowC, wt, acc, smem);
     } else {
         gram<T, VEC>(X, rows, K, rowR, rowC, diag, wt, acc, reinterpret_cast<uint4*>(smem));
     }
@@ -263,7 +276,7 @@ __device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int 
 template <typename T, bool EMBED, bool VEC>
 __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     // VEC: the ring of gram_dl; otherwise two padded blocks for gram.
-    __shared__ __attribute__((aligned(16))) char smem[VEC ? kRing * kSlotBytes : 2 * kBlockU4 * 16];
+    __shared__ __attribute__((aligned(16))) char smem[VEC ? kRingBytes : 2 * kBlockU4 * 16];
     uint4* lds = reinterpret_cast<uint4*>(smem);
     __shared__ int64_t sid[2 * kSuper];
     __shared__ float red[4];
