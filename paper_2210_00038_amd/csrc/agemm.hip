@@ -654,10 +654,275 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
         }
 }
 
+// ---------------------------------------------------------------------------
+// Clipped-gradient kernel for bf16 rows when 64 divides T: the tiles, waves,
+// stages and hand-laid issue order of agrad_bf16_kernel, but both operand
+// tiles go from HBM straight into LDS (LDS DMA: no staging registers, no LDS
+// store instructions) and the clip weights are applied to the accumulators
+// instead of to g.  A 64-row stage then lies inside one sample.  The
+// accumulators hold S / c, S being the weighted sum so far and c the weight
+// of the last sample whose weight is nonzero: entering sample j with
+// C_j != 0 multiplies them by c / C_j, and the epilogue multiplies by the
+// final c.  Rows of samples with C_j = 0 load as zeros.  (Products are exact
+// in fp32 and each sample boundary rounds once, instead of C_j g being
+// rounded to bf16.)
+//
+// LDS: two buffers of an a stage and a g stage, 512-byte rows without
+// padding (one DMA instruction fills 1 KB contiguously); the 16-byte column c
+// of row r sits at c ^ 4 (r mod 4), which puts the four rows that each half
+// of a transpose read touches on distinct bank groups.  The clip weights of
+// the batch sit in LDS after the buffers (B <= kDMaxB).
+// ---------------------------------------------------------------------------
+constexpr int kDRow = 512;                       // bytes per staged k-row
+constexpr int kDOp = kBK * kDRow;                // one operand of one stage
+constexpr int kDStage = 2 * kDOp;
+
+__device__ __forceinline__ int dswz(int row, int c16) { return c16 ^ (4 * (row & 3)); }
+
+// Half h of a transposed fragment (as frag_tr_half) from the swizzled layout.
+__device__ __forceinline__ uint2 frag_dl_half(const char* lds, int kb, int cb, int lane, int h) {
+    const int grp = lane >> 4, i = lane & 15;
+    const int row = kb + 8 * (grp >> 1) + (i >> 2) + 4 * h;
+    const int col = cb + 16 * (grp & 1) + 4 * (i & 3);
+    return lds_tr16(lds + row * kDRow + dswz(row, col >> 3) * 16 + (col & 7) * 2);
+}
+
+// LDS DMA of 16 bytes per lane (as buffer_load16_lds), issued from inline
+// assembly.  The compiler treats the LDS transpose reads as possibly reading
+// any LDS DMA destination and would wait for every DMA in flight before each
+// of them, which serialises the prefetch; hidden in assembly, the DMA is not
+// tracked, and the kernel waits for it itself (vmcnt) before the barrier that
+// publishes a stage.  rs: buffer descriptor words (base, base high, bytes,
+// flags); m0 takes the wave-uniform LDS destination.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return (u32x4_t){(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, bytes, 0x00020000u};
+}
+
+__device__ __forceinline__ void dma16_asm(const u32x4_t& rs, uint32_t off, char* lds_dst) {
+    const uint32_t m0v = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_dst;
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :: "v"(off), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(m0v)) : "memory", "m0");
+}
+
+// Position of a stage in the batch: its sample and its stage within the
+// sample (spt stages per sample), advanced one stage at a time.
+struct StagePos {
+    uint32_t smp, in;
+    __device__ __forceinline__ void next(uint32_t spt) {
+        const bool wrap = in + 1u == spt;
+        in = wrap ? 0u : in + 1u;
+        smp += wrap ? 1u : 0u;
+    }
+};
+
+__global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, int n_wg) {
+    __shared__ __attribute__((aligned(16))) char lds[2 * kDStage];
+    __shared__ float ctab[kDMaxB + 1];
+
+    const int wg = xcd_remap(blockIdx.x, n_wg);
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const GemmLayer& L = args.L[l];
+    const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
+    const int tile = wg - L.wg_begin;
+    const int mt = tile / tn, nt = tile - mt * tn;
+    const int m0 = mt * kGM, n0 = nt * kGN;
+
+    // The host guarantees T % 64 == 0, B <= kDMaxB and
+    // (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    const int B = args.B;
+    const uint32_t nrows = (uint32_t)B * (uint32_t)nT;
+    const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
+    const u32x4_t rA = raw_rsrc(L.a, nrows * rowA);
+    const u32x4_t rB = raw_rsrc(L.g, nrows * rowB);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2, wn = wave & 3;
+    // Clip weights, and a zero for the stages past the batch.
+    for (int i = tid; i <= B; i += 512) ctab[i] = i < B ? args.C[i] : 0.f;
+
+    // DMA: each operand stage is 32 instructions of 1 KB (two rows); wave w
+    // (of 8) issues numbers j = 8 i + w, i = 0..3, and lane l moves physical
+    // column l % 32 of row 2 j + l / 32, i.e. logical column dswz(row, l % 32).
+    // Columns past the matrix get an out-of-range offset (zeros).
+    uint32_t offA[4], offB[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = 2 * (8 * i + wave) + (lane >> 5);
+        const int lc = dswz(row, lane & 31);
+        offA[i] = (m0 + 8 * lc < d) ? (uint32_t)row * rowA + (uint32_t)(m0 + 8 * lc) * 2u : kOut;
+        offB[i] = (n0 + 8 * lc < p) ? (uint32_t)row * rowB + (uint32_t)(n0 + 8 * lc) * 2u : kOut;
+    }
+    // DMA piece i (0..3: a, 4..7: g) of the stage starting at row k0 into
+    // buffer `buf`; `zero` (the stage's sample has weight 0) loads zeros.
+    auto dma = [&](char* buf, uint32_t k0, bool zero, int i) {
+        if (i < 4) {
+            const uint32_t o = (offA[i] == kOut || zero) ? kOut : offA[i] + k0 * rowA;
+            dma16_asm(rA, o, buf + (8 * i + wave) * 1024);
+        } else {
+            const int j = i - 4;
+            const uint32_t o = (offB[j] == kOut || zero) ? kOut : offB[j] + k0 * rowB;
+            dma16_asm(rB, o, buf + kDOp + (8 * j + wave) * 1024);
+        }
+    };
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
+
+    const uint32_t nst = (nrows + kBK - 1) / kBK;
+    const uint32_t spt = (uint32_t)nT / kBK;             // stages per sample
+    // Weight of the stage at `pos` (0 past the batch).
+    auto cw_of = [&](const StagePos& pos) { return ctab[min(pos.smp, (uint32_t)B)]; };
+
+    uint2 fa[4][2], fb[2][2][2];
+    auto read_a = [&](const char* A, int kk, int x, int h) {
+        fa[x][h] = frag_dl_half(A, 16 * kk, 128 * wm + 32 * x, lane, h);
+    };
+    auto read_b = [&](const char* Bt, int kk, int y, int h) {
+        fb[kk & 1][y][h] = frag_dl_half(Bt, 16 * kk, 64 * wn + 32 * y, lane, h);
+    };
+
+    float c_last = 0.f;   // weight of the last sample with a nonzero weight
+    // Stage st out of buffer BUF.  Slot i of step kk issues MFMA (i / 2,
+    // i % 2) and its share of the next step's transpose reads (as in
+    // agrad_bf16_kernel).  The barrier sits between steps 2 and 3: every wave
+    // has then finished reading this buffer and waited for its DMA of stage
+    // st + 1, so step 3 reads the first fragments of stage st + 1 and its
+    // slots refill this buffer with stage st + 2, one DMA instruction each.
+    // The weights needed next (stage st + 1 for the rescale, st + 2 for the
+    // zero test) are read from LDS in step 0.
+    // pos1 / pos2: positions of stages st + 1 and st + 2.
+    StagePos pos1{0u, 0u}, pos2{0u, 0u};
+    auto stage = [&](auto buf_c, uint32_t st) {
+        constexpr int BUF = decltype(buf_c)::value;
+        char* A = lds + BUF * kDStage;
+        char* Bt = A + kDOp;
+        const char* An = lds + (BUF ^ 1) * kDStage;
+        const char* Bn = An + kDOp;
+        float c_next = 0.f, c_dma = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            const int cur = kk & 1;
+            const char* RA = kk + 1 < kBK / 16 ? A : An;
+            const char* RB = kk + 1 < kBK / 16 ? Bt : Bn;
+            const int rk = (kk + 1) & 3;
+            if (kk == kBK / 16 - 1) {
+                wait_vmcnt<0>();
+                lds_barrier();
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int x = i >> 1, y = i & 1;
+                const uint2 al = fa[x][0], ah = fa[x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
+                Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
+                if (i & 1) {
+                    read_a(RA, rk, x, 0);
+                    read_a(RA, rk, x, 1);
+                } else {
+                    read_b(RB, rk, i >> 2, (i >> 1) & 1);
+                }
+                if (kk == 0 && i == 0) {
+                    c_next = cw_of(pos1);
+                    c_dma = cw_of(pos2);
+                }
+                if (kk == kBK / 16 - 1) dma(A, (st + 2) * kBK, c_dma == 0.f, i);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        pos1.next(spt);
+        pos2.next(spt);
+        return c_next;
+    };
+    // Entering a stage with weight c; `first`: it starts a sample.  (The test
+    // on `first` is uniform: a scalar branch; the one on c is a select.)
+    auto enter = [&](bool first, float c) {
+        if (!first) return;
+        const bool nz = c != 0.f;
+        const float r = nz ? c_last / c : 1.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc[x][y][i] *= r;
+        c_last = nz ? c : c_last;
+    };
+
+    __syncthreads();      // clip weights in LDS
+    float c_cur = 0.f;
+    StagePos pos0{0u, 0u};                 // stage st
+    pos1 = pos0;
+    pos1.next(spt);
+    pos2 = pos1;
+    pos2.next(spt);
+    if (nst > 0) {
+        const float c0 = cw_of(pos0), c1 = cw_of(pos1);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dma(lds, 0, c0 == 0.f, i);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dma(lds + kDStage, kBK, c1 == 0.f, i);
+        c_cur = c0;
+        wait_vmcnt<0>();
+    }
+    lds_barrier();
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+        read_a(lds, 0, x, 0);
+        read_a(lds, 0, x, 1);
+    }
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+        read_b(lds + kDOp, 0, y, 0);
+        read_b(lds + kDOp, 0, y, 1);
+    }
+    uint32_t st = 0;
+    for (; st + 1 < nst; st += 2) {
+        enter(pos0.in == 0u, c_cur);
+        c_cur = stage(std::integral_constant<int, 0>{}, st);
+        pos0.next(spt);
+        enter(pos0.in == 0u, c_cur);
+        c_cur = stage(std::integral_constant<int, 1>{}, st + 1);
+        pos0.next(spt);
+    }
+    if (st < nst) {
+        enter(pos0.in == 0u, c_cur);
+        stage(std::integral_constant<int, 0>{}, st);
+    }
+    // Drain the DMA past the end before the workgroup exits.
+    wait_vmcnt<0>();
+
+    float* G = L.G;
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int n = n0 + 64 * wn + 32 * y + (lane & 31);
+            if (n >= p) continue;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
+                if (m < d) G[(size_t)m * p + n] = acc[x][y][i] * c_last;
+            }
+        }
+}
+
 }  // namespace
 
-int gemm_tile_m(GemmVariant v) { return v == GemmVariant::Grad ? kGM : v == GemmVariant::Wide ? kBM : kTile; }
-int gemm_tile_n(GemmVariant v) { return v == GemmVariant::Grad ? kGN : v == GemmVariant::Wide ? kBN : kTile; }
+int gemm_tile_m(GemmVariant v) {
+    return (v == GemmVariant::Grad || v == GemmVariant::GradDL) ? kGM : v == GemmVariant::Wide ? kBM : kTile;
+}
+int gemm_tile_n(GemmVariant v) {
+    return (v == GemmVariant::Grad || v == GemmVariant::GradDL) ? kGN : v == GemmVariant::Wide ? kBN : kTile;
+}
 
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned) {
     const int64_t es = bf16 ? 2 : 4;
@@ -677,6 +942,11 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
     if (v == GemmVariant::Grad) {
         if (inst_norm) return hipErrorInvalidValue;
         hipLaunchKernelGGL(agrad_bf16_kernel, grid, dim3(512), 0, s, args, n_wg);
+        return hipGetLastError();
+    }
+    if (v == GemmVariant::GradDL) {
+        if (inst_norm) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(agrad_dl_kernel, grid, dim3(512), 0, s, args, n_wg);
         return hipGetLastError();
     }
     if (v == GemmVariant::Wide) {

@@ -92,6 +92,21 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N of this wave's vector-memory operations (loads,
+// including loads into LDS) are outstanding.  They complete in order.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 16, "vmcnt immediate");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Global -> LDS copy of 16 bytes per lane (LDS DMA): lane l's bytes land at
+// lds_dst + 16 l, lds_dst being the same for the whole wave.  The offset is
+// range-checked like buffer_load16 (zeros outside the resource).
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, uint32_t off, void* lds_dst) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_dst, 16, off, 0, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // Reductions in a fixed order (deterministic).
 // ---------------------------------------------------------------------------

@@ -86,8 +86,11 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by
 //  Scalar: element loads (rows not 16-byte multiples / unaligned), 128 x 128;
 //  Vec   : 16-byte loads, register transpose, 128 x 128 (fp32, or huge bf16);
 //  Wide  : bf16, LDS transpose reads, larger tiles;
-//  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads.
-enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3 };
+//  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads (T >= 64);
+//  GradDL: as Grad with LDS DMA and the weights on the accumulators
+//          (64 divides T, B <= kDMaxB).
+enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4 };
+constexpr int kDMaxB = 4096;
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
 int gemm_tile_m(GemmVariant v);
 int gemm_tile_n(GemmVariant v);

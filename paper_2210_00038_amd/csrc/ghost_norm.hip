@@ -153,12 +153,6 @@ constexpr int kRingBytes = 64 * 1024;        // LDS ring of gram_dl
 #define BK_GHOST_DIAG_CW 256
 #endif
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 16, "vmcnt immediate");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
 // CW: bytes of each row per chunk (128 or 256).  A slot holds one 128-row
 // block of a chunk; the ring holds kRingBytes / (128 CW) slots.  Column c of
 // row r sits at column c ^ (r / 2 mod 8) (CW = 128: a 256-byte bank line
@@ -214,9 +208,7 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
 #pragma unroll
             for (int i = 0; i < LPB; ++i) {
                 const bool ok = ch * EPC + lcol[i] * EPV < K;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rs, (__attribute__((address_space(3))) void*)(slot + b * SLOT + (4 * i + wave) * 1024),
-                    16, ok ? base + roff[i] : kGhostOut, 0, 0, 0);
+                buffer_load16_lds(rs, ok ? base + roff[i] : kGhostOut, slot + b * SLOT + (4 * i + wave) * 1024);
             }
         }
     };

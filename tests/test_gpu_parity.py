@@ -149,6 +149,30 @@ def test_weighted_grad_matches_oracle(bk, B, T, d, p, dtype):
     assert _frob(G1, oracle.weighted_grad(a, g, np.ones(B))) <= GRAD_TOL[dtype]
 
 
+# bf16 layers whose T is a multiple of 64 take the kernel that applies the
+# clip weights to its accumulators (rescaled at each sample boundary, rows of
+# zero-weight samples loaded as zeros); these cases exercise its boundaries.
+@pytest.mark.parametrize("B,T,d,p,C", [
+    (1, 64, 256, 256, [0.7]),                          # a single stage
+    (3, 128, 300, 520, [0.3, 2.0, 0.05]),              # ragged tiles, two stages per sample
+    (5, 192, 264, 136, [0.0, 1.5, 0.0, 1e-3, 4.0]),    # zero weights first and inside, odd stage count
+    (4, 64, 512, 256, [1e3, 1e-3, 0.0, 0.0]),          # weights six decades apart, zeros at the end
+    (2, 64, 64, 64, [0.0, 0.0]),                       # every weight zero
+])
+def test_weighted_grad_sample_weights(bk, B, T, d, p, C):
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=5 + T + B)
+    C = torch.tensor(C, dtype=torch.float32)
+    ref = oracle.weighted_grad(a, g, C)
+    G = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), C.to(DEV)).cpu().numpy()
+    assert np.all(np.isfinite(G))
+    if not np.any(ref):
+        assert not np.any(G)
+    else:
+        err = _frob(G, ref)
+        print(f"weighted grad (sample weights) frob err {err:.2e}")
+        assert err <= GRAD_TOL[torch.bfloat16]
+
+
 @pytest.mark.parametrize("B,T,V,p,dtype", [(3, 40, 17, 24, torch.float32), (16, 256, 50257, 64, torch.bfloat16)])
 def test_embed_weighted_grad_matches_oracle(bk, B, T, V, p, dtype):
     ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.1, 99)).view(B, T)
