@@ -674,8 +674,13 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
 // the batch sit in LDS after the buffers (B <= kDMaxB).
 // ---------------------------------------------------------------------------
 constexpr int kDRow = 512;                       // bytes per staged k-row
-constexpr int kDOp = kBK * kDRow;                // one operand of one stage
-constexpr int kDStage = 2 * kDOp;
+constexpr int kDKS = kDLStageRows;               // k rows per stage
+constexpr int kDNB = kDLBuffers;                 // LDS stage buffers
+static_assert(kDKS == 32 || kDKS == 64, "stage rows");
+static_assert(kDNB >= 2 && kDNB * 2 * kDKS * kDRow <= 128 * 1024, "LDS ring");
+// Loads run up to NB + 1 stages past the last row; the Wide/Grad condition
+// (rows + 3 kBK) * row bytes < 2^31 covers that.
+static_assert((kDNB + 1) * kDKS <= 3 * kBK, "overrun bound");
 
 __device__ __forceinline__ int dswz(int row, int c16) { return c16 ^ (4 * (row & 3)); }
 
@@ -718,8 +723,37 @@ struct StagePos {
     }
 };
 
+// ---------------------------------------------------------------------------
+// Clipped-gradient kernel for bf16 rows when the stage height KS (32) divides
+// T: 256 x 256 tiles on 512 threads, waves of 128 x 64 as in
+// agrad_bf16_kernel, but both operand tiles go from HBM straight into LDS
+// (LDS DMA: no staging registers, no LDS store instructions) and the clip
+// weights are applied to the accumulators instead of to g.  A stage then lies
+// inside one sample.  The accumulators hold S / c, S being the weighted sum
+// so far and c the weight of the last sample whose weight is nonzero:
+// entering sample j with C_j != 0 multiplies them by c / C_j, and the
+// epilogue multiplies by the final c.  Rows of samples with C_j = 0 load as
+// zeros.  (Products are exact in fp32 and each sample boundary rounds once,
+// instead of C_j g being rounded to bf16.)
+//
+// LDS: a ring of NB stage buffers (an a stage and a g stage each), 512-byte
+// rows without padding (one DMA instruction fills 1 KB contiguously); the
+// 16-byte column c of row r sits at c ^ 4 (r mod 4), which puts the four rows
+// that each half of a transpose read touches on distinct bank groups.  One
+// barrier per stage, before its last 16-row step: by then every wave has read
+// all of the stage's fragments (so its buffer is refilled right after, with
+// stage s + NB) and has waited for its own DMA of stage s + 1 (so the last
+// step reads the first fragments of stage s + 1).  A stage's loads thus have
+// NB - 1 stages to land.  The clip weights of the batch sit in LDS after the
+// ring (B <= kDMaxB).
+// ---------------------------------------------------------------------------
+constexpr int kDOp = kDKS * kDRow;               // one operand of one stage
+constexpr int kDStage = 2 * kDOp;
+constexpr int kDKK = kDKS / 16;                  // 16-row MFMA steps per stage
+constexpr int kDPW = kDKS / 8;                   // DMA instructions per wave per stage
+
 __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, int n_wg) {
-    __shared__ __attribute__((aligned(16))) char lds[2 * kDStage];
+    __shared__ __attribute__((aligned(16))) char lds[kDNB * kDStage];
     __shared__ float ctab[kDMaxB + 1];
 
     const int wg = xcd_remap(blockIdx.x, n_wg);
@@ -731,8 +765,8 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
-    // The host guarantees T % 64 == 0, B <= kDMaxB and
-    // (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    // The host guarantees KS | T, B <= kDMaxB and
+    // (nrows + (NB + 1) KS) * row bytes < 2^31 for this kernel.
     const int B = args.B;
     const uint32_t nrows = (uint32_t)B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
@@ -745,26 +779,27 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // Clip weights, and a zero for the stages past the batch.
     for (int i = tid; i <= B; i += 512) ctab[i] = i < B ? args.C[i] : 0.f;
 
-    // DMA: each operand stage is 32 instructions of 1 KB (two rows); wave w
-    // (of 8) issues numbers j = 8 i + w, i = 0..3, and lane l moves physical
-    // column l % 32 of row 2 j + l / 32, i.e. logical column dswz(row, l % 32).
-    // Columns past the matrix get an out-of-range offset (zeros).
-    uint32_t offA[4], offB[4];
+    // DMA: each operand stage is KS / 2 instructions of 1 KB (two rows); wave
+    // w (of 8) issues numbers j = 8 i + w, i < KS / 16, and lane l moves
+    // physical column l % 32 of row 2 j + l / 32, i.e. logical column
+    // dswz(row, l % 32).  Columns past the matrix get an out-of-range offset.
+    constexpr int NI = kDKS / 16;
+    uint32_t offA[NI], offB[NI];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NI; ++i) {
         const int row = 2 * (8 * i + wave) + (lane >> 5);
         const int lc = dswz(row, lane & 31);
         offA[i] = (m0 + 8 * lc < d) ? (uint32_t)row * rowA + (uint32_t)(m0 + 8 * lc) * 2u : kOut;
         offB[i] = (n0 + 8 * lc < p) ? (uint32_t)row * rowB + (uint32_t)(n0 + 8 * lc) * 2u : kOut;
     }
-    // DMA piece i (0..3: a, 4..7: g) of the stage starting at row k0 into
-    // buffer `buf`; `zero` (the stage's sample has weight 0) loads zeros.
+    // DMA piece i (i < NI: a, else g) of the stage starting at row k0 into
+    // the buffer at `buf`; `zero` (the stage's sample has weight 0) loads zeros.
     auto dma = [&](char* buf, uint32_t k0, bool zero, int i) {
-        if (i < 4) {
+        if (i < NI) {
             const uint32_t o = (offA[i] == kOut || zero) ? kOut : offA[i] + k0 * rowA;
             dma16_asm(rA, o, buf + (8 * i + wave) * 1024);
         } else {
-            const int j = i - 4;
+            const int j = i - NI;
             const uint32_t o = (offB[j] == kOut || zero) ? kOut : offB[j] + k0 * rowB;
             dma16_asm(rB, o, buf + kDOp + (8 * j + wave) * 1024);
         }
@@ -778,45 +813,43 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
 
-    const uint32_t nst = (nrows + kBK - 1) / kBK;
-    const uint32_t spt = (uint32_t)nT / kBK;             // stages per sample
+    const uint32_t nst = (nrows + kDKS - 1) / kDKS;
+    const uint32_t spt = (uint32_t)nT / kDKS;            // stages per sample
     // Weight of the stage at `pos` (0 past the batch).
     auto cw_of = [&](const StagePos& pos) { return ctab[min(pos.smp, (uint32_t)B)]; };
 
     uint2 fa[4][2], fb[2][2][2];
     auto read_a = [&](const char* A, int kk, int x, int h) {
-        fa[x][h] = frag_dl_half(A, 16 * kk, 128 * wm + 32 * x, lane, h);
+        fa[x][h] = frag_dl_half(A, 16 * (kk % kDKK), 128 * wm + 32 * x, lane, h);
     };
     auto read_b = [&](const char* Bt, int kk, int y, int h) {
-        fb[kk & 1][y][h] = frag_dl_half(Bt, 16 * kk, 64 * wn + 32 * y, lane, h);
+        fb[kk & 1][y][h] = frag_dl_half(Bt, 16 * (kk % kDKK), 64 * wn + 32 * y, lane, h);
     };
 
     float c_last = 0.f;   // weight of the last sample with a nonzero weight
+    // Positions of stages st + 1 (its weight: the rescale on entering it) and
+    // st + NB (its weight: the zero test of its DMA).
+    StagePos pos1{0u, 0u}, posN{0u, 0u};
     // Stage st out of buffer BUF.  Slot i of step kk issues MFMA (i / 2,
-    // i % 2) and its share of the next step's transpose reads (as in
-    // agrad_bf16_kernel).  The barrier sits between steps 2 and 3: every wave
-    // has then finished reading this buffer and waited for its DMA of stage
-    // st + 1, so step 3 reads the first fragments of stage st + 1 and its
-    // slots refill this buffer with stage st + 2, one DMA instruction each.
-    // The weights needed next (stage st + 1 for the rescale, st + 2 for the
-    // zero test) are read from LDS in step 0.
-    // pos1 / pos2: positions of stages st + 1 and st + 2.
-    StagePos pos1{0u, 0u}, pos2{0u, 0u};
+    // i % 2) of step kk and its share of the next step's transpose reads (an
+    // even slot one half of a g fragment, double-buffered; an odd slot both
+    // halves of a fragment, whose two MFMAs of this step have then been
+    // issued).  After the barrier, the first slots of the last step refill
+    // this buffer with stage st + NB, one DMA instruction each.
     auto stage = [&](auto buf_c, uint32_t st) {
         constexpr int BUF = decltype(buf_c)::value;
         char* A = lds + BUF * kDStage;
         char* Bt = A + kDOp;
-        const char* An = lds + (BUF ^ 1) * kDStage;
+        const char* An = lds + ((BUF + 1) % kDNB) * kDStage;
         const char* Bn = An + kDOp;
         float c_next = 0.f, c_dma = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
+        for (int kk = 0; kk < kDKK; ++kk) {
             const int cur = kk & 1;
-            const char* RA = kk + 1 < kBK / 16 ? A : An;
-            const char* RB = kk + 1 < kBK / 16 ? Bt : Bn;
-            const int rk = (kk + 1) & 3;
-            if (kk == kBK / 16 - 1) {
-                wait_vmcnt<0>();
+            const char* RA = kk + 1 < kDKK ? A : An;
+            const char* RB = kk + 1 < kDKK ? Bt : Bn;
+            if (kk == kDKK - 1) {
+                wait_vmcnt<(kDNB - 2) * kDPW>();
                 lds_barrier();
             }
 #pragma unroll
@@ -825,21 +858,21 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
                 const uint2 al = fa[x][0], ah = fa[x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
                 Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
                 if (i & 1) {
-                    read_a(RA, rk, x, 0);
-                    read_a(RA, rk, x, 1);
+                    read_a(RA, kk + 1, x, 0);
+                    read_a(RA, kk + 1, x, 1);
                 } else {
-                    read_b(RB, rk, i >> 2, (i >> 1) & 1);
+                    read_b(RB, kk + 1, i >> 2, (i >> 1) & 1);
                 }
                 if (kk == 0 && i == 0) {
                     c_next = cw_of(pos1);
-                    c_dma = cw_of(pos2);
+                    c_dma = cw_of(posN);
                 }
-                if (kk == kBK / 16 - 1) dma(A, (st + 2) * kBK, c_dma == 0.f, i);
+                if (kk == kDKK - 1 && i < kDPW) dma(A, (st + kDNB) * kDKS, c_dma == 0.f, i);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
         pos1.next(spt);
-        pos2.next(spt);
+        posN.next(spt);
         return c_next;
     };
     // Entering a stage with weight c; `first`: it starts a sample.  (The test
@@ -862,17 +895,20 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     StagePos pos0{0u, 0u};                 // stage st
     pos1 = pos0;
     pos1.next(spt);
-    pos2 = pos1;
-    pos2.next(spt);
-    if (nst > 0) {
-        const float c0 = cw_of(pos0), c1 = cw_of(pos1);
+    // Prologue: stages 0 .. NB - 1 into the NB buffers.
+    {
+        StagePos q = pos0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) dma(lds, 0, c0 == 0.f, i);
+        for (int b = 0; b < kDNB; ++b) {
+            const bool z = cw_of(q) == 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) dma(lds + kDStage, kBK, c1 == 0.f, i);
-        c_cur = c0;
-        wait_vmcnt<0>();
+            for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (uint32_t)b * kDKS, z, i);
+            q.next(spt);
+        }
+        posN = q;
     }
+    c_cur = cw_of(pos0);
+    wait_vmcnt<(kDNB - 1) * kDPW>();
     lds_barrier();
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
@@ -884,19 +920,22 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         read_b(lds + kDOp, 0, y, 0);
         read_b(lds + kDOp, 0, y, 1);
     }
+    auto run = [&](auto buf_c, uint32_t st) {
+        enter(pos0.in == 0u, c_cur);
+        c_cur = stage(buf_c, st);
+        pos0.next(spt);
+    };
     uint32_t st = 0;
-    for (; st + 1 < nst; st += 2) {
-        enter(pos0.in == 0u, c_cur);
-        c_cur = stage(std::integral_constant<int, 0>{}, st);
-        pos0.next(spt);
-        enter(pos0.in == 0u, c_cur);
-        c_cur = stage(std::integral_constant<int, 1>{}, st + 1);
-        pos0.next(spt);
+    for (; st + kDNB <= nst; st += kDNB) {
+        run(std::integral_constant<int, 0>{}, st);
+        run(std::integral_constant<int, 1>{}, st + 1);
+        if constexpr (kDNB > 2) run(std::integral_constant<int, 2 % kDNB>{}, st + 2);
+        if constexpr (kDNB > 3) run(std::integral_constant<int, 3 % kDNB>{}, st + 3);
     }
-    if (st < nst) {
-        enter(pos0.in == 0u, c_cur);
-        stage(std::integral_constant<int, 0>{}, st);
-    }
+    static_assert(kDNB <= 4, "ring unroll");
+    if (st < nst) run(std::integral_constant<int, 0>{}, st++);
+    if (kDNB > 2 && st < nst) run(std::integral_constant<int, 1>{}, st++);
+    if (kDNB > 3 && st < nst) run(std::integral_constant<int, 2 % kDNB>{}, st++);
     // Drain the DMA past the end before the workgroup exits.
     wait_vmcnt<0>();
 

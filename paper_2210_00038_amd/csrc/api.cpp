@@ -291,12 +291,13 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     const bool bf16 = dt == BK_BF16;
 
     // The clipped gradient runs the Wide layers with T >= 64 on the 256 x 256
-    // kernels: with the weights on the accumulators when 64 divides T (and B
-    // fits the kernel's LDS table), else on g.
+    // kernels: with the weights on the accumulators when the stage height
+    // divides T (and B fits the kernel's LDS table), else on g.
     auto grad_variant = [&](const bk_layer& L) {
         const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
         if (v != bk::GemmVariant::Wide || L.T < 64) return v;
-        return (L.T % 64 == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL : bk::GemmVariant::Grad;
+        return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL
+                                                                 : bk::GemmVariant::Grad;
     };
     for (int var = 0; var < 5; ++var) {
         bk::GemmArgs a{};

@@ -88,9 +88,17 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by
 //  Wide  : bf16, LDS transpose reads, larger tiles;
 //  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads (T >= 64);
 //  GradDL: as Grad with LDS DMA and the weights on the accumulators
-//          (64 divides T, B <= kDMaxB).
+//          (kDLStageRows divides T, B <= kDMaxB).
 enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4 };
 constexpr int kDMaxB = 4096;
+#ifndef BK_DL_KS
+#define BK_DL_KS 32
+#endif
+#ifndef BK_DL_NB
+#define BK_DL_NB 4
+#endif
+constexpr int kDLStageRows = BK_DL_KS;   // k rows per stage of the GradDL kernel
+constexpr int kDLBuffers = BK_DL_NB;     // its LDS stage buffers
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
 int gemm_tile_m(GemmVariant v);
 int gemm_tile_n(GemmVariant v);
