@@ -27,6 +27,12 @@ What is computed, and where the paper defines it
 * weighted_grad         -- Algorithm 1, sum of clipped gradients
                            a^T diag(C) dL/ds (App. B.3 with the clip weights).
 * embed_weighted_grad   -- the same for an embedding layer.
+* per_sample_grads      -- the instantiated per-sample gradients a_i^T g_i
+                           (App. B.4.1), kept by BK-MixOpt on the layers that
+                           instantiate (Section 3.2; Algorithm "BKAL-mixed").
+* weighted_sum          -- sum_i C_i (a_i^T g_i) from stored per-sample
+                           gradients (App. B.5), BK-MixOpt's clipped gradient
+                           on those layers.
 * philox4x32_10 / noise -- Algorithm 1, Gaussian noise sigma R N(0, I).  The
                            paper does not fix a generator; the reading used
                            here is Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
@@ -53,7 +59,7 @@ __all__ = [
     "embed_norm_sq", "embed_norm_sq_pairs", "aggregate", "clip_factors", "weighted_grad",
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
     "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
-    "bk_layer_norm", "bk_stack",
+    "bk_layer_norm", "bk_stack", "per_sample_grads", "weighted_sum",
 ]
 
 F64 = np.float64
@@ -204,6 +210,28 @@ def weighted_grad(a, g, C) -> np.ndarray:
     return a.reshape(B * T, d).T @ (c_row[:, None] * g.reshape(B * T, p))
 
 
+def per_sample_grads(a, g) -> np.ndarray:
+    """dL_i/dW = a_i^T g_i for every sample  (a: [B,T,d], g: [B,T,p]) -> [B, d, p]."""
+    a = _f64(a)
+    g = _f64(g)
+    B, T, d = a.shape
+    p = g.shape[2]
+    P = np.zeros((B, d, p), dtype=F64)
+    for i in range(B):
+        P[i] = a[i].T @ g[i]
+    return P
+
+
+def weighted_sum(P, C) -> np.ndarray:
+    """sum_i C_i P_i over stored per-sample gradients P [B, d, p] -> [d, p]."""
+    P = _f64(P)
+    C = _f64(C)
+    G = np.zeros(P.shape[1:], dtype=F64)
+    for i in range(P.shape[0]):
+        G += C[i] * P[i]
+    return G
+
+
 def embed_weighted_grad(ids, g, C, V: int) -> np.ndarray:
     """G[v, :] = sum_i C_i sum_{t: x_it = v} g_it  -> [V, p] (every row present)."""
     ids = _ids(ids)
@@ -325,17 +353,25 @@ def bk_layer_norm(layer_kind: str, x, g, V: int = 0) -> np.ndarray:
 
 
 def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed: int,
-             step: int = 0, with_noise: bool = True):
+             step: int = 0, with_noise: bool = True, mixopt: bool = False):
     """layers: objects with .kind, .T, .d, .p; inputs: list of (a or ids, g).
 
     Returns dict with per-layer norms [L, B], totals [B], C [B], the clipped
-    gradients G_l (before noise) and, if with_noise, G_hat_l with tensor_id = l."""
+    gradients G_l (before noise) and, if with_noise, G_hat_l with tensor_id = l.
+    mixopt: BK-MixOpt -- a linear layer that instantiates (2 T^2 >= p d) keeps
+    its per-sample gradients and forms G_l as their weighted sum (App. B.5);
+    every other layer takes the book-keeping GEMM a^T diag(C) g."""
     norms = np.stack([bk_layer_norm(L.kind, x, g, L.d) for L, (x, g) in zip(layers, inputs)])
     total = aggregate(norms)
     C = clip_factors(total, mode, R, gamma)
     G, Ghat = [], []
     for l, (L, (x, g)) in enumerate(zip(layers, inputs)):
-        Gl = embed_weighted_grad(x, g, C, L.d) if L.kind == "embed" else weighted_grad(x, g, C)
+        if L.kind == "embed":
+            Gl = embed_weighted_grad(x, g, C, L.d)
+        elif mixopt and not use_ghost(L.T, L.d, L.p):
+            Gl = weighted_sum(per_sample_grads(x, g), C)
+        else:
+            Gl = weighted_grad(x, g, C)
         G.append(Gl)
         if with_noise:
             Ghat.append(add_noise(Gl, std, seed, l, step))

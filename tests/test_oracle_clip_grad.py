@@ -109,3 +109,52 @@ def test_stack_composes_the_steps():
                                rtol=1e-12)
     assert out["paths"] == ["ghost" if 2 * 25 < 12 else "inst", "inst", "embed"]
     assert len(out["Ghat"]) == 3 and out["Ghat"][2].shape == (10, 3)
+
+
+# --- BK-MixOpt: stored per-sample gradients and their weighted sum (App. B.4.1, B.5) ---
+
+def test_per_sample_grads_hand_example():
+    # one token: a_1 = (1, 2), g_1 = (3): the per-sample gradient is the outer product
+    P = oracle.per_sample_grads(np.array([[[1.0, 2.0]]]), np.array([[[3.0]]]))
+    np.testing.assert_array_equal(P, [[[3.0], [6.0]]])
+    # two tokens add: a = [(1,0),(0,1)], g = [(1,1),(2,-1)] -> [[1,1],[2,-1]]
+    P = oracle.per_sample_grads(np.array([[[1.0, 0.0], [0.0, 1.0]]]), np.array([[[1.0, 1.0], [2.0, -1.0]]]))
+    np.testing.assert_array_equal(P, [[[1.0, 1.0], [2.0, -1.0]]])
+
+
+def test_per_sample_grad_norms_match_ghost_form():
+    a, g = _rand(4, 7, 5), _rand(4, 7, 3)
+    P = oracle.per_sample_grads(a, g)
+    np.testing.assert_allclose((P ** 2).sum(axis=(1, 2)), oracle.linear_norm_sq_gram(a, g), rtol=1e-12)
+
+
+def test_weighted_sum_equals_book_keeping_gemm():
+    # sum_i C_i (a_i^T g_i) is the same matrix as a^T diag(C) g over the flattened rows
+    a, g, C = _rand(5, 6, 4), _rand(5, 6, 7), np.abs(_rand(5))
+    np.testing.assert_allclose(oracle.weighted_sum(oracle.per_sample_grads(a, g), C),
+                               oracle.weighted_grad(a, g, C), rtol=1e-12, atol=1e-12)
+
+
+def test_weighted_sum_selects_and_is_linear():
+    P = _rand(4, 3, 2)
+    for j in range(4):
+        e = np.zeros(4)
+        e[j] = 1.0
+        np.testing.assert_array_equal(oracle.weighted_sum(P, e), P[j])
+    C1, C2 = _rand(4), _rand(4)
+    np.testing.assert_allclose(oracle.weighted_sum(P, C1 + 2 * C2),
+                               oracle.weighted_sum(P, C1) + 2 * oracle.weighted_sum(P, C2), rtol=1e-12, atol=1e-12)
+
+
+def test_mixopt_stack_matches_base_stack():
+    # BK-MixOpt changes how G_l is formed on instantiated layers, not its value
+    class L:
+        def __init__(self, kind, T, d, p):
+            self.kind, self.T, self.d, self.p = kind, T, d, p
+    layers = [L("linear", 6, 3, 4), L("linear", 2, 5, 4)]          # instantiate (72 >= 12), ghost (8 < 20)
+    ins = [(_rand(3, 6, 3), _rand(3, 6, 4)), (_rand(3, 2, 5), _rand(3, 2, 4))]
+    base = oracle.bk_stack(layers, ins, "abadi", 1.0, 0.0, 0.0, 1, with_noise=False)
+    mix = oracle.bk_stack(layers, ins, "abadi", 1.0, 0.0, 0.0, 1, with_noise=False, mixopt=True)
+    assert base["paths"] == ["inst", "ghost"]
+    for gb, gm in zip(base["G"], mix["G"]):
+        np.testing.assert_allclose(gm, gb, rtol=1e-12, atol=1e-12)
