@@ -75,18 +75,30 @@ typedef enum { BK_CLIP_ABADI = 0, BK_CLIP_AUTO = 1 } bk_clip;
 
 typedef enum { BK_LINEAR = 0, BK_EMBEDDING = 1 } bk_layer_kind;
 
+/* Layer flags (bk_layer.flags).
+ *   BK_LAYER_MIXOPT: BK-MixOpt (Section 3.2; the MixOpt branch of Algorithm
+ *   "BKAL-mixed").  A linear layer that instantiates its per-sample gradients
+ *   for the norm (bk_use_ghost == 0) keeps them in P, and its clipped gradient
+ *   is their weighted sum sum_i C_i P_i (App. B.5) instead of the GEMM
+ *   a^T diag(C) g.  Ghost-norm and embedding layers ignore the flag. */
+enum { BK_LAYER_MIXOPT = 1 };
+
 /* One generalized linear layer of a stack (used by the grouped calls).
  *   kind == BK_LINEAR   : x = a [B, T, d] of dtype dt, g [B, T, p], G [d, p]
  *   kind == BK_EMBEDDING: x = token ids int64 [B, T] (values in [0, d)),
  *                         d = vocabulary size V, g [B, T, p], G [V, p]
- * G may be NULL in calls that only compute norms. */
+ * G may be NULL in calls that only compute norms.  P (device, float32
+ * [B, d, p]) is used only by a BK_LAYER_MIXOPT linear layer that
+ * instantiates: bk_layer_norms writes the per-sample gradients there and
+ * bk_weighted_grads of the same step reads them; otherwise it may be NULL. */
 typedef struct bk_layer {
     int32_t kind;
-    int32_t reserved;        /* must be 0 */
+    int32_t flags;           /* 0 or BK_LAYER_MIXOPT */
     int64_t T, d, p;
     const void* x;
     const void* g;
     float* G;
+    float* P;
 } bk_layer;
 
 /* Operation ids for bk_workspace_size. */
@@ -130,6 +142,22 @@ bk_status bk_inst_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int
                        int64_t d, int64_t p, float* norm_sq, void* ws, size_t ws_bytes,
                        void* stream);
 
+/* The same instantiation keeping the per-sample gradients (BK-MixOpt,
+ * App. B.4.1): P[i] = a_i^T g_i, P [B, d, p] float32 out (device), and
+ * norm_sq[i] = ||P[i]||_F^2.  Other arguments and the workspace as
+ * bk_inst_norm (bk_workspace_size(BK_OP_INST_NORM, ...)). */
+bk_status bk_per_sample_grads(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T,
+                              int64_t d, int64_t p, float* norm_sq, float* P, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Weighted sum of stored per-sample gradients (App. B.5), BK-MixOpt's
+ * clipped gradient on an instantiated layer:
+ *   G[e] = sum_i C[i] P[i n + e]   for e in [0, n), i ascending, float32
+ * (one fused multiply-add per sample).  P [B, n], C [B], G [n] float32
+ * (device); B = 0 writes zeros.  Needs no workspace. */
+bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, float* G,
+                          void* stream);
+
 /* Ghost norm of an embedding layer (Section 2.1 names the embedding among the
  * generalized linear layers; App. D.1 lists it as ghost-norm only).  Its input
  * a_i is the one-hot encoding of the ids x_i, so a_i a_i^T is the token-id
@@ -150,8 +178,10 @@ bk_status bk_clip_factors(const float* norm_sq, int64_t L, int64_t B, bk_clip mo
 
 /* Algorithm 1, sum of clipped gradients (App. B.3 with the clip weights):
  *   G = a^T diag(C) g = sum_i C_i a_i^T g_i,   G [d,p] float32 out,
- * one GEMM over the flattened B*T rows, C_i applied to the rows of g as they
- * are loaded (for bf16 the product C_i g is rounded to bf16 before the MFMA). */
+ * one GEMM over the flattened B*T rows.  For bf16 layers with 16-byte rows
+ * and 32 | T the weights multiply the float32 accumulators (each GEMM stage
+ * lies inside one sample); otherwise C_i multiplies the rows of g as they are
+ * loaded (for bf16 the product C_i g is rounded to bf16 before the MFMA). */
 bk_status bk_weighted_grad(const void* a, const void* g, const float* C, bk_dtype dt,
                            int64_t B, int64_t T, int64_t d, int64_t p, float* G, void* ws,
                            size_t ws_bytes, void* stream);
@@ -200,7 +230,8 @@ size_t bk_layer_norms_workspace_size(const bk_layer* layers, int64_t n, bk_dtype
 bk_status bk_layer_norms(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
                          float* norm_sq, void* ws, size_t ws_bytes, void* stream);
 
-/* Clipped gradients of every layer into layers[l].G. */
+/* Clipped gradients of every layer into layers[l].G (BK_LAYER_MIXOPT
+ * instantiated layers: the weighted sum of their P). */
 size_t bk_weighted_grads_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
                                         int64_t B);
 bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, bk_dtype dt,

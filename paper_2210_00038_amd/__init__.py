@@ -21,10 +21,11 @@ import torch
 
 __all__ = [
     "BK_OK", "BK_ERR_INVALID_VALUE", "BK_ERR_NOT_SUPPORTED", "BK_ERR_WORKSPACE", "BK_ERR_LAUNCH",
-    "BK_F32", "BK_BF16", "BK_CLIP_ABADI", "BK_CLIP_AUTO", "BK_LINEAR", "BK_EMBEDDING",
+    "BK_F32", "BK_BF16", "BK_CLIP_ABADI", "BK_CLIP_AUTO", "BK_LINEAR", "BK_EMBEDDING", "BK_LAYER_MIXOPT",
     "BK_OP_GHOST_NORM", "BK_OP_INST_NORM", "BK_OP_EMBED_GHOST_NORM", "BK_OP_WEIGHTED_GRAD",
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
+    "bk_per_sample_grads", "bk_weighted_sum",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
     "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
     "bk_layer_norms_workspace_size", "bk_weighted_grads_workspace_size",
@@ -35,6 +36,7 @@ BK_OK, BK_ERR_INVALID_VALUE, BK_ERR_NOT_SUPPORTED, BK_ERR_WORKSPACE, BK_ERR_LAUN
 BK_F32, BK_BF16 = 0, 1
 BK_CLIP_ABADI, BK_CLIP_AUTO = 0, 1
 BK_LINEAR, BK_EMBEDDING = 0, 1
+BK_LAYER_MIXOPT = 1
 (BK_OP_GHOST_NORM, BK_OP_INST_NORM, BK_OP_EMBED_GHOST_NORM, BK_OP_WEIGHTED_GRAD,
  BK_OP_EMBED_WEIGHTED_GRAD) = range(5)
 
@@ -43,6 +45,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbk.so")
 # Every symbol include/bk.h declares.
 EXPORTS = (
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
+    "bk_per_sample_grads", "bk_weighted_sum",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
     "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
     "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_status_string",
@@ -58,9 +61,9 @@ class BKError(RuntimeError):
 
 class bk_layer(ctypes.Structure):
     """Mirror of ``struct bk_layer`` in include/bk.h."""
-    _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32), ("T", ctypes.c_int64),
+    _fields_ = [("kind", ctypes.c_int32), ("flags", ctypes.c_int32), ("T", ctypes.c_int64),
                 ("d", ctypes.c_int64), ("p", ctypes.c_int64), ("x", ctypes.c_void_p),
-                ("g", ctypes.c_void_p), ("G", ctypes.c_void_p)]
+                ("g", ctypes.c_void_p), ("G", ctypes.c_void_p), ("P", ctypes.c_void_p)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -78,6 +81,9 @@ _SIG = {
     "bk_ghost_norm": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_inst_norm": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_embed_ghost_norm": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
+    "bk_per_sample_grads": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
+                                  _vp]),
+    "bk_weighted_sum": (_st, [_vp, _vp, _i64, _i64, _vp, _vp]),
     "bk_clip_factors": (_st, [_vp, _i64, _i64, ctypes.c_int, _f32, _f32, _vp, _vp, _vp]),
     "bk_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_embed_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp,
@@ -207,6 +213,36 @@ def bk_inst_norm(a, g, norm_sq=None, ws=None, stream=None) -> torch.Tensor:
     return _linear_norm("bk_inst_norm", BK_OP_INST_NORM, a, g, norm_sq, ws, stream)
 
 
+def bk_per_sample_grads(a, g, norm_sq=None, P=None, ws=None, stream=None):
+    """(norm_sq [B], P [B,d,p]): per-sample gradients a_i^T g_i kept (BK-MixOpt, App. B.4.1)."""
+    _dev(a, "a"), _dev(g, "g")
+    if a.dim() != 3 or g.dim() != 3 or a.shape[:2] != g.shape[:2] or a.dtype != g.dtype:
+        raise ValueError("a must be [B,T,d] and g [B,T,p] of one dtype")
+    B, T, d = a.shape
+    p = g.shape[2]
+    dt = _dtype_code(a)
+    norm_sq = _out(norm_sq, (B,), a.device)
+    P = _out(P, (B, d, p), a.device)
+    ws, nws = _workspace(bk_workspace_size(BK_OP_INST_NORM, dt, B, T, d, p), a.device, ws)
+    _check(lib.bk_per_sample_grads(_ptr(a), _ptr(g), dt, B, T, d, p, _ptr(norm_sq), _ptr(P), _ptr(ws),
+                                   nws, _stream(stream)), "bk_per_sample_grads")
+    return norm_sq, P
+
+
+def bk_weighted_sum(P, C, G=None, stream=None) -> torch.Tensor:
+    """sum_i C_i P_i over stored per-sample gradients P [B, ...] (App. B.5), float32."""
+    _dev(P, "P"), _dev(C, "C")
+    if P.dtype != torch.float32 or C.dtype != torch.float32 or C.dim() != 1 or P.shape[0] != C.shape[0]:
+        raise ValueError("P must be float32 [B, ...] and C float32 [B]")
+    if not P.is_contiguous():
+        raise ValueError("P must be contiguous")
+    B = P.shape[0]
+    G = _out(G, tuple(P.shape[1:]), P.device)
+    n = G.numel()
+    _check(lib.bk_weighted_sum(_ptr(P), _ptr(C), B, n, _ptr(G), _stream(stream)), "bk_weighted_sum")
+    return G
+
+
 def bk_embed_ghost_norm(ids, g, V: int, norm_sq=None, ws=None, stream=None) -> torch.Tensor:
     """Per-sample gradient norm of an embedding layer with vocabulary V."""
     _dev(ids, "ids"), _dev(g, "g")
@@ -304,7 +340,8 @@ def bk_philox_raw(seed: int, tensor_id: int, step: int, q0: int, nq: int, out=No
 
 # -------------------------------------------------------------------- grouped
 def make_layers(specs: Sequence[dict]):
-    """ctypes bk_layer array from dicts {kind, x, g, G (optional), V (embedding)}.
+    """ctypes bk_layer array from dicts {kind, x, g, G (optional), V (embedding),
+    mixopt (optional bool), P (optional float32 [B,d,p], BK-MixOpt store)}.
 
     x is a [B,T,d] for a linear layer or int64 ids [B,T] for an embedding; the
     tensors must stay alive while the array is used."""
@@ -320,13 +357,14 @@ def make_layers(specs: Sequence[dict]):
         else:
             d = x.shape[2]
         arr[k].kind = kind
-        arr[k].reserved = 0
+        arr[k].flags = BK_LAYER_MIXOPT if s.get("mixopt") else 0
         arr[k].T = g.shape[1]
         arr[k].d = d
         arr[k].p = g.shape[2]
         arr[k].x = _ptr(x)
         arr[k].g = _ptr(g)
         arr[k].G = _ptr(G)
+        arr[k].P = _ptr(s.get("P"))
     return arr
 
 

@@ -216,6 +216,21 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
                 for (int i = 0; i < 16; ++i) s += acc[x][y][i] * acc[x][y][i];
         const float tot = block_sum_256(s, red);
         if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
+        if (L.G) {   // keep the per-sample gradient (BK-MixOpt): P[sample] [d,p]
+            float* P = L.G + (size_t)sample * d * p;
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    const int n = n0 + (2 * wn + y) * 32 + (lane & 31);
+                    if (n >= p) continue;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int m = m0 + (2 * wm + x) * 32 + acc_row(i, lane);
+                        if (m < d) P[(size_t)m * p + n] = acc[x][y][i];
+                    }
+                }
+        }
     } else {
         float* G = L.G;
 #pragma unroll
@@ -427,6 +442,21 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
             }
         const float tot = block_sum_256(s, red);
         if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
+        if (L.G) {   // keep the per-sample gradient (BK-MixOpt): P[sample] [d,p]
+            float* P = L.G + (size_t)sample * d * p;
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    const int n = n0 + 64 * wn + 32 * y + (lane & 31);
+                    if (n >= p) continue;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
+                        if (m < d) P[(size_t)m * p + n] = acc[x][y][i];
+                    }
+                }
+        }
     } else {
         float* G = L.G;
 #pragma unroll

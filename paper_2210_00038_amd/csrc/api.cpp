@@ -116,13 +116,27 @@ size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t V) {
     return align_up((size_t)(B * T) * sizeof(uint64_t)) + align_up((size_t)V * sizeof(int32_t));
 }
 
+// BK-MixOpt layer that keeps its instantiated per-sample gradients in P.
+bool keeps_grads(const bk_layer& L) {
+    return L.kind == BK_LINEAR && (L.flags & BK_LAYER_MIXOPT) && bk_use_ghost(L.T, L.d, L.p) != 1;
+}
+
 bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, bool need_G) {
     if (L.kind != BK_LINEAR && L.kind != BK_EMBEDDING)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld has unknown kind %d", fn, (long long)l, L.kind);
-    if (L.reserved != 0)
-        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: reserved field must be 0", fn, (long long)l);
+    if ((L.flags & ~BK_LAYER_MIXOPT) != 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: unknown flags 0x%x", fn, (long long)l, L.flags);
     bk_status s = check_dims(fn, B, L.T, L.d, L.p);
     if (s != BK_OK) return s;
+    if (keeps_grads(L) && B * L.d * L.p > 0) {
+        if (!L.P)
+            return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: BK_LAYER_MIXOPT needs P [B,d,p]", fn,
+                        (long long)l);
+        if ((reinterpret_cast<uintptr_t>(L.P) & 3u) != 0)
+            return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: P not 4-byte aligned", fn, (long long)l);
+        if (B > INT64_MAX / (L.d * L.p))
+            return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: B*d*p overflows", fn, (long long)l);
+    }
     const bool has_tokens = B > 0 && L.T > 0;
     if (has_tokens && (!L.x || (!L.g && L.p > 0)))
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: NULL input pointer", fn, (long long)l);
@@ -214,7 +228,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             bk::GemmLayer& g = a.L[k];
             g.a = L.x;
             g.g = L.g;
-            g.G = nullptr;
+            g.G = keeps_grads(L) ? L.P : nullptr;
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
@@ -275,6 +289,18 @@ size_t weighted_grads_ws(const bk_layer* layers, int64_t n, int64_t B) {
     return tot;
 }
 
+// Appends one weighted-sum job (P [B, n] -> G [n]) to a grouped launch.
+bk_status add_wsum_layer(bk::WsumArgs& w, int64_t& wg, const float* P, float* G, int64_t n) {
+    bk::WsumLayer& L = w.L[w.n++];
+    L.P = P;
+    L.G = G;
+    L.n = n;
+    L.wg_begin = (uint32_t)wg;
+    L.vec = (aligned16(P) && aligned16(G) && n % 4 == 0) ? 1u : 0u;
+    wg += cdiv(n, bk::kWsumPerWG);
+    return BK_OK;
+}
+
 bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, const float* C,
                          bk_dtype dt, int64_t B, void* ws, size_t ws_bytes, hipStream_t s) {
     if (n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative layer count", fn);
@@ -315,7 +341,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         };
         for (int64_t l = 0; l < n; ++l) {
             const bk_layer& L = layers[l];
-            if (L.kind != BK_LINEAR || L.d * L.p == 0) continue;
+            if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
             const auto v = grad_variant(L);
             if ((int)v != var) continue;
             bk::GemmLayer& g = a.L[a.n++];
@@ -332,6 +358,28 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.part_off = 0;
             wg += (int64_t)g.tm * g.tn;
             if (a.n == bk::kMaxGemm && (st = flush()) != BK_OK) return st;
+        }
+        if ((st = flush()) != BK_OK) return st;
+    }
+    // BK-MixOpt layers: weighted sums of their stored per-sample gradients.
+    {
+        bk::WsumArgs w{};
+        w.B = (int32_t)B;
+        w.C = C;
+        int64_t wg = 0;
+        auto flush = [&]() -> bk_status {
+            if (w.n == 0) return BK_OK;
+            if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+            hipError_t e = bk::launch_wsum(w, (int)wg, s);
+            w.n = 0;
+            wg = 0;
+            return e == hipSuccess ? BK_OK : hip_fail(e, "weighted sum launch");
+        };
+        for (int64_t l = 0; l < n; ++l) {
+            const bk_layer& L = layers[l];
+            if (!keeps_grads(L) || L.d * L.p == 0) continue;
+            if ((st = add_wsum_layer(w, wg, L.P, L.G, L.d * L.p)) != BK_OK) return st;
+            if (w.n == bk::kMaxWsum && (st = flush()) != BK_OK) return st;
         }
         if ((st = flush()) != BK_OK) return st;
     }
@@ -430,6 +478,7 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         bk::GemmLayer& g = a.L[0];
         g.a = L.x;
         g.g = L.g;
+        g.G = (L.flags & BK_LAYER_MIXOPT) ? L.P : nullptr;
         g.T = (int32_t)L.T;
         g.d = (int32_t)L.d;
         g.p = (int32_t)L.p;
@@ -509,6 +558,48 @@ bk_status bk_inst_norm(const void* a, const void* g, bk_dtype dt, int64_t B, int
                        int64_t p, float* norm_sq, void* ws, size_t ws_bytes, void* stream) {
     return single_norm("bk_inst_norm", Path::Inst, linear_layer(a, g, T, d, p, nullptr), dt, B,
                        norm_sq, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_per_sample_grads(const void* a, const void* g, bk_dtype dt, int64_t B, int64_t T,
+                              int64_t d, int64_t p, float* norm_sq, float* P, void* ws,
+                              size_t ws_bytes, void* stream) {
+    const char* fn = "bk_per_sample_grads";
+    bk_status st = check_dims(fn, B, T, d, p);
+    if (st != BK_OK) return st;
+    if (B * d * p > 0) {
+        if (!P) return fail(BK_ERR_INVALID_VALUE, "%s: NULL per-sample gradient output", fn);
+        if ((reinterpret_cast<uintptr_t>(P) & 3u) != 0)
+            return fail(BK_ERR_INVALID_VALUE, "%s: P not 4-byte aligned", fn);
+        if (B > INT64_MAX / (d * p)) return fail(BK_ERR_INVALID_VALUE, "%s: B*d*p overflows", fn);
+    }
+    bk_layer L = linear_layer(a, g, T, d, p, nullptr);
+    L.P = P;
+    L.flags = BK_LAYER_MIXOPT;
+    // The layer may satisfy the ghost rule; the explicit call instantiates anyway.
+    bk_layer Lc = L;
+    Lc.flags = 0;
+    if ((st = check_layer(fn, Lc, 0, B, false)) != BK_OK) return st;
+    return single_norm(fn, Path::Inst, L, dt, B, norm_sq, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, float* G, void* stream) {
+    const char* fn = "bk_weighted_sum";
+    if (B < 0 || n < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (B > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: batch too large", fn);
+    if (n == 0) return BK_OK;
+    if (!G) return fail(BK_ERR_INVALID_VALUE, "%s: NULL output", fn);
+    if (B > 0 && (!P || !C)) return fail(BK_ERR_INVALID_VALUE, "%s: NULL input", fn);
+    if (B > 0 && n > INT64_MAX / B) return fail(BK_ERR_INVALID_VALUE, "%s: B*n overflows", fn);
+    if (((reinterpret_cast<uintptr_t>(P) | reinterpret_cast<uintptr_t>(C) | reinterpret_cast<uintptr_t>(G)) & 3u) != 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: pointers must be 4-byte aligned", fn);
+    if (cdiv(n, bk::kWsumPerWG) > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many elements", fn);
+    bk::WsumArgs w{};
+    w.B = (int32_t)B;
+    w.C = C;
+    int64_t wg = 0;
+    add_wsum_layer(w, wg, P, G, n);
+    hipError_t e = bk::launch_wsum(w, (int)wg, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "weighted sum launch");
 }
 
 bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B, int64_t T,

@@ -36,7 +36,8 @@ struct GhostArgs {
 struct GemmLayer {
     const void* a;      // [B,T,d]
     const void* g;      // [B,T,p]
-    float* G;           // [d,p] out (clipped gradient)
+    float* G;           // [d,p] out (clipped gradient); instantiated norm: the
+                        // per-sample gradients [B,d,p] out, or nullptr
     int32_t T, d, p;
     int32_t tm, tn;     // output tiles along d and p
     int32_t wg_begin;
@@ -103,6 +104,22 @@ GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool ali
 int gemm_tile_m(GemmVariant v);
 int gemm_tile_n(GemmVariant v);
 
+// ---- weighted sum of stored per-sample gradients -------------------------------
+struct WsumLayer {
+    const float* P;     // [B, n]
+    float* G;           // [n]
+    int64_t n;
+    uint32_t wg_begin;
+    uint32_t vec;       // P, G 16-byte aligned and 4 | n
+};
+constexpr int kMaxWsum = 100;
+struct WsumArgs {
+    int32_t n, B;
+    const float* C;
+    WsumLayer L[kMaxWsum];
+};
+constexpr int kWsumPerWG = 1024;    // elements per workgroup
+
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
@@ -112,6 +129,7 @@ hipError_t launch_reduce(const ReduceArgs& args, int n_threads, hipStream_t s);
 hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, float R, float gamma,
                        float* C, float* total_sq, hipStream_t s);
 hipError_t launch_noise(const NoiseArgs& args, int n_wg, hipStream_t s);
+hipError_t launch_wsum(const WsumArgs& args, int n_wg, hipStream_t s);
 hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q0, int64_t nq,
                              uint32_t* out, hipStream_t s);
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,

@@ -121,10 +121,10 @@ def test_grouped_validation():
     for k in range(2):
         arr[k].kind, arr[k].T, arr[k].d, arr[k].p = bk.BK_LINEAR, 8, 16, 16
         arr[k].x = arr[k].g = arr[k].G = 0x10000
-    arr[1].reserved = 1
+    arr[1].flags = 2                                        # not a known flag
     st = bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
-    assert st == bk.BK_ERR_INVALID_VALUE and "reserved" in bk.bk_last_error()
-    arr[1].reserved = 0
+    assert st == bk.BK_ERR_INVALID_VALUE and "flags" in bk.bk_last_error()
+    arr[1].flags = 0
     arr[1].kind = 5
     assert bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None) == bk.BK_ERR_INVALID_VALUE
     arr[1].kind = bk.BK_LINEAR
@@ -141,3 +141,32 @@ def test_status_strings():
     assert bk.bk_status_string(bk.BK_OK) == "BK_OK"
     assert bk.bk_status_string(bk.BK_ERR_WORKSPACE) == "BK_ERR_WORKSPACE"
     assert "gfx950" in bk.bk_version()
+
+
+def test_mixopt_validation():
+    """BK-MixOpt store: needed (and checked) only on a linear layer that instantiates."""
+    arr = (bk.bk_layer * 1)()
+    arr[0].kind, arr[0].T, arr[0].d, arr[0].p = bk.BK_LINEAR, 64, 16, 16     # 2T^2 >= pd: instantiates
+    arr[0].x = arr[0].g = arr[0].G = 0x10000
+    arr[0].flags = bk.BK_LAYER_MIXOPT
+    st = bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    assert st == bk.BK_ERR_INVALID_VALUE and "needs P" in bk.bk_last_error()
+    assert bk.lib.bk_weighted_grads(arr, 1, FAKE, bk.BK_BF16, 4, FAKE, 1 << 20, None) == bk.BK_ERR_INVALID_VALUE
+    arr[0].P = 0x10002                                       # misaligned
+    st = bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    assert st == bk.BK_ERR_INVALID_VALUE and "aligned" in bk.bk_last_error()
+    # a ghost-norm layer ignores the flag: no store needed, validation reaches the workspace check
+    arr[0].T, arr[0].d, arr[0].p, arr[0].P = 8, 64, 64, None
+    need = bk.bk_layer_norms_workspace_size(arr, 1, bk.BK_BF16, 4)
+    assert need > 0
+    assert bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, need - 1, None) == bk.BK_ERR_WORKSPACE
+    # single-layer calls
+    L = bk.lib
+    assert L.bk_per_sample_grads(FAKE, FAKE, bk.BK_BF16, 2, 8, 4, 4, FAKE, None, FAKE, 1 << 20, None) == \
+        bk.BK_ERR_INVALID_VALUE
+    assert L.bk_per_sample_grads(None, None, bk.BK_BF16, 0, 8, 4, 4, None, None, None, 0, None) == bk.BK_OK
+    assert L.bk_weighted_sum(FAKE, FAKE, 3, -1, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_weighted_sum(None, FAKE, 3, 10, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_weighted_sum(FAKE, FAKE, 3, 10, None, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_weighted_sum(0x10002, FAKE, 3, 10, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_weighted_sum(None, None, 3, 0, None, None) == bk.BK_OK             # nothing to do

@@ -227,11 +227,14 @@ def _stack_inputs(layers, B, dtype, seed):
     return ins
 
 
-def _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, std, seed):
+def _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, std, seed, mixopt=False):
     dev_ins = [(x.to(DEV), g.to(DEV)) for x, g in ins]
     Gs = [torch.empty(L.d, L.p, device=DEV) for L in layers]
+    # BK-MixOpt: every linear layer carries the flag; those that instantiate get a store
+    Ps = [torch.empty(B, L.d, L.p, device=DEV) if mixopt and L.kind != "embed" and not bk.bk_use_ghost(L.T, L.d, L.p)
+          else None for L in layers]
     specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
-              "V": L.d} for L, (x, g), G in zip(layers, dev_ins, Gs)]
+              "V": L.d, "mixopt": mixopt, "P": P} for L, (x, g), G, P in zip(layers, dev_ins, Gs, Ps)]
     arr = bk.make_layers(specs)
     n = len(layers)
     norm_sq = torch.empty(n, B, device=DEV)
@@ -302,3 +305,57 @@ def test_grouped_noise_equals_per_tensor_noise(bk):
     got = bk.bk_add_noise_grouped([G.clone() for G in Gs], 0.6, 31, tensor_ids=[10, 11, 12, 13], step=2)
     for r, o in zip(ref, got):
         assert torch.equal(r, o)
+
+
+# ---------------------------------------------------------------- BK-MixOpt
+@pytest.mark.parametrize("B,T,d,p,dtype", [
+    (3, 20, 40, 24, torch.float32),           # 16-byte rows, one 128 x 128 tile
+    (2, 77, 70, 33, torch.float32),           # rows not 16-byte multiples: scalar loads
+    (2, 70, 520, 264, torch.bfloat16),        # ragged 256 x 128 tiles of the wide kernel
+    (2, 129, 100, 60, torch.bfloat16),        # scalar-load bf16 path
+])
+def test_per_sample_grads_match_oracle(bk, B, T, d, p, dtype):
+    a, g = _pair(B, T, d, p, dtype, seed=31 + T)
+    ref_P = oracle.per_sample_grads(a, g)
+    norm, P = bk.bk_per_sample_grads(a.to(DEV), g.to(DEV))
+    P = P.cpu().numpy()
+    for i in range(B):
+        assert _frob(P[i], ref_P[i]) <= GRAD_TOL[dtype], i
+    assert _rel(norm.cpu().numpy(), oracle.linear_norm_sq(a, g)) <= NORM_TOL[dtype]
+
+
+@pytest.mark.parametrize("B,shape", [(5, (33, 7)), (16, (768, 768)), (1, (3,)), (7, (1000,))])
+def test_weighted_sum_matches_oracle(bk, B, shape):
+    gen = torch.Generator().manual_seed(B)
+    P = torch.randn((B,) + shape, generator=gen)
+    C = torch.rand(B, generator=gen) + 0.05
+    ref = oracle.weighted_sum(P.reshape(B, -1).numpy(), C.numpy()).reshape(shape)
+    G = bk.bk_weighted_sum(P.to(DEV), C.to(DEV)).cpu().numpy()
+    assert _frob(G, ref) <= 1e-6
+    # no samples: zeros
+    Z = bk.bk_weighted_sum(torch.empty((0,) + shape, device=DEV), torch.empty(0, device=DEV))
+    assert torch.count_nonzero(Z).item() == 0
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_private_grad_mixopt_matches_oracle(bk, dtype):
+    """BK-MixOpt on a mixed stack: the instantiated layer forms G from its stored per-sample
+    gradients; the result equals the oracle's MixOpt path and the base path."""
+    Lr = wl.Layer
+    layers = [Lr("linear", 40, 64, 96),       # ghost
+              Lr("linear", 150, 96, 130),     # instantiate: keeps per-sample gradients
+              Lr("linear", 64, 72, 48),       # instantiate (8192 > 3456)
+              Lr("embed", 40, 500, 64)]
+    B = 5
+    ins = _stack_inputs(layers, B, dtype, seed=7)
+    for mode, R, gamma in [(0, 1e-2, 0.0), (1, 1.0, 0.01)]:
+        norms, C, tot, G = _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, 0.0, seed=3, mixopt=True)
+        _, _, _, G_base = _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, 0.0, seed=3)
+        ref = oracle.bk_stack(layers, ins, "abadi" if mode == 0 else "auto", R, gamma, 0.0, seed=3,
+                              with_noise=False, mixopt=True)
+        assert ref["paths"] == ["ghost", "inst", "inst", "embed"]
+        assert _rel(norms, ref["norms"]) <= NORM_TOL[dtype]
+        assert _rel(C, ref["C"]) <= NORM_TOL[dtype]
+        for l in range(len(layers)):
+            assert _frob(G[l], ref["G"][l]) <= GRAD_TOL[dtype], l
+            assert _frob(G[l], G_base[l]) <= GRAD_TOL[dtype], l
