@@ -38,8 +38,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense MFMA
 
 
-def algorithmic_work(w: wl.Workload):
-    """Per-step algorithmic flops / bytes of each phase (paper's per-module costs)."""
+def algorithmic_work(w: wl.Workload, mixopt: bool = False):
+    """Per-step algorithmic flops / bytes of each phase (paper's per-module costs).
+    mixopt: instantiated layers keep their per-sample gradients (written by the
+    norm phase, 4Bpd bytes) and form G as their weighted sum (2Bpd flops,
+    reading 4Bpd and writing 4pd bytes) instead of the 2BTpd GEMM."""
     es = 2 if w.dtype == "bf16" else 4
     B = w.B
     out = {"norm_flops": 0.0, "norm_bytes": 0.0, "gemm_flops": 0.0, "gemm_bytes": 0.0,
@@ -58,8 +61,13 @@ def algorithmic_work(w: wl.Workload):
                 out["inst_layers"] += 1
                 out["norm_flops"] += 2.0 * B * L.T * L.p * L.d               # instantiation, App. B.4.1
             out["norm_bytes"] += B * L.T * (L.d + L.p) * es
-            out["gemm_flops"] += 2.0 * B * L.T * L.p * L.d                   # a^T diag(C) g, App. B.3
-            out["gemm_bytes"] += B * L.T * (L.d + L.p) * es + 4.0 * L.d * L.p
+            if mixopt and not ghost:
+                out["norm_bytes"] += 4.0 * B * L.d * L.p                     # stored per-sample gradients
+                out["gemm_flops"] += 2.0 * B * L.p * L.d                     # weighted sum, App. B.5
+                out["gemm_bytes"] += 4.0 * B * L.d * L.p + 4.0 * L.d * L.p
+            else:
+                out["gemm_flops"] += 2.0 * B * L.T * L.p * L.d               # a^T diag(C) g, App. B.3
+                out["gemm_bytes"] += B * L.T * (L.d + L.p) * es + 4.0 * L.d * L.p
         out["noise_elems"] += float(L.d) * L.p
     return out
 
@@ -101,7 +109,8 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = {"agrad_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+KERNEL_SOURCES = {"agrad_dl_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+                  "agrad_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip"}
 
 
@@ -146,6 +155,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-5)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mixopt", action="store_true",
+                    help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (reference for the HBM byte counters)")
     args = ap.parse_args()
@@ -169,8 +180,10 @@ def main():
     n, B = len(w.layers), w.B
 
     ins, Gs = make_inputs(w, dev)
+    keep = [args.mixopt and L.kind != "embed" and not bk.bk_use_ghost(L.T, L.d, L.p) for L in w.layers]
+    Ps = [torch.empty(B, L.d, L.p, device=dev) if k else None for L, k in zip(w.layers, keep)]
     specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
-              "V": L.d} for L, (x, g), G in zip(w.layers, ins, Gs)]
+              "V": L.d, "mixopt": args.mixopt, "P": P} for L, (x, g), G, P in zip(w.layers, ins, Gs, Ps)]
     arr = bk.make_layers(specs)
     norm_sq = torch.empty(n, B, device=dev)
     C = torch.empty(B, device=dev)
@@ -214,7 +227,7 @@ def main():
 
     ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs])   # ms
     ph_ms = ph.mean(axis=0)
-    work = algorithmic_work(w)
+    work = algorithmic_work(w, args.mixopt)
     ms_step = elapsed * 1e3 / args.steps
     peak_mfma = PEAK_MFMA_TFLOPS[w.dtype]
     phases = {
@@ -228,9 +241,12 @@ def main():
     # Dominant kernel: the phase with the most time among the two big ones.
     if phases["weighted_grads"]["ms"] >= phases["norms"]["ms"]:
         ach = phases["weighted_grads"]["tflops"]
-        roof = {"kernel": "agrad_bf16_kernel (clip-weighted gradient, all layers in one launch)",
+        # bf16 layers with 32 | T take the LDS-DMA kernel, other T the register-staged one
+        gk = "agrad_dl_kernel" if all(L.T % 32 == 0 for L in w.layers if L.kind != "embed") \
+            else "agrad_bf16_kernel"
+        roof = {"kernel": f"{gk} (clip-weighted gradient, all layers in one launch)",
                 "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                "frac": ach / peak_mfma, "traffic": measured_traffic("agrad_bf16_kernel", w.name),
+                "frac": ach / peak_mfma, "traffic": measured_traffic(gk, w.name),
                 "per_launch": f"{work['gemm_flops'] / 1e9:.1f} GFLOP (sum over layers of 2 B T d p)"}
     elif work["norm_flops"] / max(work["norm_bytes"], 1.0) > peak_mfma * 1e3 / PEAK_HBM_GBS:
         # above the ridge point (long sequences): the norm kernels are MFMA-bound
@@ -253,7 +269,8 @@ def main():
         "metric": METRIC, "value": B / (ms_step / 1e3), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
-        "config": {"workload": w.name, "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
+        "config": {"workload": w.name, "variant": "BK-MixOpt" if args.mixopt else "BK",
+                   "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
                    "clip": w.clip, "sigma": w.sigma, "paths": {"ghost": work["ghost_layers"],
                    "inst": work["inst_layers"], "embed": work["embed_layers"]}},
         "roofline": roof,
