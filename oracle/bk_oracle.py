@@ -33,6 +33,11 @@ What is computed, and where the paper defines it
 * weighted_sum          -- sum_i C_i (a_i^T g_i) from stored per-sample
                            gradients (App. B.5), BK-MixOpt's clipped gradient
                            on those layers.
+* unfold / tokens_from_nchw -- a 2-D convolution as a generalized linear layer
+                           (App. B: d = input channels x kernel size, p =
+                           output channels, T = output height x width): the
+                           activation a_i is the unfolded input, and the
+                           output gradient is taken token-major [T, p].
 * philox4x32_10 / noise -- Algorithm 1, Gaussian noise sigma R N(0, I).  The
                            paper does not fix a generator; the reading used
                            here is Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
@@ -59,7 +64,8 @@ __all__ = [
     "embed_norm_sq", "embed_norm_sq_pairs", "aggregate", "clip_factors", "weighted_grad",
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
     "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
-    "bk_layer_norm", "bk_stack", "per_sample_grads", "weighted_sum",
+    "bk_layer_norm", "bk_stack", "per_sample_grads", "weighted_sum", "conv_out_size", "unfold",
+    "tokens_from_nchw",
 ]
 
 F64 = np.float64
@@ -230,6 +236,40 @@ def weighted_sum(P, C) -> np.ndarray:
     for i in range(P.shape[0]):
         G += C[i] * P[i]
     return G
+
+
+def conv_out_size(n: int, k: int, stride: int, pad: int) -> int:
+    return (n + 2 * pad - k) // stride + 1
+
+
+def unfold(x, kh: int, kw: int, stride: int = 1, pad: int = 0, ld: int = 0) -> np.ndarray:
+    """x [B, C, H, W] -> a [B, T, ld] with T = Ho Wo, token t = (oh, ow) row-major, and
+    column (c, i, j) -> c kh kw + i kw + j holding x[c, oh stride + i - pad, ow stride + j - pad]
+    (0 outside the image); columns d = C kh kw .. ld-1 are zero (ld = 0: ld = d).
+    With W [p, C, kh, kw] reshaped to [p, d] the convolution output is s = a W^T."""
+    x = _f64(x)
+    B, Cc, H, Wd = x.shape
+    Ho, Wo = conv_out_size(H, kh, stride, pad), conv_out_size(Wd, kw, stride, pad)
+    d = Cc * kh * kw
+    ld = ld or d
+    a = np.zeros((B, Ho * Wo, ld), dtype=F64)
+    for oh in range(Ho):
+        for ow in range(Wo):
+            t = oh * Wo + ow
+            for c in range(Cc):
+                for i in range(kh):
+                    for j in range(kw):
+                        h, w = oh * stride + i - pad, ow * stride + j - pad
+                        if 0 <= h < H and 0 <= w < Wd:
+                            a[:, t, c * kh * kw + i * kw + j] = x[:, c, h, w]
+    return a
+
+
+def tokens_from_nchw(y) -> np.ndarray:
+    """[B, C, H, W] -> [B, H W, C] (the output gradient of a convolution, token-major)."""
+    y = _f64(y)
+    B, Cc, H, Wd = y.shape
+    return y.reshape(B, Cc, H * Wd).transpose(0, 2, 1).copy()
 
 
 def embed_weighted_grad(ids, g, C, V: int) -> np.ndarray:

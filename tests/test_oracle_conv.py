@@ -1,0 +1,64 @@
+"""Pins of the oracle's convolution-as-linear-layer view (CPU only): unfold and the
+token-major output gradient reproduce torch's conv2d and its per-sample weight
+gradient, and the linear-layer definitions then give the conv layer's norms."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+
+def _case(seed, B, Cin, H, W, Cout, k, stride, pad):
+    gen = torch.Generator().manual_seed(seed)
+    x = torch.randn(B, Cin, H, W, generator=gen, dtype=torch.float64)
+    Wt = torch.randn(Cout, Cin, k, k, generator=gen, dtype=torch.float64)
+    return x, Wt
+
+
+@pytest.mark.parametrize("B,Cin,H,W,Cout,k,stride,pad", [
+    (2, 3, 9, 7, 4, 3, 1, 1), (1, 2, 8, 8, 5, 3, 2, 1), (2, 4, 6, 5, 3, 1, 1, 0), (1, 3, 11, 11, 2, 7, 2, 3)])
+def test_unfold_reproduces_conv2d(B, Cin, H, W, Cout, k, stride, pad):
+    x, Wt = _case(B + H, B, Cin, H, W, Cout, k, stride, pad)
+    s_ref = torch.nn.functional.conv2d(x, Wt, stride=stride, padding=pad).numpy()   # [B, Cout, Ho, Wo]
+    a = oracle.unfold(x.numpy(), k, k, stride, pad)
+    s = a @ Wt.reshape(Cout, -1).numpy().T                                          # [B, T, Cout]
+    np.testing.assert_allclose(s, oracle.tokens_from_nchw(s_ref), rtol=1e-12, atol=1e-12)
+    # padded columns are zero and change nothing
+    a_pad = oracle.unfold(x.numpy(), k, k, stride, pad, ld=a.shape[2] + 5)
+    np.testing.assert_array_equal(a_pad[:, :, :a.shape[2]], a)
+    assert not np.any(a_pad[:, :, a.shape[2]:])
+
+
+def test_tokens_from_nchw_small():
+    y = np.arange(2 * 3 * 2 * 2, dtype=np.float64).reshape(2, 3, 2, 2)
+    t = oracle.tokens_from_nchw(y)
+    assert t.shape == (2, 4, 3)
+    assert t[1, 2, 0] == y[1, 0, 1, 0] and t[0, 3, 2] == y[0, 2, 1, 1]
+
+
+def test_conv_per_sample_grads_and_norms_match_autograd():
+    B, Cin, H, W, Cout, k, stride, pad = 3, 2, 7, 6, 4, 3, 2, 1
+    x, Wt = _case(11, B, Cin, H, W, Cout, k, stride, pad)
+    gen = torch.Generator().manual_seed(5)
+    Ho, Wo = oracle.conv_out_size(H, k, stride, pad), oracle.conv_out_size(W, k, stride, pad)
+    dy = torch.randn(B, Cout, Ho, Wo, generator=gen, dtype=torch.float64)   # dL/ds
+    a = oracle.unfold(x.numpy(), k, k, stride, pad)
+    g = oracle.tokens_from_nchw(dy.numpy())
+    P = oracle.per_sample_grads(a, g)                                        # [B, d, p]
+    norms = oracle.linear_norm_sq(a, g)
+    ghost = oracle.linear_norm_sq_gram(a, g)
+    C = np.array([0.5, 2.0, 0.0])
+    G = oracle.weighted_grad(a, g, C)
+    for i in range(B):
+        Wv = Wt.clone().requires_grad_(True)
+        s = torch.nn.functional.conv2d(x[i:i + 1], Wv, stride=stride, padding=pad)
+        (s * dy[i:i + 1]).sum().backward()
+        gi = Wv.grad.reshape(Cout, -1).numpy().T                             # [d, p]
+        np.testing.assert_allclose(P[i], gi, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(norms[i], (gi ** 2).sum(), rtol=1e-12)
+        np.testing.assert_allclose(ghost[i], (gi ** 2).sum(), rtol=1e-10)
+    # the clipped gradient of the conv weight is sum_i C_i grad_i
+    Wv = Wt.clone().requires_grad_(True)
+    s = torch.nn.functional.conv2d(x, Wv, stride=stride, padding=pad)
+    (s * dy * torch.tensor(C).view(B, 1, 1, 1)).sum().backward()
+    np.testing.assert_allclose(G, Wv.grad.reshape(Cout, -1).numpy().T, rtol=1e-12, atol=1e-12)
