@@ -301,6 +301,22 @@ __device__ __forceinline__ uint2 frag_tr_half(const char* lds, int kb, int cb, i
     return lds_tr16(lds + row * S + col * 2);
 }
 
+// Full TM x TN float32 partial tile of a K slice (row-major, stride TN) from
+// the 4 x 2 accumulators of a wave owning rows [r0, r0 + 128) and columns
+// [c0, c0 + 64), each value multiplied by `scale`.
+template <int TM, int TN>
+__device__ __forceinline__ void store_partial_tile(float* P, const f32x16_t (&acc)[4][2], int r0, int c0,
+                                                   int lane, float scale) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int n = c0 + 32 * y + (lane & 31);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) P[(r0 + 32 * x + acc_row(i, lane)) * TN + n] = acc[x][y][i] * scale;
+        }
+}
+
 // Two bf16 in one word, each multiplied by c, rounded to nearest even.
 __device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float c) {
     const f32x2_t f = {__uint_as_float(w << 16) * c, __uint_as_float(w & 0xFFFF0000u) * c};
@@ -326,9 +342,10 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int tiles = L.tm * tn;
-    const int local = wg - L.wg_begin;
-    const int sample = INST ? local / tiles : 0;
-    const int tile = local - sample * tiles;
+    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
+    const int sample = INST ? local / (tiles * ks) : 0;
+    const int rem = local - sample * tiles * ks;
+    const int tile = rem / ks, slice = rem - tile * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kBM, n0 = nt * kBN;
 
@@ -388,9 +405,12 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
         }
     };
 
-    const uint32_t nst = (nrows + kBK - 1) / kBK;
-    if (nst > 0) fetch(0);
-    for (uint32_t st = 0; st < nst; ++st) {
+    // This workgroup's stages (K slice `slice` of `ks`).
+    const uint32_t nst_all = (nrows + kBK - 1) / kBK;
+    const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
+    const uint32_t nst = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
+    if (st_begin < nst) fetch(st_begin * kBK);
+    for (uint32_t st = st_begin; st < nst; ++st) {
         lds_barrier();
 #pragma unroll
         for (int j = 0; j < 8; ++j)
@@ -427,6 +447,12 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
         }
     }
 
+    if (ks > 1) {
+        store_partial_tile<kBM, kBN>(
+            args.tiles + ((size_t)L.ptile_off + ((size_t)sample * tiles + tile) * ks + slice) * (kBM * kBN),
+            acc, 128 * wm, 64 * wn, lane, 1.f);
+        return;
+    }
     if constexpr (INST) {
         float s = 0.f;
 #pragma unroll
@@ -502,7 +528,8 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
-    const int tile = wg - L.wg_begin;
+    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
+    const int tile = local / ks, slice = local - tile * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
@@ -541,7 +568,12 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     uint4 va[4], vb[4];
     float c0 = 0.f, c1 = 0.f;
     uint32_t split = 0;
-    uint32_t fk0 = 0, fq = 0, frem = 0;   // next fetch: first row, its sample, row in sample
+    // This workgroup's stages (K slice `slice` of `ks`).
+    const uint32_t nst_all = (nrows + kBK - 1) / kBK;
+    const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
+    const uint32_t st_end = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
+    // next fetch: first row, its sample, row in sample
+    uint32_t fk0 = st_begin * kBK, fq = fk0 / (uint32_t)nT, frem = fk0 - fq * (uint32_t)nT;
     auto load_a = [&](int j) { va[j] = buffer_load16(rA, offA == kOut ? kOut : offA + (fk0 + 16u * j) * rowA); };
     auto load_b = [&](int j) { vb[j] = buffer_load16(rB, offB == kOut ? kOut : offB + (fk0 + 16u * j) * rowB); };
     auto load_c = [&]() {
@@ -631,7 +663,7 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
         }
     };
 
-    const uint32_t nst = (nrows + kBK - 1) / kBK;
+    const uint32_t nst = st_end - st_begin;
     if (nst > 0) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -669,6 +701,11 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     }
     if (st < nst) stage(std::integral_constant<int, 0>{});
 
+    if (ks > 1) {
+        store_partial_tile<kGM, kGN>(args.tiles + ((size_t)L.ptile_off + (size_t)tile * ks + slice) * (kGM * kGN),
+                                     acc, 128 * wm, 64 * wn, lane, 1.f);
+        return;
+    }
     float* G = L.G;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
@@ -684,25 +721,6 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
         }
 }
 
-// ---------------------------------------------------------------------------
-// Clipped-gradient kernel for bf16 rows when 64 divides T: the tiles, waves,
-// stages and hand-laid issue order of agrad_bf16_kernel, but both operand
-// tiles go from HBM straight into LDS (LDS DMA: no staging registers, no LDS
-// store instructions) and the clip weights are applied to the accumulators
-// instead of to g.  A 64-row stage then lies inside one sample.  The
-// accumulators hold S / c, S being the weighted sum so far and c the weight
-// of the last sample whose weight is nonzero: entering sample j with
-// C_j != 0 multiplies them by c / C_j, and the epilogue multiplies by the
-// final c.  Rows of samples with C_j = 0 load as zeros.  (Products are exact
-// in fp32 and each sample boundary rounds once, instead of C_j g being
-// rounded to bf16.)
-//
-// LDS: two buffers of an a stage and a g stage, 512-byte rows without
-// padding (one DMA instruction fills 1 KB contiguously); the 16-byte column c
-// of row r sits at c ^ 4 (r mod 4), which puts the four rows that each half
-// of a transpose read touches on distinct bank groups.  The clip weights of
-// the batch sit in LDS after the buffers (B <= kDMaxB).
-// ---------------------------------------------------------------------------
 constexpr int kDRow = 512;                       // bytes per staged k-row
 constexpr int kDKS = kDLStageRows;               // k rows per stage
 constexpr int kDNB = kDLBuffers;                 // LDS stage buffers
@@ -791,7 +809,8 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
-    const int tile = wg - L.wg_begin;
+    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
+    const int tile = local / ks, slice = local - tile * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
@@ -843,8 +862,11 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
 
-    const uint32_t nst = (nrows + kDKS - 1) / kDKS;
+    const uint32_t nst_all = (nrows + kDKS - 1) / kDKS;
     const uint32_t spt = (uint32_t)nT / kDKS;            // stages per sample
+    // This workgroup's stages (K slice `slice` of `ks`).
+    const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
+    const uint32_t st_end = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
     // Weight of the stage at `pos` (0 past the batch).
     auto cw_of = [&](const StagePos& pos) { return ctab[min(pos.smp, (uint32_t)B)]; };
 
@@ -922,17 +944,17 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 
     __syncthreads();      // clip weights in LDS
     float c_cur = 0.f;
-    StagePos pos0{0u, 0u};                 // stage st
+    StagePos pos0{st_begin / spt, st_begin % spt};        // stage st
     pos1 = pos0;
     pos1.next(spt);
-    // Prologue: stages 0 .. NB - 1 into the NB buffers.
+    // Prologue: stages st_begin .. st_begin + NB - 1 into the NB buffers.
     {
         StagePos q = pos0;
 #pragma unroll
         for (int b = 0; b < kDNB; ++b) {
             const bool z = cw_of(q) == 0.f;
 #pragma unroll
-            for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (uint32_t)b * kDKS, z, i);
+            for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (st_begin + (uint32_t)b) * kDKS, z, i);
             q.next(spt);
         }
         posN = q;
@@ -950,12 +972,14 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         read_b(lds + kDOp, 0, y, 0);
         read_b(lds + kDOp, 0, y, 1);
     }
+    // The first stage of the slice sets the weight even inside a sample.
     auto run = [&](auto buf_c, uint32_t st) {
-        enter(pos0.in == 0u, c_cur);
+        enter(pos0.in == 0u || st == st_begin, c_cur);
         c_cur = stage(buf_c, st);
         pos0.next(spt);
     };
-    uint32_t st = 0;
+    const uint32_t nst = st_end;
+    uint32_t st = st_begin;
     for (; st + kDNB <= nst; st += kDNB) {
         run(std::integral_constant<int, 0>{}, st);
         run(std::integral_constant<int, 1>{}, st + 1);
@@ -969,6 +993,11 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // Drain the DMA past the end before the workgroup exits.
     wait_vmcnt<0>();
 
+    if (ks > 1) {
+        store_partial_tile<kGM, kGN>(args.tiles + ((size_t)L.ptile_off + (size_t)tile * ks + slice) * (kGM * kGN),
+                                     acc, 128 * wm, 64 * wn, lane, c_last);
+        return;
+    }
     float* G = L.G;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
@@ -982,6 +1011,54 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
                 if (m < d) G[(size_t)m * p + n] = acc[x][y][i] * c_last;
             }
         }
+}
+
+// Sum of the K slices of split layers, slice 0 first.  Workgroup -> layer by
+// red_begin; inside a layer, tile group (sample * tiles + tile for the
+// instantiated norm, tile otherwise) and one kSplitRedWG-element chunk of it.
+// Clipped gradient: the sum goes to G.  Instantiated norm: its squares (of
+// elements inside the matrix) are summed into one norm partial per chunk,
+// and with G set (BK-MixOpt) the sum is also kept in G [B,d,p].
+template <int TM, int TN, bool INST>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) {
+    __shared__ float red[4];
+    constexpr int CH = TM * TN / kSplitRedWG;
+    const int wg = blockIdx.x;
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].red_begin) ++l;
+    const GemmLayer& L = args.L[l];
+    const int job = wg - L.red_begin;
+    const int tg = job / CH, ch = job - tg * CH;
+    const int tiles = L.tm * L.tn;
+    const int sample = INST ? tg / tiles : 0;
+    const int tile = tg - sample * tiles;
+    const int mt = tile / L.tn, nt = tile - mt * L.tn;
+    const int e = ch * kSplitRedWG + 4 * (int)threadIdx.x;
+    const int m = mt * TM + e / TN, n = nt * TN + e % TN;
+    const float* src = args.tiles + ((size_t)L.ptile_off + (size_t)tg * max(L.ksplit, 1)) * (TM * TN) + e;
+    float4 sum = *reinterpret_cast<const float4*>(src);
+    for (int q = 1; q < max(L.ksplit, 1); ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(src + (size_t)q * (TM * TN));
+        sum.x += v.x;
+        sum.y += v.y;
+        sum.z += v.z;
+        sum.w += v.w;
+    }
+    const float r[4] = {sum.x, sum.y, sum.z, sum.w};
+    const bool row_ok = m < L.d;
+    float* out = L.G ? L.G + (size_t)sample * L.d * L.p : nullptr;
+    if constexpr (INST) {
+        float sq = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sq += (row_ok && n + j < L.p) ? r[j] * r[j] : 0.f;
+        const float tot = block_sum_256(sq, red);
+        if (threadIdx.x == 0) args.part[(size_t)L.part_off + (size_t)tg * CH + ch] = tot;
+    }
+    if (out && row_ok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (n + j < L.p) out[(size_t)m * L.p + n + j] = r[j];
+    }
 }
 
 }  // namespace
@@ -1001,6 +1078,19 @@ GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool ali
     // with 32-bit buffer offsets.
     if (bf16 && (rows + 3 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) return GemmVariant::Wide;
     return GemmVariant::Vec;
+}
+
+hipError_t launch_split_reduce(const GemmArgs& args, int n_wg, bool inst_norm, GemmVariant v,
+                               hipStream_t s) {
+    if (n_wg <= 0) return hipSuccess;
+    const dim3 grid(n_wg), block(256);
+    if (inst_norm && v == GemmVariant::Wide)
+        hipLaunchKernelGGL((split_reduce_kernel<kBM, kBN, true>), grid, block, 0, s, args);
+    else if (!inst_norm && (v == GemmVariant::Grad || v == GemmVariant::GradDL))
+        hipLaunchKernelGGL((split_reduce_kernel<kGM, kGN, false>), grid, block, 0, s, args);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,

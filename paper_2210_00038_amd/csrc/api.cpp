@@ -76,14 +76,39 @@ struct NormPlan {
     int64_t npart;      // partials per sample
     int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads;
                         // instantiation: bk::GemmVariant
+    int64_t tiles = 0;  // instantiation: output tiles per sample
+    int64_t ksplit = 1; // instantiation: K slices per tile (wide kernel only)
 };
+
+// Tile shape and slice-reduction chunks of the split-capable kernels.
+constexpr int64_t kWideTile = 256 * 128;        // agemm_bf16_kernel
+constexpr int64_t kGradTile = 256 * 256;        // agrad_* kernels
+constexpr int64_t kWideChunks = kWideTile / bk::kSplitRedWG;
+constexpr int64_t kGradChunks = kGradTile / bk::kSplitRedWG;
+
+// K slices of an instantiated norm on the wide kernel: when a layer gives
+// fewer than 128 workgroups (few samples, few tiles, long T), cut each
+// per-sample GEMM into slices of at least 4 stages, towards 256 workgroups.
+int64_t inst_ksplit(int64_t B, int64_t tiles, int64_t T) {
+    const int64_t wgs = B * tiles, nst = cdiv(T, 64);
+    if (wgs == 0 || wgs >= 128 || nst < 8) return 1;
+    return std::max<int64_t>(1, std::min(cdiv(256, wgs), nst / 4));
+}
+
+// K slices of a clipped-gradient tile (agrad kernels): a layer with fewer than
+// 8 output tiles and at least 64 stages gets slices of about 32 stages.
+int64_t grad_ksplit(int64_t tiles, int64_t nst) {
+    if (tiles >= 8 || nst < 64) return 1;
+    return std::min<int64_t>(256, cdiv(nst, 32));
+}
 
 void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
     const size_t es = elem_bytes(dt);
     if (np.path == Path::Inst) {
         const auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
         np.var = (int)v;
-        np.npart = cdiv(L.d, bk::gemm_tile_m(v)) * cdiv(L.p, bk::gemm_tile_n(v));
+        np.tiles = cdiv(L.d, bk::gemm_tile_m(v)) * cdiv(L.p, bk::gemm_tile_n(v));
+        np.npart = np.tiles;
     } else {
         const int64_t nsb = cdiv(L.T, bk::kSuper);
         np.npart = nsb * (nsb + 1) / 2;
@@ -96,6 +121,25 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
     }
 }
 
+// Workgroup count, and the K split of instantiated norms on the wide kernel
+// (a split layer reports one partial per slice-reduction chunk).
+void finish_norm_plan(NormPlan& np, const bk_layer& L, int64_t B) {
+    if (np.path == Path::Inst && np.var == (int)bk::GemmVariant::Wide) {
+        np.ksplit = inst_ksplit(B, np.tiles, L.T);
+        if (np.ksplit > 1) np.npart = np.tiles * kWideChunks;
+    }
+    np.nwg = np.path == Path::Inst ? B * np.tiles * np.ksplit : B * np.npart;
+}
+
+// Partial sums of a layer's norm (floats) and its K-split partial tiles (floats).
+size_t norm_part_floats(const NormPlan& np, int64_t B) { return (size_t)(B * np.npart); }
+size_t norm_tile_floats(const NormPlan& np, int64_t B) {
+    return np.ksplit > 1 ? (size_t)(B * np.tiles * np.ksplit * kWideTile) : 0;
+}
+size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
+    return align_up(norm_part_floats(np, B) * sizeof(float)) + norm_tile_floats(np, B) * sizeof(float);
+}
+
 NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
     if (L.kind == BK_EMBEDDING) {
@@ -104,12 +148,8 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
         np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
     }
     set_norm_variant(np, L, dt);
-    np.nwg = B * np.npart;
+    finish_norm_plan(np, L, B);
     return np;
-}
-
-size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
-    return align_up((size_t)(B * np.npart) * sizeof(float));
 }
 
 size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t V) {
@@ -178,16 +218,21 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     float* part = static_cast<float*>(ws);
     const bool bf16 = dt == BK_BF16;
 
-    // Batches of same-kernel layers; each batch is one launch.
-    struct Item { int64_t l; NormPlan np; int64_t part_off; };
+    // Batches of same-kernel layers; each batch is one launch.  Workspace:
+    // every layer's partial sums (aligned runs), then the K-split partial
+    // tiles of the split instantiated layers.
+    struct Item { int64_t l; NormPlan np; int64_t part_off; int64_t tile_off; };
     std::vector<Item> items;
     items.reserve((size_t)n);
-    int64_t off = 0;
+    int64_t off = 0, toff = 0;
     for (int64_t l = 0; l < n; ++l) {
         const NormPlan np = norm_plan(layers[l], dt, B);
-        items.push_back({l, np, off});
-        off += (int64_t)(norm_ws_bytes(np, B) / sizeof(float));
+        items.push_back({l, np, off, toff});
+        off += (int64_t)(align_up(norm_part_floats(np, B) * sizeof(float)) / sizeof(float));
+        toff += (int64_t)(norm_tile_floats(np, B) / kWideTile);
     }
+    float* tiles = part + off;
+    if (toff > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many partial tiles", fn);
 
     auto flush_ghost = [&](std::vector<const Item*>& v, bool embed, bool vec) -> bk_status {
         if (v.empty()) return BK_OK;
@@ -222,9 +267,11 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
         a.B = (int32_t)B;
         a.C = nullptr;
         a.part = part;
-        int64_t wg = 0;
+        a.tiles = tiles;
+        int64_t wg = 0, red = 0;
         for (size_t k = 0; k < v.size(); ++k) {
             const bk_layer& L = layers[v[k]->l];
+            const NormPlan& np = v[k]->np;
             bk::GemmLayer& g = a.L[k];
             g.a = L.x;
             g.g = L.g;
@@ -236,10 +283,16 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(var)));
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
-            wg += v[k]->np.nwg;
+            g.ksplit = (int32_t)np.ksplit;
+            g.ptile_off = (int32_t)v[k]->tile_off;
+            g.red_begin = (int32_t)red;
+            wg += np.nwg;
+            if (np.ksplit > 1) red += B * np.tiles * kWideChunks;
         }
-        if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        if (wg > INT32_MAX || red > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
         hipError_t e = bk::launch_gemm(a, (int)wg, bf16, true, bk::GemmVariant(var), s);
+        if (e == hipSuccess && red > 0)
+            e = bk::launch_split_reduce(a, (int)red, true, bk::GemmVariant(var), s);
         v.clear();
         return e == hipSuccess ? BK_OK : hip_fail(e, "instantiated norm launch");
     };
@@ -281,12 +334,37 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     return BK_OK;
 }
 
-size_t weighted_grads_ws(const bk_layer* layers, int64_t n, int64_t B) {
-    size_t tot = 0;
-    for (int64_t l = 0; l < n; ++l)
-        if (layers[l].kind == BK_EMBEDDING)
-            tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T, layers[l].d));
-    return tot;
+// Kernel variant of a linear layer's clipped gradient: the Wide layers with
+// T >= 64 run on the 256 x 256 kernels, with the weights on the accumulators
+// when the stage height divides T (and B fits the kernel's LDS table), else
+// on g.
+bk::GemmVariant grad_variant(const bk_layer& L, bool bf16, int64_t B) {
+    const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
+    if (v != bk::GemmVariant::Wide || L.T < 64) return v;
+    return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL : bk::GemmVariant::Grad;
+}
+
+// Tiles and K slices of a linear layer's clipped gradient on variant v.
+struct GradPlan { int64_t tm, tn, ksplit; };
+GradPlan grad_plan(const bk_layer& L, bk::GemmVariant v, int64_t B) {
+    GradPlan g{cdiv(L.d, bk::gemm_tile_m(v)), cdiv(L.p, bk::gemm_tile_n(v)), 1};
+    if (v == bk::GemmVariant::Grad || v == bk::GemmVariant::GradDL) {
+        const int64_t rows = v == bk::GemmVariant::Grad ? 64 : bk::kDLStageRows;
+        g.ksplit = grad_ksplit(g.tm * g.tn, cdiv(B * L.T, rows));
+    }
+    return g;
+}
+
+size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    size_t tot = 0, tiles = 0;
+    for (int64_t l = 0; l < n; ++l) {
+        const bk_layer& L = layers[l];
+        if (L.kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, L.T, L.d));
+        if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
+        const GradPlan g = grad_plan(L, grad_variant(L, dt == BK_BF16, B), B);
+        if (g.ksplit > 1) tiles += (size_t)(g.tm * g.tn * g.ksplit * kGradTile) * sizeof(float);
+    }
+    return std::max(tot, tiles);
 }
 
 // Appends one weighted-sum job (P [B, n] -> G [n]) to a grouped launch.
@@ -311,39 +389,38 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     for (int64_t l = 0; l < n; ++l)
         if ((st = check_layer(fn, layers[l], l, B, true)) != BK_OK) return st;
     if (B > 0 && !C) return fail(BK_ERR_INVALID_VALUE, "%s: NULL clip factors", fn);
-    const size_t need = weighted_grads_ws(layers, n, B);
+    const size_t need = weighted_grads_ws(layers, n, dt, B);
     if (ws_bytes < need || (need > 0 && !ws))
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
     const bool bf16 = dt == BK_BF16;
 
-    // The clipped gradient runs the Wide layers with T >= 64 on the 256 x 256
-    // kernels: with the weights on the accumulators when the stage height
-    // divides T (and B fits the kernel's LDS table), else on g.
-    auto grad_variant = [&](const bk_layer& L) {
-        const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
-        if (v != bk::GemmVariant::Wide || L.T < 64) return v;
-        return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL
-                                                                 : bk::GemmVariant::Grad;
-    };
+    // Grouped launches by kernel variant.  Layers with few output tiles run
+    // K-split (grad_plan); their partial tiles sit in the workspace (launches
+    // follow each other on the stream, so each starts from offset 0).
     for (int var = 0; var < 5; ++var) {
         bk::GemmArgs a{};
         a.B = (int32_t)B;
         a.C = C;
         a.part = nullptr;
-        int64_t wg = 0;
+        a.tiles = static_cast<float*>(ws);
+        int64_t wg = 0, ptile = 0, red = 0;
         auto flush = [&]() -> bk_status {
             if (a.n == 0) return BK_OK;
-            if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+            if (wg > INT32_MAX || red > INT32_MAX || ptile > INT32_MAX)
+                return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
             hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, bk::GemmVariant(var), s);
+            if (e == hipSuccess && red > 0)
+                e = bk::launch_split_reduce(a, (int)red, false, bk::GemmVariant(var), s);
             a.n = 0;
-            wg = 0;
+            wg = ptile = red = 0;
             return e == hipSuccess ? BK_OK : hip_fail(e, "clipped gradient launch");
         };
         for (int64_t l = 0; l < n; ++l) {
             const bk_layer& L = layers[l];
             if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
-            const auto v = grad_variant(L);
+            const auto v = grad_variant(L, bf16, B);
             if ((int)v != var) continue;
+            const GradPlan gp = grad_plan(L, v, B);
             bk::GemmLayer& g = a.L[a.n++];
             g.a = L.x;
             g.g = L.g;
@@ -352,11 +429,18 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(v));
-            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(v));
+            g.tm = (int32_t)gp.tm;
+            g.tn = (int32_t)gp.tn;
             g.wg_begin = (int32_t)wg;
             g.part_off = 0;
-            wg += (int64_t)g.tm * g.tn;
+            g.ksplit = (int32_t)gp.ksplit;
+            g.ptile_off = (int32_t)ptile;
+            g.red_begin = (int32_t)red;
+            wg += gp.tm * gp.tn * gp.ksplit;
+            if (gp.ksplit > 1) {
+                ptile += gp.tm * gp.tn * gp.ksplit;
+                red += gp.tm * gp.tn * kGradChunks;
+            }
             if (a.n == bk::kMaxGemm && (st = flush()) != BK_OK) return st;
         }
         if ((st = flush()) != BK_OK) return st;
@@ -462,7 +546,7 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
     NormPlan np{};
     np.path = want;
     set_norm_variant(np, L, dt);
-    np.nwg = B * np.npart;
+    finish_norm_plan(np, L, B);
     const size_t need = norm_ws_bytes(np, B);
     if (ws_bytes < need || (need > 0 && !ws))
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
@@ -484,7 +568,13 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.p = (int32_t)L.p;
         g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bk::GemmVariant(np.var)));
         g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(np.var)));
+        g.ksplit = (int32_t)np.ksplit;
+        a.tiles = part + align_up(norm_part_floats(np, B) * sizeof(float)) / sizeof(float);
         e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, bk::GemmVariant(np.var), s);
+        const int64_t red = np.ksplit > 1 ? B * np.tiles * kWideChunks : 0;
+        if (red > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        if (e == hipSuccess && red > 0)
+            e = bk::launch_split_reduce(a, (int)red, true, bk::GemmVariant(np.var), s);
     } else {
         bk::GhostArgs a{};
         a.n = 1;
@@ -537,10 +627,18 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
             const int64_t nsb = cdiv(T, bk::kSuper);
             return align_up((size_t)(B * (nsb * (nsb + 1) / 2)) * sizeof(float));
         }
-        case BK_OP_INST_NORM:   // upper bound over the tile shapes (alignment is not known here)
-            return align_up((size_t)(B * cdiv(d, bk::kTile) * cdiv(p, bk::kTile)) * sizeof(float));
-        case BK_OP_WEIGHTED_GRAD:
-            return 0;
+        case BK_OP_INST_NORM: {  // upper bound over the kernels (alignment is not known here)
+            const size_t small = align_up((size_t)(B * cdiv(d, bk::kTile) * cdiv(p, bk::kTile)) * sizeof(float));
+            L.kind = BK_LINEAR;
+            NormPlan np{};
+            np.path = Path::Inst;
+            set_norm_variant(np, L, dt);     // NULL pointers count as aligned
+            finish_norm_plan(np, L, B);
+            return std::max(small, norm_ws_bytes(np, B));
+        }
+        case BK_OP_WEIGHTED_GRAD:   // 16-byte aligned rows assumed (an upper bound)
+            L.kind = BK_LINEAR;
+            return weighted_grads_ws(&L, 1, dt, B);
         case BK_OP_EMBED_WEIGHTED_GRAD:
             return embed_grad_ws_bytes(B, T, d);
         default:
@@ -694,7 +792,7 @@ size_t bk_weighted_grads_workspace_size(const bk_layer* layers, int64_t n, bk_dt
     if (n < 0 || (n > 0 && !layers) || B < 0 || check_dtype("", dt) != BK_OK) return 0;
     for (int64_t l = 0; l < n; ++l)
         if (check_dims("", B, layers[l].T, layers[l].d, layers[l].p) != BK_OK) return 0;
-    return weighted_grads_ws(layers, n, B);
+    return weighted_grads_ws(layers, n, dt, B);
 }
 
 bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, bk_dtype dt,

@@ -42,15 +42,24 @@ struct GemmLayer {
     int32_t tm, tn;     // output tiles along d and p
     int32_t wg_begin;
     int32_t part_off;   // instantiated norm: first partial of this layer
-    int32_t pad;
+    // K split (layers with few output tiles): each tile's contraction is cut
+    // into ksplit slices of whole stages, one workgroup each, which write
+    // float32 partial tiles to GemmArgs::tiles (this layer's from tile
+    // ptile_off on, [sample][tile][slice]); a second kernel adds the slices in
+    // order, its workgroups for this layer starting at red_begin.
+    int32_t ksplit;     // 1: no split
+    int32_t ptile_off;
+    int32_t red_begin;
 };
-constexpr int kMaxGemm = 56;
+constexpr int kMaxGemm = 48;
 struct GemmArgs {
     int32_t n, B;
     const float* C;     // [B] clip factors (clipped gradient)
     float* part;        // partial sums (instantiated norm), [layer][sample][tile]
+    float* tiles;       // K-split partial tiles
     GemmLayer L[kMaxGemm];
 };
+constexpr int kSplitRedWG = 1024;   // tile elements per workgroup of the slice reduction
 
 // ---- fixed-order reduction of partial sums ---------------------------------
 struct ReduceLayer {
@@ -125,6 +134,12 @@ hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, 
                         hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,
                        hipStream_t s);
+// Adds the K slices of every split layer of `args` (launched with
+// launch_gemm) in order: into G (clipped gradient), or squared into the norm
+// partials and optionally kept in G (instantiated norm).  n_wg: the sum of
+// the split layers' reduction workgroups.
+hipError_t launch_split_reduce(const GemmArgs& args, int n_wg, bool inst_norm, GemmVariant v,
+                               hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& args, int n_threads, hipStream_t s);
 hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, float R, float gamma,
                        float* C, float* total_sq, hipStream_t s);

@@ -359,3 +359,39 @@ def test_private_grad_mixopt_matches_oracle(bk, dtype):
         for l in range(len(layers)):
             assert _frob(G[l], ref["G"][l]) <= GRAD_TOL[dtype], l
             assert _frob(G[l], G_base[l]) <= GRAD_TOL[dtype], l
+
+
+# ------------------------------------------------ K-split (few tiles, long K)
+# Layers with few output tiles and a long contraction (convolutions at image
+# scale, skinny adapters) cut each tile's K range into slices whose partial
+# tiles are added in order by a second kernel.
+@pytest.mark.parametrize("B,T,d,p", [
+    (2, 2048, 152, 64),      # one 256 x 128 tile per sample, 8 slices
+    (3, 1000, 96, 200),      # ragged T, one tile, 4 slices
+    (1, 4096, 520, 136),     # several tiles, one sample
+])
+def test_inst_norm_k_split(bk, B, T, d, p):
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=T + d)
+    ref = oracle.linear_norm_sq(a, g)
+    assert _rel(bk.bk_inst_norm(a.to(DEV), g.to(DEV)).cpu().numpy(), ref) <= NORM_TOL[torch.bfloat16]
+    norm, P = bk.bk_per_sample_grads(a.to(DEV), g.to(DEV))
+    assert _rel(norm.cpu().numpy(), ref) <= NORM_TOL[torch.bfloat16]
+    ref_P = oracle.per_sample_grads(a, g)
+    P = P.cpu().numpy()
+    for i in range(B):
+        assert _frob(P[i], ref_P[i]) <= GRAD_TOL[torch.bfloat16], i
+
+
+@pytest.mark.parametrize("B,T,d,p,zero", [
+    (4, 1024, 152, 64, []),          # LDS-DMA kernel (32 | T), one tile, 4 slices
+    (8, 1000, 152, 64, []),          # register-staged kernel (T >= 64), one tile, 4 slices
+    (6, 512, 264, 136, [0, 3]),      # zero weights at slice starts and inside
+    (16, 256, 40, 24, [15]),         # tiny output, many slices
+])
+def test_weighted_grad_k_split(bk, B, T, d, p, zero):
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B + T)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(B)) + 0.1
+    C[zero] = 0.0
+    ref = oracle.weighted_grad(a, g, C)
+    G = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), C.to(DEV)).cpu().numpy()
+    assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
