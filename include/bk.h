@@ -158,6 +158,25 @@ bk_status bk_per_sample_grads(const void* a, const void* g, bk_dtype dt, int64_t
 bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, float* G,
                           void* stream);
 
+/* A 2-D convolution as a generalized linear layer (App. B: d = input
+ * channels x kernel size, p = output channels, T = output height x width).
+ * bk_unfold writes the layer's activation a:
+ *   x [B, C, H, W] (dtype dt, NCHW) -> a [B, T, ld], T = Ho Wo,
+ *   Ho = (H + 2 pad - kh) / stride + 1, Wo = (W + 2 pad - kw) / stride + 1,
+ *   token t = oh Wo + ow, column c kh kw + i kw + j =
+ *   x[b, c, oh stride + i - pad, ow stride + j - pad] (0 outside the image),
+ *   columns d = C kh kw .. ld-1 zero.  ld >= d; with ld a multiple of 8 the
+ *   bf16 rows take the 16-byte kernel paths, and the layer's gradient rows
+ *   d .. ld-1 come out zero.  kh, kw, stride >= 1, pad >= 0, Ho, Wo >= 1.
+ * bk_tokens_from_nchw writes the layer's output gradient token-major:
+ *   y [B, C, H, W] -> out [B, H W, C] (same dtype).
+ * Both are copies (bit-exact), device buffers, no workspace. */
+bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H, int64_t W,
+                    int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t ld, void* a,
+                    void* stream);
+bk_status bk_tokens_from_nchw(const void* y, bk_dtype dt, int64_t B, int64_t C, int64_t H,
+                              int64_t W, void* out, void* stream);
+
 /* Ghost norm of an embedding layer (Section 2.1 names the embedding among the
  * generalized linear layers; App. D.1 lists it as ghost-norm only).  Its input
  * a_i is the one-hot encoding of the ids x_i, so a_i a_i^T is the token-id

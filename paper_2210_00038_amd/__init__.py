@@ -25,9 +25,10 @@ __all__ = [
     "BK_OP_GHOST_NORM", "BK_OP_INST_NORM", "BK_OP_EMBED_GHOST_NORM", "BK_OP_WEIGHTED_GRAD",
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_per_sample_grads", "bk_weighted_sum",
+    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
     "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
+    "conv_out_size",
     "bk_layer_norms_workspace_size", "bk_weighted_grads_workspace_size",
     "bk_private_grad_workspace_size", "bk_status_string", "bk_last_error", "bk_version",
 ]
@@ -45,7 +46,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbk.so")
 # Every symbol include/bk.h declares.
 EXPORTS = (
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_per_sample_grads", "bk_weighted_sum",
+    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
     "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
     "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_status_string",
@@ -84,6 +85,8 @@ _SIG = {
     "bk_per_sample_grads": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _sz,
                                   _vp]),
     "bk_weighted_sum": (_st, [_vp, _vp, _i64, _i64, _vp, _vp]),
+    "bk_unfold": (_st, [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _vp, _vp]),
+    "bk_tokens_from_nchw": (_st, [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp]),
     "bk_clip_factors": (_st, [_vp, _i64, _i64, ctypes.c_int, _f32, _f32, _vp, _vp, _vp]),
     "bk_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_embed_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp,
@@ -241,6 +244,36 @@ def bk_weighted_sum(P, C, G=None, stream=None) -> torch.Tensor:
     n = G.numel()
     _check(lib.bk_weighted_sum(_ptr(P), _ptr(C), B, n, _ptr(G), _stream(stream)), "bk_weighted_sum")
     return G
+
+
+def conv_out_size(n: int, k: int, stride: int, pad: int) -> int:
+    return (n + 2 * pad - k) // stride + 1
+
+
+def bk_unfold(x, kh: int, kw: int, stride: int = 1, pad: int = 0, ld: int = 0, a=None, stream=None):
+    """Unfolded input of a 2-D convolution: x [B,C,H,W] -> a [B, Ho Wo, ld] (ld = 0: C kh kw)."""
+    _dev(x, "x")
+    if x.dim() != 4 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [B, C, H, W] tensor")
+    B, C, H, W = x.shape
+    Ho, Wo = conv_out_size(H, kh, stride, pad), conv_out_size(W, kw, stride, pad)
+    ld = ld or C * kh * kw
+    a = _out(a, (B, Ho * Wo, ld), x.device, dtype=x.dtype)
+    _check(lib.bk_unfold(_ptr(x), _dtype_code(x), B, C, H, W, kh, kw, stride, pad, ld, _ptr(a),
+                         _stream(stream)), "bk_unfold")
+    return a
+
+
+def bk_tokens_from_nchw(y, out=None, stream=None):
+    """Token-major output gradient of a convolution: y [B,C,H,W] -> [B, H W, C]."""
+    _dev(y, "y")
+    if y.dim() != 4 or not y.is_contiguous():
+        raise ValueError("y must be a contiguous [B, C, H, W] tensor")
+    B, C, H, W = y.shape
+    out = _out(out, (B, H * W, C), y.device, dtype=y.dtype)
+    _check(lib.bk_tokens_from_nchw(_ptr(y), _dtype_code(y), B, C, H, W, _ptr(out), _stream(stream)),
+           "bk_tokens_from_nchw")
+    return out
 
 
 def bk_embed_ghost_norm(ids, g, V: int, norm_sq=None, ws=None, stream=None) -> torch.Tensor:

@@ -700,6 +700,48 @@ bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, 
     return e == hipSuccess ? BK_OK : hip_fail(e, "weighted sum launch");
 }
 
+bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H, int64_t W,
+                    int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t ld, void* a,
+                    void* stream) {
+    const char* fn = "bk_unfold";
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if (B < 0 || C < 0 || H < 0 || W < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (kh < 1 || kw < 1 || stride < 1 || pad < 0)
+        return fail(BK_ERR_INVALID_VALUE, "%s: kernel, stride >= 1 and pad >= 0 required", fn);
+    if (H > (1 << 20) || W > (1 << 20) || kh > (1 << 20) || kw > (1 << 20) || pad > (1 << 20) || C > (1 << 24))
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: dimensions too large", fn);
+    const int64_t Ho = (H + 2 * pad - kh) / stride + 1, Wo = (W + 2 * pad - kw) / stride + 1;
+    if (H + 2 * pad < kh || W + 2 * pad < kw || Ho < 1 || Wo < 1)
+        return fail(BK_ERR_INVALID_VALUE, "%s: kernel larger than the padded image", fn);
+    const int64_t d = C * kh * kw;
+    if (ld < d) return fail(BK_ERR_INVALID_VALUE, "%s: ld %lld < C kh kw = %lld", fn, (long long)ld, (long long)d);
+    const int64_t T = Ho * Wo;
+    if (B > 0 && T > INT64_MAX / B / std::max<int64_t>(ld, 1))
+        return fail(BK_ERR_INVALID_VALUE, "%s: output size overflows", fn);
+    if (B * T * ld == 0) return BK_OK;
+    if (!x || !a) return fail(BK_ERR_INVALID_VALUE, "%s: NULL pointer", fn);
+    const bk::UnfoldShape sh{B, C, H, W, kh, kw, stride, pad, Ho, Wo, T, ld};
+    hipError_t e = bk::launch_unfold(x, a, sh, dt == BK_BF16, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "unfold launch");
+}
+
+bk_status bk_tokens_from_nchw(const void* y, bk_dtype dt, int64_t B, int64_t C, int64_t H, int64_t W,
+                              void* out, void* stream) {
+    const char* fn = "bk_tokens_from_nchw";
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if (B < 0 || C < 0 || H < 0 || W < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (B > 65535 || C > ((int64_t)1 << 36) || H * W > ((int64_t)1 << 36))
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: dimensions too large", fn);
+    if (B * C * H * W == 0) return BK_OK;
+    if (!y || !out) return fail(BK_ERR_INVALID_VALUE, "%s: NULL pointer", fn);
+    if ((H * W + 31) / 32 > INT32_MAX || (C + 31) / 32 > 65535)
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+    hipError_t e = bk::launch_tokens(y, out, B, C, H * W, dt == BK_BF16, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "token transpose launch");
+}
+
 bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B, int64_t T,
                               int64_t p, int64_t V, float* norm_sq, void* ws, size_t ws_bytes,
                               void* stream) {

@@ -9,6 +9,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace bk {
 
 constexpr int kSuper = 128;   // ghost norm: rows of a super block of the T x T Gram
@@ -129,6 +131,13 @@ struct WsumArgs {
 };
 constexpr int kWsumPerWG = 1024;    // elements per workgroup
 
+// ---- convolution data preparation ------------------------------------------
+struct UnfoldShape {
+    int64_t B, C, H, W;         // input x [B, C, H, W]
+    int64_t kh, kw, stride, pad;
+    int64_t Ho, Wo, T, ld;      // output a [B, T = Ho Wo, ld]
+};
+
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
@@ -145,6 +154,8 @@ hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, flo
                        float* C, float* total_sq, hipStream_t s);
 hipError_t launch_noise(const NoiseArgs& args, int n_wg, hipStream_t s);
 hipError_t launch_wsum(const WsumArgs& args, int n_wg, hipStream_t s);
+hipError_t launch_unfold(const void* x, void* a, const UnfoldShape& s, bool bf16, hipStream_t st);
+hipError_t launch_tokens(const void* y, void* out, int64_t B, int64_t C, int64_t HW, bool bf16, hipStream_t st);
 hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q0, int64_t nq,
                              uint32_t* out, hipStream_t s);
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,

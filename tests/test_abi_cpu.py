@@ -170,3 +170,19 @@ def test_mixopt_validation():
     assert L.bk_weighted_sum(FAKE, FAKE, 3, 10, None, None) == bk.BK_ERR_INVALID_VALUE
     assert L.bk_weighted_sum(0x10002, FAKE, 3, 10, FAKE, None) == bk.BK_ERR_INVALID_VALUE
     assert L.bk_weighted_sum(None, None, 3, 0, None, None) == bk.BK_OK             # nothing to do
+
+
+def test_conv_prep_validation():
+    L = bk.lib
+    # kernel larger than the padded image, bad stride / pad, ld < C kh kw
+    assert L.bk_unfold(FAKE, bk.BK_BF16, 1, 3, 4, 4, 7, 7, 1, 0, 147, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_unfold(FAKE, bk.BK_BF16, 1, 3, 8, 8, 3, 3, 0, 1, 27, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_unfold(FAKE, bk.BK_BF16, 1, 3, 8, 8, 3, 3, 1, -1, 27, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_unfold(FAKE, bk.BK_BF16, 1, 3, 8, 8, 3, 3, 1, 1, 26, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_unfold(None, bk.BK_BF16, 1, 3, 8, 8, 3, 3, 1, 1, 32, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_unfold(None, bk.BK_BF16, 0, 3, 8, 8, 3, 3, 1, 1, 32, None, None) == bk.BK_OK        # empty
+    assert L.bk_unfold(FAKE, 9, 1, 3, 8, 8, 3, 3, 1, 1, 32, FAKE, None) == bk.BK_ERR_INVALID_VALUE  # dtype
+    assert L.bk_tokens_from_nchw(FAKE, bk.BK_F32, -1, 3, 4, 4, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_tokens_from_nchw(None, bk.BK_F32, 2, 3, 4, 4, FAKE, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_tokens_from_nchw(None, bk.BK_F32, 2, 0, 4, 4, None, None) == bk.BK_OK
+    assert bk.conv_out_size(224, 7, 2, 3) == 112 and bk.conv_out_size(56, 1, 2, 0) == 28

@@ -395,3 +395,59 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     ref = oracle.weighted_grad(a, g, C)
     G = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), C.to(DEV)).cpu().numpy()
     assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
+
+
+# ------------------------------------------- convolution layers via unfold
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,C,H,W,k,stride,pad,ld", [
+    (2, 3, 17, 13, 7, 2, 3, 152),     # conv1-like: d = 147 padded to 152
+    (3, 8, 9, 9, 3, 1, 1, 0),         # d = 72, no padding
+    (1, 5, 12, 10, 1, 2, 0, 8),       # 1 x 1 stride 2 (downsample), d = 5 -> 8
+    (2, 4, 6, 7, 3, 2, 0, 40),        # no padding, odd output
+])
+def test_unfold_and_tokens_bit_exact(bk, dtype, B, C, H, W, k, stride, pad, ld):
+    gen = torch.Generator().manual_seed(C * H + k)
+    x = torch.randn(B, C, H, W, generator=gen).to(dtype)
+    a = bk.bk_unfold(x.to(DEV), k, k, stride, pad, ld).cpu()
+    ref = oracle.unfold(x.float().numpy(), k, k, stride, pad, ld)       # exact copies of dtype values
+    assert np.array_equal(a.float().numpy(), ref)
+    y = torch.randn(B, C, H, W, generator=gen).to(dtype)
+    t = bk.bk_tokens_from_nchw(y.to(DEV)).cpu()
+    assert np.array_equal(t.float().numpy(), oracle.tokens_from_nchw(y.float().numpy()))
+
+
+def test_conv_stack_matches_oracle(bk):
+    """A small ResNet-shaped conv stack through unfold + token-major gradients +
+    the BK path (norms by the layerwise rule, clipping, clipped gradients)."""
+    B, dtype = 4, torch.bfloat16
+    # (C_in, C_out, k, stride, pad, H_in): early layers instantiate, late ones ghost
+    convs = [(3, 16, 7, 2, 3, 64), (16, 16, 3, 1, 1, 32), (16, 32, 3, 2, 1, 32), (32, 64, 3, 2, 1, 16),
+             (64, 128, 1, 1, 0, 4)]
+    gen = torch.Generator().manual_seed(3)
+    specs, ref_in, Gs, layers = [], [], [], []
+    for (ci, co, k, s, pd, h) in convs:
+        x = torch.randn(B, ci, h, h, generator=gen).to(dtype)
+        ho = bk.conv_out_size(h, k, s, pd)
+        dy = (torch.randn(B, co, ho, ho, generator=gen) * 1e-2).to(dtype)
+        d = ci * k * k
+        ld = (d + 7) // 8 * 8
+        a = bk.bk_unfold(x.to(DEV), k, k, s, pd, ld)
+        g = bk.bk_tokens_from_nchw(dy.to(DEV))
+        G = torch.empty(ld, co, device=DEV)
+        specs.append({"kind": bk.BK_LINEAR, "x": a, "g": g, "G": G})
+        Gs.append(G)
+        ref_in.append((oracle.unfold(x.float().numpy(), k, k, s, pd, ld), oracle.tokens_from_nchw(dy.float().numpy())))
+        layers.append(wl.Layer("linear", ho * ho, ld, co))
+    arr = bk.make_layers(specs)
+    n = len(specs)
+    norm_sq, C, tot = torch.empty(n, B, device=DEV), torch.empty(B, device=DEV), torch.empty(B, device=DEV)
+    bk.bk_private_grad(arr, n, bk.BK_BF16, B, bk.BK_CLIP_ABADI, 1e-2, 0.0, 0.0, 1, 0, norm_sq, C, tot)
+    torch.cuda.synchronize()
+    ref = oracle.bk_stack(layers, ref_in, "abadi", 1e-2, 0.0, 0.0, 1, with_noise=False)
+    assert ref["paths"][:2] == ["inst", "inst"] and ref["paths"][-1] == "ghost"
+    assert _rel(norm_sq.cpu().numpy(), ref["norms"]) <= NORM_TOL[dtype]
+    assert _rel(C.cpu().numpy(), ref["C"]) <= NORM_TOL[dtype]
+    for l, (ci, co, k, s, pd, h) in enumerate(convs):
+        G = Gs[l].cpu().numpy()
+        assert _frob(G, ref["G"][l]) <= GRAD_TOL[dtype], l
+        assert not np.any(G[ci * k * k:]), l                 # padded columns of a give zero rows
