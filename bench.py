@@ -3,6 +3,7 @@
 One step = the whole path of Algorithm 1 after book-keeping, over one batch of
 a synthetic layer stack whose inputs already sit in HBM:
 
+    convolution layers: unfold x and make dL/ds token-major        -> a, g
     per-layer per-sample norms (ghost / instantiated / embedding)  -> [L, B]
     clip factors                                                   -> [B]
     clip-weighted gradients of every layer                         -> G_l
@@ -15,7 +16,7 @@ dominant kernel measured with HIP events on the launch stream over the timed
 steps, and the float64 CPU oracle timed on a bounded sample of the same
 workload on the host.
 
-    python bench.py [--steps K] [--warmup W] [--workload N] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--workload N] [--mixopt] [--gpus 1]
 """
 from __future__ import annotations
 
@@ -38,22 +39,36 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense MFMA
 
 
+def true_d(L: wl.Layer) -> int:
+    """Input width of the layer's linear view without the zero padding columns."""
+    return L.conv[0] * L.conv[1] ** 2 if L.kind == "conv" else L.d
+
+
 def algorithmic_work(w: wl.Workload, mixopt: bool = False):
     """Per-step algorithmic flops / bytes of each phase (paper's per-module costs).
     mixopt: instantiated layers keep their per-sample gradients (written by the
     norm phase, 4Bpd bytes) and form G as their weighted sum (2Bpd flops,
-    reading 4Bpd and writing 4pd bytes) instead of the 2BTpd GEMM."""
+    reading 4Bpd and writing 4pd bytes) instead of the 2BTpd GEMM.
+    Convolution layers count as linear layers of width d = C_in k^2 (App. B);
+    their preparation reads x and dL/ds once and writes a and g once."""
     es = 2 if w.dtype == "bf16" else 4
     B = w.B
     out = {"norm_flops": 0.0, "norm_bytes": 0.0, "gemm_flops": 0.0, "gemm_bytes": 0.0,
-           "noise_elems": 0.0, "ghost_layers": 0, "inst_layers": 0, "embed_layers": 0}
-    for L in w.layers:
+           "noise_elems": 0.0, "prep_bytes": 0.0, "ghost_layers": 0, "inst_layers": 0,
+           "embed_layers": 0, "conv_layers": 0}
+    for L0 in w.layers:
+        L = L0
+        if L0.kind == "conv":
+            cin, k, stride, pad, hin = L0.conv
+            out["conv_layers"] += 1
+            out["prep_bytes"] += B * es * (cin * hin * hin + L0.T * true_d(L0) + 2 * L0.T * L0.p)
+            L = wl.Layer("linear", L0.T, true_d(L0), L0.p)
         if L.kind == "embed":
             out["embed_layers"] += 1
             out["norm_bytes"] += B * L.T * (L.p * es + 8)
             out["gemm_bytes"] += B * L.T * (L.p * es + 8) + 4.0 * L.d * L.p
         else:
-            ghost = 2 * L.T * L.T < L.p * L.d
+            ghost = 2 * L0.T * L0.T < L0.p * L0.d        # the decision sees the padded width
             if ghost:
                 out["ghost_layers"] += 1
                 out["norm_flops"] += 2.0 * B * L.T * L.T * (L.p + L.d)       # ghost norm, App. B.4
@@ -68,14 +83,23 @@ def algorithmic_work(w: wl.Workload, mixopt: bool = False):
             else:
                 out["gemm_flops"] += 2.0 * B * L.T * L.p * L.d               # a^T diag(C) g, App. B.3
                 out["gemm_bytes"] += B * L.T * (L.d + L.p) * es + 4.0 * L.d * L.p
-        out["noise_elems"] += float(L.d) * L.p
+        out["noise_elems"] += float(L0.d) * L0.p
     return out
 
 
 def make_inputs(w: wl.Workload, dev):
-    ins = [wl.draw_layer(w, l, device=dev) for l in range(len(w.layers))]
+    """Per layer the (a, g) the path reads, its G, and for convolution layers
+    the raw NCHW (x, dL/ds) that the preparation phase turns into a and g."""
+    ins, raw = [], []
+    for l, L in enumerate(w.layers):
+        t = wl.draw_layer(w, l, device=dev)
+        if L.kind == "conv":
+            raw.append((l, t))
+            t = (torch.empty(w.B, L.T, L.d, dtype=w.torch_dtype, device=dev),
+                 torch.empty(w.B, L.T, L.p, dtype=w.torch_dtype, device=dev))
+        ins.append(t)
     Gs = [torch.empty(L.d, L.p, device=dev) for L in w.layers]
-    return ins, Gs
+    return ins, raw, Gs
 
 
 def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
@@ -93,12 +117,16 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
     for l, L in enumerate(w.layers):
         x, g = wl.draw_layer(w, l)
         t0 = time.perf_counter()
-        n = oracle.bk_layer_norm(L.kind, x, g, L.d)
+        kind = L.kind
+        if kind == "conv":
+            cin, k, stride, pad, _ = L.conv
+            x, g, kind = oracle.unfold(x, k, k, stride, pad, L.d), oracle.tokens_from_nchw(g), "linear"
+        n = oracle.bk_layer_norm(kind, x, g, L.d)
         C = oracle.clip_factors(n, w.clip, w.R, w.gamma)
         G = (oracle.embed_weighted_grad(x, g, C, L.d) if L.kind == "embed" else oracle.weighted_grad(x, g, C))
         oracle.add_noise(G, w.noise_std, w.wid, l, 0)
         t_used += time.perf_counter() - t0
-        done += 2.0 * w.B * L.T * L.p * L.d
+        done += 2.0 * w.B * L.T * L.p * true_d(L)
         nl += 1
         if t_used >= budget_s:
             break
@@ -153,7 +181,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-5)")
+    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-6)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mixopt", action="store_true",
                     help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
@@ -179,7 +207,7 @@ def main():
     mode = bk.BK_CLIP_ABADI if w.clip == "abadi" else bk.BK_CLIP_AUTO
     n, B = len(w.layers), w.B
 
-    ins, Gs = make_inputs(w, dev)
+    ins, raw, Gs = make_inputs(w, dev)
     keep = [args.mixopt and L.kind != "embed" and not bk.bk_use_ghost(L.T, L.d, L.p) for L in w.layers]
     Ps = [torch.empty(B, L.d, L.p, device=dev) if k else None for L, k in zip(w.layers, keep)]
     specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
@@ -198,7 +226,17 @@ def main():
     g_nel = (ctypes.c_int64 * n)(*[G.numel() for G in Gs])
     g_tid = (ctypes.c_uint32 * n)(*range(n))
 
+    convs = bk.make_convs([{"x": x, "dy": dy, "a": ins[l][0], "g": ins[l][1], "k": w.layers[l].conv[1],
+                            "stride": w.layers[l].conv[2], "pad": w.layers[l].conv[3], "ld": w.layers[l].d}
+                           for l, (x, dy) in raw])
+
+    def prep():
+        if raw:
+            bk._check(bk.lib.bk_conv_prep(convs, len(raw), dt, B, sp), "bk_conv_prep")
+
     def step(ev=None):
+        if ev: ev[5].record(stream)
+        prep()
         if ev: ev[0].record(stream)
         bk._check(bk.lib.bk_layer_norms(arr, n, dt, B, norm_sq.data_ptr(), ws_n.data_ptr(),
                                         ws_n.numel(), sp), "bk_layer_norms")
@@ -216,7 +254,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -225,7 +263,8 @@ def main():
     elapsed = time.perf_counter() - t0
     assert torch.isfinite(C).all().item(), "non-finite clip factors"
 
-    ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs])   # ms
+    ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] + [e[5].elapsed_time(e[0])]
+                   for e in evs])   # ms
     ph_ms = ph.mean(axis=0)
     work = algorithmic_work(w, args.mixopt)
     ms_step = elapsed * 1e3 / args.steps
@@ -238,13 +277,18 @@ def main():
                            "gbs": work["gemm_bytes"] / ph_ms[2] / 1e6},
         "noise": {"ms": ph_ms[3], "gbs": 8.0 * work["noise_elems"] / ph_ms[3] / 1e6},
     }
+    if raw:
+        phases = {"prep": {"ms": ph_ms[4], "gbs": work["prep_bytes"] / ph_ms[4] / 1e6}, **phases}
     # Dominant kernel: the phase with the most time among the two big ones.
     if phases["weighted_grads"]["ms"] >= phases["norms"]["ms"]:
         ach = phases["weighted_grads"]["tflops"]
         # bf16 layers with 32 | T take the LDS-DMA kernel, other T the register-staged one
         gk = "agrad_dl_kernel" if all(L.T % 32 == 0 for L in w.layers if L.kind != "embed") \
             else "agrad_bf16_kernel"
-        roof = {"kernel": f"{gk} (clip-weighted gradient, all layers in one launch)",
+        what = ("clip-weighted gradient, all layers in one launch" if gk == "agrad_dl_kernel" or
+                not any(L.T % 32 == 0 and L.T >= 64 for L in w.layers if L.kind != "embed")
+                else "clip-weighted gradient phase: one launch per kernel variant")
+        roof = {"kernel": f"{gk} ({what})",
                 "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
                 "frac": ach / peak_mfma, "traffic": measured_traffic(gk, w.name),
                 "per_launch": f"{work['gemm_flops'] / 1e9:.1f} GFLOP (sum over layers of 2 B T d p)"}
@@ -272,7 +316,8 @@ def main():
         "config": {"workload": w.name, "variant": "BK-MixOpt" if args.mixopt else "BK",
                    "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
                    "clip": w.clip, "sigma": w.sigma, "paths": {"ghost": work["ghost_layers"],
-                   "inst": work["inst_layers"], "embed": work["embed_layers"]}},
+                   "inst": work["inst_layers"], "embed": work["embed_layers"],
+                   "conv": work["conv_layers"]}},
         "roofline": roof,
         "phases": phases,
         "mfma_frac": {"ghost_norm_paper_flops": phases["norms"].get("tflops", 0) / peak_mfma,

@@ -177,6 +177,25 @@ bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H,
 bk_status bk_tokens_from_nchw(const void* y, bk_dtype dt, int64_t B, int64_t C, int64_t H,
                               int64_t W, void* out, void* stream);
 
+/* One convolution layer of bk_conv_prep (App. B, the convolution as a
+ * generalized linear layer with T = Ho Wo, d = C kh kw, p output channels). */
+typedef struct bk_conv {
+    const void* x;    /* [B, C, H, W] input, or NULL: no unfold for this layer */
+    const void* dy;   /* [B, p, Ho, Wo] output gradient dL/ds, or NULL: no transpose */
+    void* a;          /* out: [B, Ho Wo, ld] unfolded input (bk_unfold) */
+    void* g;          /* out: [B, Ho Wo, p] token-major gradient (bk_tokens_from_nchw) */
+    int64_t C, H, W, kh, kw, stride, pad, ld, p;
+} bk_conv;
+
+/* Every convolution of a step at once: for each of the n layers, a =
+ * bk_unfold(x) and g = bk_tokens_from_nchw(dy) with the shapes above, all of
+ * dtype dt and batch B.  The results are those of the single calls (bit-
+ * exact copies); the work of all layers shares one launch (a few when more
+ * than 24 layers or shapes outside the grouped kernel's limits).  Outputs
+ * must not overlap each other or the inputs.  Every layer is checked before
+ * any work is queued; n <= 4096, B <= 65535. */
+bk_status bk_conv_prep(const bk_conv* convs, int64_t n, bk_dtype dt, int64_t B, void* stream);
+
 /* Ghost norm of an embedding layer (Section 2.1 names the embedding among the
  * generalized linear layers; App. D.1 lists it as ghost-norm only).  Its input
  * a_i is the one-hot encoding of the ids x_i, so a_i a_i^T is the token-id

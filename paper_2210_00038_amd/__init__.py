@@ -25,7 +25,8 @@ __all__ = [
     "BK_OP_GHOST_NORM", "BK_OP_INST_NORM", "BK_OP_EMBED_GHOST_NORM", "BK_OP_WEIGHTED_GRAD",
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw",
+    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv",
+    "bk_conv_prep", "make_convs",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
     "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
     "conv_out_size",
@@ -46,7 +47,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbk.so")
 # Every symbol include/bk.h declares.
 EXPORTS = (
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw",
+    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv_prep",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
     "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
     "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_status_string",
@@ -65,6 +66,13 @@ class bk_layer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("flags", ctypes.c_int32), ("T", ctypes.c_int64),
                 ("d", ctypes.c_int64), ("p", ctypes.c_int64), ("x", ctypes.c_void_p),
                 ("g", ctypes.c_void_p), ("G", ctypes.c_void_p), ("P", ctypes.c_void_p)]
+
+
+class bk_conv(ctypes.Structure):
+    """Mirror of ``struct bk_conv`` in include/bk.h."""
+    _fields_ = [("x", ctypes.c_void_p), ("dy", ctypes.c_void_p), ("a", ctypes.c_void_p),
+                ("g", ctypes.c_void_p)] + [(f, ctypes.c_int64) for f in
+                                           ("C", "H", "W", "kh", "kw", "stride", "pad", "ld", "p")]
 
 
 if not os.path.exists(LIB_PATH):
@@ -87,6 +95,7 @@ _SIG = {
     "bk_weighted_sum": (_st, [_vp, _vp, _i64, _i64, _vp, _vp]),
     "bk_unfold": (_st, [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _vp, _vp]),
     "bk_tokens_from_nchw": (_st, [_vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp]),
+    "bk_conv_prep": (_st, [ctypes.POINTER(bk_conv), _i64, ctypes.c_int, _i64, _vp]),
     "bk_clip_factors": (_st, [_vp, _i64, _i64, ctypes.c_int, _f32, _f32, _vp, _vp, _vp]),
     "bk_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_embed_weighted_grad": (_st, [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp,
@@ -274,6 +283,33 @@ def bk_tokens_from_nchw(y, out=None, stream=None):
     _check(lib.bk_tokens_from_nchw(_ptr(y), _dtype_code(y), B, C, H, W, _ptr(out), _stream(stream)),
            "bk_tokens_from_nchw")
     return out
+
+
+def make_convs(specs: Sequence[dict]):
+    """ctypes bk_conv array from dicts {x [B,C,H,W] (or None with C, H, W given), dy [B,p,Ho,Wo]
+    (or None with p given), a, g (preallocated outputs [B, Ho Wo, ld] and [B, Ho Wo, p]),
+    k or (kh, kw), stride, pad, ld (0: C kh kw)}."""
+    arr = (bk_conv * len(specs))()
+    for c, sp in zip(arr, specs):
+        x, dy = sp.get("x"), sp.get("dy")
+        for t, nm in ((x, "x"), (dy, "dy"), (sp.get("a"), "a"), (sp.get("g"), "g")):
+            if t is not None:
+                _dev(t, nm)
+        C, H, W = x.shape[1:] if x is not None else (sp["C"], sp["H"], sp["W"])
+        kh, kw = sp.get("kh", sp.get("k")), sp.get("kw", sp.get("k"))
+        c.x, c.dy = _ptr(x) if x is not None else None, _ptr(dy) if dy is not None else None
+        c.a = _ptr(sp["a"]) if sp.get("a") is not None else None
+        c.g = _ptr(sp["g"]) if sp.get("g") is not None else None
+        c.C, c.H, c.W, c.kh, c.kw = C, H, W, kh, kw
+        c.stride, c.pad = sp.get("stride", 1), sp.get("pad", 0)
+        c.ld = sp.get("ld") or C * kh * kw
+        c.p = dy.shape[1] if dy is not None else sp.get("p", 0)
+    return arr
+
+
+def bk_conv_prep(convs, n: int, dtype, B: int, stream=None):
+    """Unfold and transpose every convolution layer of `convs` (a bk_conv array) in one call."""
+    _check(lib.bk_conv_prep(convs, n, dtype, B, _stream(stream)), "bk_conv_prep")
 
 
 def bk_embed_ghost_norm(ids, g, V: int, norm_sq=None, ws=None, stream=None) -> torch.Tensor:

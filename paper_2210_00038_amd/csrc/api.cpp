@@ -700,12 +700,11 @@ bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, 
     return e == hipSuccess ? BK_OK : hip_fail(e, "weighted sum launch");
 }
 
-bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H, int64_t W,
-                    int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t ld, void* a,
-                    void* stream) {
-    const char* fn = "bk_unfold";
-    bk_status st = check_dtype(fn, dt);
-    if (st != BK_OK) return st;
+namespace {
+
+// Shape checks of one unfold (App. B): fills sh on success.
+bk_status check_unfold(const char* fn, int64_t B, int64_t C, int64_t H, int64_t W, int64_t kh, int64_t kw,
+                       int64_t stride, int64_t pad, int64_t ld, bk::UnfoldShape* sh) {
     if (B < 0 || C < 0 || H < 0 || W < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
     if (kh < 1 || kw < 1 || stride < 1 || pad < 0)
         return fail(BK_ERR_INVALID_VALUE, "%s: kernel, stride >= 1 and pad >= 0 required", fn);
@@ -719,9 +718,31 @@ bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H,
     const int64_t T = Ho * Wo;
     if (B > 0 && T > INT64_MAX / B / std::max<int64_t>(ld, 1))
         return fail(BK_ERR_INVALID_VALUE, "%s: output size overflows", fn);
-    if (B * T * ld == 0) return BK_OK;
+    *sh = bk::UnfoldShape{B, C, H, W, kh, kw, stride, pad, Ho, Wo, T, ld};
+    return BK_OK;
+}
+
+bk_status check_tokens(const char* fn, int64_t B, int64_t C, int64_t HW) {
+    if (B < 0 || C < 0 || HW < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (B > 65535 || C > ((int64_t)1 << 36) || HW > ((int64_t)1 << 36))
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: dimensions too large", fn);
+    if ((HW + 31) / 32 > INT32_MAX || (C + 31) / 32 > 65535)
+        return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+    return BK_OK;
+}
+
+}  // namespace
+
+bk_status bk_unfold(const void* x, bk_dtype dt, int64_t B, int64_t C, int64_t H, int64_t W,
+                    int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t ld, void* a,
+                    void* stream) {
+    const char* fn = "bk_unfold";
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    bk::UnfoldShape sh{};
+    if ((st = check_unfold(fn, B, C, H, W, kh, kw, stride, pad, ld, &sh)) != BK_OK) return st;
+    if (B * sh.T * ld == 0) return BK_OK;
     if (!x || !a) return fail(BK_ERR_INVALID_VALUE, "%s: NULL pointer", fn);
-    const bk::UnfoldShape sh{B, C, H, W, kh, kw, stride, pad, Ho, Wo, T, ld};
     hipError_t e = bk::launch_unfold(x, a, sh, dt == BK_BF16, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? BK_OK : hip_fail(e, "unfold launch");
 }
@@ -731,15 +752,38 @@ bk_status bk_tokens_from_nchw(const void* y, bk_dtype dt, int64_t B, int64_t C, 
     const char* fn = "bk_tokens_from_nchw";
     bk_status st = check_dtype(fn, dt);
     if (st != BK_OK) return st;
-    if (B < 0 || C < 0 || H < 0 || W < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
-    if (B > 65535 || C > ((int64_t)1 << 36) || H * W > ((int64_t)1 << 36))
-        return fail(BK_ERR_NOT_SUPPORTED, "%s: dimensions too large", fn);
+    if (H < 0 || W < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (H > ((int64_t)1 << 20) || W > ((int64_t)1 << 20)) return fail(BK_ERR_NOT_SUPPORTED, "%s: dimensions too large", fn);
+    if ((st = check_tokens(fn, B, C, H * W)) != BK_OK) return st;
     if (B * C * H * W == 0) return BK_OK;
     if (!y || !out) return fail(BK_ERR_INVALID_VALUE, "%s: NULL pointer", fn);
-    if ((H * W + 31) / 32 > INT32_MAX || (C + 31) / 32 > 65535)
-        return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
     hipError_t e = bk::launch_tokens(y, out, B, C, H * W, dt == BK_BF16, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? BK_OK : hip_fail(e, "token transpose launch");
+}
+
+bk_status bk_conv_prep(const bk_conv* convs, int64_t n, bk_dtype dt, int64_t B, void* stream) {
+    const char* fn = "bk_conv_prep";
+    bk_status st = check_dtype(fn, dt);
+    if (st != BK_OK) return st;
+    if (n < 0 || B < 0) return fail(BK_ERR_INVALID_VALUE, "%s: negative size", fn);
+    if (n == 0) return BK_OK;
+    if (!convs) return fail(BK_ERR_INVALID_VALUE, "%s: NULL layer array", fn);
+    if (n > 4096) return fail(BK_ERR_NOT_SUPPORTED, "%s: more than 4096 layers", fn);
+    std::vector<bk::ConvPrepLayer> L((size_t)n);
+    for (int64_t l = 0; l < n; ++l) {
+        const bk_conv& c = convs[l];
+        char where[64];
+        std::snprintf(where, sizeof where, "%s (layer %lld)", fn, (long long)l);
+        bk::UnfoldShape sh{};
+        if ((st = check_unfold(where, B, c.C, c.H, c.W, c.kh, c.kw, c.stride, c.pad, c.ld, &sh)) != BK_OK) return st;
+        if ((st = check_tokens(where, B, c.p, sh.T)) != BK_OK) return st;
+        if ((c.x && !c.a) || (c.dy && !c.g))
+            return fail(BK_ERR_INVALID_VALUE, "%s: NULL output for a given input", where);
+        const bool unf = c.x && B * sh.T * c.ld > 0, tok = c.dy && B * sh.T * c.p > 0;
+        L[(size_t)l] = bk::ConvPrepLayer{unf ? c.x : nullptr, tok ? c.dy : nullptr, c.a, c.g, sh, c.p};
+    }
+    hipError_t e = bk::launch_conv_prep(L.data(), (int)n, B, dt == BK_BF16, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? BK_OK : hip_fail(e, "convolution preparation launch");
 }
 
 bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B, int64_t T,

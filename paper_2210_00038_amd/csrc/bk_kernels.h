@@ -138,6 +138,38 @@ struct UnfoldShape {
     int64_t Ho, Wo, T, ld;      // output a [B, T = Ho Wo, ld]
 };
 
+// One layer of a grouped preparation: unfold x -> a (when x is set) and
+// transpose dy [B, p, T] -> g [B, T, p] (when dy is set).
+struct ConvPrepLayer {
+    const void* x;
+    const void* dy;
+    void* a;
+    void* g;
+    UnfoldShape s;
+    int64_t p;
+};
+
+// Device-side jobs of the grouped preparation kernel (32-bit sizes; the
+// launcher sends larger shapes to the element-wise kernels).
+struct UnfoldJob {
+    const void* x;
+    void* a;
+    int C, H, W, kh, kw, stride, pad, Ho, Wo, ld;
+    int cc, ngroups, Wp, table_off;   // channels per group, groups, patch row length, table offset
+};
+struct TokensJob {
+    const void* y;
+    void* out;
+    int C, HW, tiles_t, tiles_c;
+};
+constexpr int kMaxPrepJobs = 24;
+struct PrepArgs {
+    int nu, nt;
+    UnfoldJob u[kMaxPrepJobs];
+    TokensJob t[kMaxPrepJobs];
+    int blk_end[2 * kMaxPrepJobs];
+};
+
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
@@ -155,6 +187,7 @@ hipError_t launch_clip(const float* norm_sq, int64_t L, int64_t B, int mode, flo
 hipError_t launch_noise(const NoiseArgs& args, int n_wg, hipStream_t s);
 hipError_t launch_wsum(const WsumArgs& args, int n_wg, hipStream_t s);
 hipError_t launch_unfold(const void* x, void* a, const UnfoldShape& s, bool bf16, hipStream_t st);
+hipError_t launch_conv_prep(const ConvPrepLayer* L, int n, int64_t B, bool bf16, hipStream_t st);
 hipError_t launch_tokens(const void* y, void* out, int64_t B, int64_t C, int64_t HW, bool bf16, hipStream_t st);
 hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q0, int64_t nq,
                              uint32_t* out, hipStream_t s);

@@ -3,20 +3,221 @@
 // height x width): the unfolded input a [B, T, ld] and the token-major output
 // gradient g [B, T, p] that the BK kernels take.
 //
-// unfold: one thread per output element (b, t, column); consecutive threads
-// write consecutive columns of a row, so the stores coalesce and the gathers
-// from x hit the rows of one (c, i) run.  Columns d .. ld-1 are zero.
-// tokens: [B, C, HW] -> [B, HW, C] transpose through a 32 x 33 LDS tile
-// (coalesced reads and writes, no bank conflicts).
+// Both run in one grouped kernel over a list of layers (one launch prepares
+// every convolution of a step): its workgroups are split among unfold jobs,
+// then transpose jobs, by cumulative block counts.
+//
+// unfold (LDS path): one workgroup per (sample b, output row oh, channel
+// group).  It copies the input rows that output row reads, for its channels,
+// into LDS with coalesced loads (zero rows above and below the image, zero
+// columns left and right), builds a table of the patch offset of each of its
+// columns (column (c, i, j) -> patch row (c, i), column j; -1 for the zero
+// columns d .. ld-1), and then writes the Wo output rows of its column range
+// as 16-byte stores, each gathering VE values from LDS at offset + ow stride.
+// x is read from HBM about kh / stride times (once per output row that uses
+// an input row); a is written once.  Shapes whose patch does not fit, or
+// whose ld is not a multiple of VE, take the one-element-per-thread kernel.
+//
+// tokens: [B, C, HW] -> [B, HW, C] through a 64 x 64 LDS tile, read along
+// HW and written as 16-byte rows along C (C a multiple of VE); other C take a
+// 32 x 33 tile with scalar stores.
 #include "bk_device.h"
 #include "bk_kernels.h"
 
 namespace bk {
 namespace {
 
+constexpr int kUnfoldThreads = 256;
+constexpr int64_t kUnfoldLds = 40 * 1024;     // patch + offset table per workgroup
+constexpr int64_t kUnfoldWGs = 1024;          // channel groups are split until the grid has this many
+constexpr int kFillUnroll = 8;                // independent input loads in flight per thread
+
 template <typename E>
-__global__ __launch_bounds__(256) void unfold_kernel(const E* __restrict__ x, E* __restrict__ a,
-                                                     UnfoldShape s) {
+struct Vec16 {
+    static constexpr int N = 16 / (int)sizeof(E);
+    E v[N];
+};
+
+// LDS layout: patch [cc][kh][Wp] of E, then one zero element, then (16-byte
+// aligned) the int offset table of the group's columns.
+struct UnfoldPlan {
+    int cc = 0, ngroups = 0, Wp = 0;
+    int64_t table_off = 0, lds = 0;
+};
+
+UnfoldPlan unfold_plan(const UnfoldShape& s, int es) {
+    UnfoldPlan p;
+    const int ve = 16 / es;
+    if (s.ld % ve != 0 || s.B > 65535 || s.Ho > 65535 || s.ld > INT32_MAX) return p;
+    if (s.Wo * (s.ld / ve) > INT32_MAX) return p;          // items of one workgroup fit an int
+    const int64_t Wp = (s.Wo - 1) * s.stride + s.kw;
+    const int64_t khkw = s.kh * s.kw, d = s.C * khkw;
+    const int64_t per_c = s.kh * Wp * es + khkw * 4;
+    const int64_t fixed = (s.ld - d) * 4 + es + 16 + 16;
+    const int64_t cap = (kUnfoldLds - fixed) / per_c;      // channels whose patch and table fit
+    int64_t cc = cap;
+    // more groups when (sample, output row) pairs alone do not fill the chip
+    const int64_t want = (kUnfoldWGs + s.B * s.Ho - 1) / (s.B * s.Ho);
+    if (want > 1) cc = std::min(cc, (s.C + want - 1) / want);
+    if (cc < s.C) {                           // group column ranges stay 16-byte aligned
+        cc = (cc + ve - 1) / ve * ve;
+        if (cc > cap) cc -= ve;
+    }
+    cc = std::min<int64_t>(cc, s.C);
+    if (cc < 1 || cc * s.kh * Wp >= 65536) return p;
+    p.cc = (int)cc;
+    p.ngroups = (int)((s.C + cc - 1) / cc);
+    p.Wp = (int)Wp;
+    p.table_off = (cc * s.kh * Wp * es + es + 15) / 16 * 16;
+    const int64_t ncols_max = std::max<int64_t>(cc * khkw, s.ld - (s.C - 1) / cc * cc * khkw);
+    p.lds = p.table_off + ncols_max * 4;
+    if (p.lds > 64 * 1024) p.cc = 0;
+    return p;
+}
+
+// n / dv for 0 <= n < 2^16 (every LDS patch index): the float estimate is
+// within one of the quotient, and one step either way makes it exact.
+__device__ __forceinline__ int small_div(int n, int dv, float rdv) {
+    int q = (int)((float)n * rdv);
+    const int rem = n - q * dv;
+    q += (rem >= dv) - (rem < 0);
+    return q;
+}
+
+// One unfold workgroup: channel group g of output row oh of sample b.
+template <typename E>
+__device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int oh, int g,
+                                             unsigned char* smem) {
+    const E* __restrict__ x = static_cast<const E*>(J.x);
+    E* __restrict__ a = static_cast<E*>(J.a);
+    E* patch = reinterpret_cast<E*>(smem);
+    int* offs = reinterpret_cast<int*>(smem + J.table_off);
+    constexpr int VE = Vec16<E>::N;
+    const int tid = threadIdx.x;
+    const int kh = J.kh, kw = J.kw, khkw = kh * kw, stride = J.stride, pad = J.pad;
+    const int H = J.H, W = J.W, Wo = J.Wo, Wp = J.Wp, C = J.C, cc = J.cc;
+    const int c0 = g * cc, cg = min(cc, C - c0);
+    const int d = C * khkw, ld = J.ld;
+    const int col0 = c0 * khkw;
+    const int ncols = (c0 + cg == C) ? ld - col0 : cg * khkw;
+    const int zslot = cc * kh * Wp;
+
+    // input rows (c, i) of this output row, zero outside the image; the
+    // patch is walked flat (element e = row Wp + wp) so every lane loads
+    const int nel = cg * kh * Wp;
+    const float rWp = 1.0f / (float)Wp, rkh = 1.0f / (float)kh;
+    const E* xb = x + (b * C + c0) * (int64_t)H * W;
+    for (int e0 = tid; e0 < nel; e0 += kFillUnroll * kUnfoldThreads) {
+        E v[kFillUnroll];
+#pragma unroll
+        for (int u = 0; u < kFillUnroll; ++u) {
+            const int e = e0 + u * kUnfoldThreads;
+            v[u] = E{};
+            if (e < nel) {
+                const int r = small_div(e, Wp, rWp), wp = e - r * Wp;
+                const int cr = small_div(r, kh, rkh), i = r - cr * kh;
+                const int h = oh * stride + i - pad, w = wp - pad;
+                if (h >= 0 && h < H && w >= 0 && w < W) v[u] = xb[((int64_t)cr * H + h) * W + w];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kFillUnroll; ++u) {
+            const int e = e0 + u * kUnfoldThreads;
+            if (e < nel) patch[e] = v[u];
+        }
+    }
+    if (tid == 0) patch[zslot] = E{};
+    for (int col = tid; col < ncols; col += kUnfoldThreads) {
+        const int gc = col0 + col;
+        int off = -1;
+        if (gc < d) {
+            const int c = gc / khkw, rr = gc - c * khkw;
+            const int i = rr / kw, j = rr - i * kw;
+            off = ((c - c0) * kh + i) * Wp + j;
+        }
+        offs[col] = off;
+    }
+    __syncthreads();
+
+    // output rows t = oh Wo + ow, columns col0 .. col0 + ncols, VE at a time
+    const int nch = ncols / VE;
+    const int items = Wo * nch;
+    int e = tid;
+    int ow = e / nch, k = e - ow * nch;
+    const int dow = kUnfoldThreads / nch, dk = kUnfoldThreads - dow * nch;
+    E* dst0 = a + (b * J.Ho * Wo + (int64_t)oh * Wo) * ld + col0;
+    for (; e < items; e += kUnfoldThreads) {
+        Vec16<E> out;
+        const int base = ow * stride;
+#pragma unroll
+        for (int q = 0; q < VE; ++q) {
+            const int o = offs[k * VE + q];
+            out.v[q] = patch[o < 0 ? zslot : o + base];
+        }
+        *reinterpret_cast<Vec16<E>*>(dst0 + (int64_t)ow * ld + k * VE) = out;
+        ow += dow;
+        k += dk;
+        if (k >= nch) { k -= nch; ++ow; }
+    }
+}
+
+// One transpose workgroup: a 64 (HW) x 64 (C) tile of sample b; LDS rows
+// are tokens, padded by one 16-byte chunk.
+template <typename E>
+__device__ __forceinline__ void tokens_block(const TokensJob& J, int64_t b, int ty, int tx,
+                                             unsigned char* smem) {
+    constexpr int VE = Vec16<E>::N, LDR = 64 + VE;
+    E* tile = reinterpret_cast<E*>(smem);
+    const int64_t C = J.C, HW = J.HW;
+    const int64_t c0 = (int64_t)ty * 64, t0 = (int64_t)tx * 64;
+    const int tid = threadIdx.x;
+    const E* src = static_cast<const E*>(J.y) + b * C * HW;
+    E* dst = static_cast<E*>(J.out) + b * C * HW;
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+        const int idx = it * 256 + tid, cl = idx >> 6, tl = idx & 63;
+        const int64_t c = c0 + cl, t = t0 + tl;
+        E v{};
+        if (c < C && t < HW) v = src[c * HW + t];
+        tile[tl * LDR + cl] = v;
+    }
+    __syncthreads();
+    constexpr int CPR = 64 / VE;                        // 16-byte chunks per tile row
+#pragma unroll
+    for (int it = 0; it < CPR / 4; ++it) {
+        const int idx = it * 256 + tid, tl = idx / CPR, q = idx % CPR;
+        const int64_t t = t0 + tl, c = c0 + q * VE;
+        if (t < HW && c < C)
+            *reinterpret_cast<Vec16<E>*>(dst + t * C + c) = *reinterpret_cast<const Vec16<E>*>(&tile[tl * LDR + q * VE]);
+    }
+}
+
+template <typename E>
+constexpr int tokens_lds() { return 64 * (64 + Vec16<E>::N) * (int)sizeof(E); }
+
+// Workgroups [blk_end[j-1], blk_end[j]) belong to job j: the unfold jobs
+// first, then the transpose jobs.
+template <typename E>
+__global__ __launch_bounds__(kUnfoldThreads) void conv_prep_kernel(PrepArgs A) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int blk = blockIdx.x;
+    int j = 0;
+    while (blk >= A.blk_end[j]) ++j;
+    const int local = blk - (j ? A.blk_end[j - 1] : 0);
+    if (j < A.nu) {
+        const UnfoldJob& J = A.u[j];
+        const int g = local % J.ngroups, rest = local / J.ngroups;
+        unfold_block<E>(J, rest / J.Ho, rest % J.Ho, g, smem);
+    } else {
+        const TokensJob& J = A.t[j - A.nu];
+        const int tx = local % J.tiles_t, rest = local / J.tiles_t;
+        tokens_block<E>(J, rest / J.tiles_c, rest % J.tiles_c, tx, smem);
+    }
+}
+
+template <typename E>
+__global__ __launch_bounds__(256) void unfold_any_kernel(const E* __restrict__ x, E* __restrict__ a,
+                                                         UnfoldShape s) {
     const int64_t total = s.B * s.T * s.ld;
     const int64_t d = s.C * s.kh * s.kw;
     for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
@@ -56,31 +257,100 @@ __global__ __launch_bounds__(256) void tokens_kernel(const E* __restrict__ y, E*
     }
 }
 
+// Jobs that the grouped kernel takes, and the separate launches of the rest.
+struct PrepBuilder {
+    PrepArgs A{};
+    int64_t blocks = 0;
+    int lds = 0;
+};
+
+template <typename E>
+hipError_t flush(PrepBuilder& P, hipStream_t st) {
+    if (P.A.nu + P.A.nt == 0) return hipSuccess;
+    hipLaunchKernelGGL(conv_prep_kernel<E>, dim3((unsigned)P.blocks), dim3(kUnfoldThreads), (size_t)P.lds, st, P.A);
+    const hipError_t e = hipGetLastError();
+    P = PrepBuilder{};
+    return e;
+}
+
+template <typename E>
+hipError_t add_unfold(PrepBuilder& P, const void* x, void* a, const UnfoldShape& s, hipStream_t st) {
+    if (s.B * s.T * s.ld == 0) return hipSuccess;
+    const UnfoldPlan p = unfold_plan(s, (int)sizeof(E));
+    const int64_t nblk = p.cc > 0 ? (int64_t)p.ngroups * s.Ho * s.B : 0;
+    if (p.cc == 0 || reinterpret_cast<uintptr_t>(a) % 16 != 0 || nblk > INT32_MAX / 4 ||
+        std::max<int64_t>({s.C, s.H, s.W, s.kh, s.kw, s.stride, s.pad}) > INT32_MAX) {
+        const int64_t total = s.B * s.T * s.ld;
+        const int64_t nb = std::min<int64_t>((total + 255) / 256, 65536);
+        hipLaunchKernelGGL(unfold_any_kernel<E>, dim3((unsigned)nb), dim3(256), 0, st,
+                           static_cast<const E*>(x), static_cast<E*>(a), s);
+        return hipGetLastError();
+    }
+    if (P.A.nu == kMaxPrepJobs || P.A.nt > 0 || P.blocks + nblk > INT32_MAX / 2) {
+        const hipError_t e = flush<E>(P, st);
+        if (e != hipSuccess) return e;
+    }
+    UnfoldJob& J = P.A.u[P.A.nu];
+    J = UnfoldJob{x, a, (int)s.C, (int)s.H, (int)s.W, (int)s.kh, (int)s.kw, (int)s.stride, (int)s.pad,
+                  (int)s.Ho, (int)s.Wo, (int)s.ld, p.cc, p.ngroups, p.Wp, (int)p.table_off};
+    P.blocks += nblk;
+    P.A.blk_end[P.A.nu++] = (int)P.blocks;
+    P.lds = std::max<int>(P.lds, (int)p.lds);
+    return hipSuccess;
+}
+
+template <typename E>
+hipError_t add_tokens(PrepBuilder& P, const void* y, void* out, int64_t B, int64_t C, int64_t HW,
+                      hipStream_t st) {
+    if (B * C * HW == 0) return hipSuccess;
+    const int64_t tt = (HW + 63) / 64, tc = (C + 63) / 64, nblk = tt * tc * B;
+    if (C % Vec16<E>::N != 0 || reinterpret_cast<uintptr_t>(out) % 16 != 0 || nblk > INT32_MAX / 4 ||
+        C > INT32_MAX || HW > INT32_MAX) {
+        const dim3 grid((unsigned)((HW + 31) / 32), (unsigned)((C + 31) / 32), (unsigned)B);
+        hipLaunchKernelGGL(tokens_kernel<E>, grid, dim3(256), 0, st, static_cast<const E*>(y),
+                           static_cast<E*>(out), C, HW);
+        return hipGetLastError();
+    }
+    if (P.A.nt == kMaxPrepJobs || P.blocks + nblk > INT32_MAX / 2) {
+        const hipError_t e = flush<E>(P, st);
+        if (e != hipSuccess) return e;
+    }
+    TokensJob& J = P.A.t[P.A.nt];
+    J = TokensJob{y, out, (int)C, (int)HW, (int)tt, (int)tc};
+    P.blocks += nblk;
+    P.A.blk_end[P.A.nu + P.A.nt++] = (int)P.blocks;
+    P.lds = std::max<int>(P.lds, tokens_lds<E>());
+    return hipSuccess;
+}
+
+template <typename E>
+hipError_t conv_prep_typed(const ConvPrepLayer* L, int n, int64_t B, hipStream_t st) {
+    PrepBuilder P;
+    hipError_t e = hipSuccess;
+    for (int l = 0; l < n && e == hipSuccess; ++l)
+        if (L[l].x) e = add_unfold<E>(P, L[l].x, L[l].a, L[l].s, st);
+    for (int l = 0; l < n && e == hipSuccess; ++l)
+        if (L[l].dy) e = add_tokens<E>(P, L[l].dy, L[l].g, B, L[l].p, L[l].s.T, st);
+    if (e == hipSuccess) e = flush<E>(P, st);
+    return e;
+}
+
 }  // namespace
 
+hipError_t launch_conv_prep(const ConvPrepLayer* L, int n, int64_t B, bool bf16, hipStream_t st) {
+    return bf16 ? conv_prep_typed<uint16_t>(L, n, B, st) : conv_prep_typed<float>(L, n, B, st);
+}
+
 hipError_t launch_unfold(const void* x, void* a, const UnfoldShape& s, bool bf16, hipStream_t st) {
-    const int64_t total = s.B * s.T * s.ld;
-    if (total == 0) return hipSuccess;
-    const int64_t nb = std::min<int64_t>((total + 255) / 256, 65536);
-    if (bf16)
-        hipLaunchKernelGGL(unfold_kernel<uint16_t>, dim3((unsigned)nb), dim3(256), 0, st,
-                           static_cast<const uint16_t*>(x), static_cast<uint16_t*>(a), s);
-    else
-        hipLaunchKernelGGL(unfold_kernel<float>, dim3((unsigned)nb), dim3(256), 0, st,
-                           static_cast<const float*>(x), static_cast<float*>(a), s);
-    return hipGetLastError();
+    const ConvPrepLayer L{x, nullptr, a, nullptr, s, 0};
+    return launch_conv_prep(&L, 1, s.B, bf16, st);
 }
 
 hipError_t launch_tokens(const void* y, void* out, int64_t B, int64_t C, int64_t HW, bool bf16, hipStream_t st) {
-    if (B * C * HW == 0) return hipSuccess;
-    const dim3 grid((unsigned)((HW + 31) / 32), (unsigned)((C + 31) / 32), (unsigned)B);
-    if (bf16)
-        hipLaunchKernelGGL(tokens_kernel<uint16_t>, grid, dim3(256), 0, st, static_cast<const uint16_t*>(y),
-                           static_cast<uint16_t*>(out), C, HW);
-    else
-        hipLaunchKernelGGL(tokens_kernel<float>, grid, dim3(256), 0, st, static_cast<const float*>(y),
-                           static_cast<float*>(out), C, HW);
-    return hipGetLastError();
+    UnfoldShape s{};
+    s.T = HW;
+    const ConvPrepLayer L{nullptr, y, nullptr, out, s, C};
+    return launch_conv_prep(&L, 1, B, bf16, st);
 }
 
 }  // namespace bk

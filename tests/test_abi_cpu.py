@@ -186,3 +186,27 @@ def test_conv_prep_validation():
     assert L.bk_tokens_from_nchw(None, bk.BK_F32, 2, 3, 4, 4, FAKE, None) == bk.BK_ERR_INVALID_VALUE
     assert L.bk_tokens_from_nchw(None, bk.BK_F32, 2, 0, 4, 4, None, None) == bk.BK_OK
     assert bk.conv_out_size(224, 7, 2, 3) == 112 and bk.conv_out_size(56, 1, 2, 0) == 28
+
+
+def test_grouped_conv_prep_validation():
+    L = bk.lib
+    mk = lambda **kw: (bk.bk_conv * 1)(bk.bk_conv(**{**dict(x=FAKE, dy=FAKE, a=FAKE, g=FAKE, C=3, H=8, W=8, kh=3,
+                                                           kw=3, stride=1, pad=1, ld=32, p=4), **kw}))
+    assert L.bk_conv_prep(None, 0, bk.BK_BF16, 2, None) == bk.BK_OK                    # no layers
+    assert L.bk_conv_prep(None, 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_conv_prep(mk(), -1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_conv_prep(mk(), 1, 7, 2, None) == bk.BK_ERR_INVALID_VALUE              # dtype
+    assert L.bk_conv_prep(mk(ld=26), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE  # ld < C kh kw
+    assert L.bk_conv_prep(mk(stride=0), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_conv_prep(mk(kh=11), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE  # kernel > padded image
+    assert L.bk_conv_prep(mk(a=None), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE  # x without a
+    assert L.bk_conv_prep(mk(g=None), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE  # dy without g
+    assert L.bk_conv_prep(mk(p=-1), 1, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
+    assert L.bk_conv_prep(mk(), 1, bk.BK_BF16, 70000, None) == bk.BK_ERR_NOT_SUPPORTED
+    # nothing to do: no inputs, or an empty batch
+    assert L.bk_conv_prep(mk(x=None, dy=None, a=None, g=None), 1, bk.BK_BF16, 2, None) == bk.BK_OK
+    assert L.bk_conv_prep(mk(), 1, bk.BK_BF16, 0, None) == bk.BK_OK
+    # a bad layer after a good one rejects the whole call (checked before any work)
+    two = (bk.bk_conv * 2)(mk()[0], mk(ld=1)[0])
+    assert L.bk_conv_prep(two, 2, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
+    assert b"layer 1" in L.bk_last_error()

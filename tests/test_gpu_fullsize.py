@@ -143,3 +143,53 @@ def test_config1_full(bk):
     assert np.linalg.norm(G - ref["G"][0]) / np.linalg.norm(ref["G"][0]) <= 1e-4
     noise = G1[0].cpu().numpy() - G
     assert np.max(np.abs(noise - (ref["Ghat"][0] - ref["G"][0]))) <= 2e-5 * 8
+
+
+def test_conv_stack_full_sampled_parity(bk):
+    """ResNet-18 convolutions at 224x224, B = 16: the GPU unfolds x and makes
+    dL/ds token-major (checked bit-exact against the oracle's unfold on sampled
+    layers), then one bk_private_grad call runs the stack as in bench.py."""
+    w = wl.get(6)
+    print(f"workload 6: {w.name}, {len(w.layers)} layers, B={w.B}", flush=True)
+    raw = [wl.draw_layer(w, l, device=DEV) for l in range(len(w.layers))]
+    ins = []
+    for L, (x, dy) in zip(w.layers, raw):
+        if L.kind == "conv":
+            cin, k, stride, pad, _ = L.conv
+            ins.append((bk.bk_unfold(x, k, k, stride, pad, L.d), bk.bk_tokens_from_nchw(dy)))
+        else:
+            ins.append((x, dy))
+    norms, C, tot, G0 = _run(bk, w, ins, 0.0)
+    for L in w.layers:
+        assert bk.bk_use_ghost(L.T, L.d, L.p) == oracle.use_ghost(L.T, L.d, L.p)
+    ref_tot = oracle.aggregate(norms)
+    assert np.max(np.abs(C - oracle.clip_factors(ref_tot, w.clip, w.R, w.gamma)) / C) <= 1e-5
+
+    n = len(w.layers)
+    picks = {0, 9, 10, 14, n - 2, n - 1}          # 7x7 stem, 1x1 downsamples, ghost 3x3, classifier
+    rng = np.random.default_rng(6)
+    for l in sorted(picks):
+        L = w.layers[l]
+        x, dy = (t.cpu() for t in raw[l])
+        if L.kind == "conv":
+            cin, k, stride, pad, _ = L.conv
+            a, g = oracle.unfold(x, k, k, stride, pad, L.d), oracle.tokens_from_nchw(dy)
+            assert np.array_equal(ins[l][0].cpu().double().numpy(), a), l
+            assert np.array_equal(ins[l][1].cpu().double().numpy(), g), l
+        else:
+            a, g = x.double().numpy(), dy.double().numpy()
+        ref_n = oracle.linear_norm_sq_gram(a, g) if oracle.use_ghost(L.T, L.d, L.p) else oracle.linear_norm_sq(a, g)
+        rel = np.max(np.abs(norms[l] - ref_n) / ref_n)
+        print(f"  layer {l} ({L.kind} T={L.T} d={L.d} p={L.p}): norm rel err {rel:.2e}", flush=True)
+        assert rel <= NORM_TOL, l
+        rows = np.sort(rng.choice(L.d, min(32, L.d), replace=False))
+        cols = np.sort(rng.choice(L.p, 32, replace=False))
+        ref = oracle.weighted_grad(a[:, :, rows], g[:, :, cols], C)
+        got = G0[l][torch.as_tensor(rows, device=DEV)][:, torch.as_tensor(cols, device=DEV)].cpu().numpy()
+        pad_rows = rows >= (L.conv[0] * L.conv[1] ** 2 if L.kind == "conv" else L.d)
+        assert np.all(got[pad_rows] == 0.0), l                # zero columns of a give zero gradient rows
+        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+        print(f"  layer {l}: gradient block frob err {err:.2e}", flush=True)
+        assert err <= GRAD_TOL, l
+    del raw, ins, G0
+    torch.cuda.empty_cache()

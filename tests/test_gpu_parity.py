@@ -404,6 +404,9 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     (3, 8, 9, 9, 3, 1, 1, 0),         # d = 72, no padding
     (1, 5, 12, 10, 1, 2, 0, 8),       # 1 x 1 stride 2 (downsample), d = 5 -> 8
     (2, 4, 6, 7, 3, 2, 0, 40),        # no padding, odd output
+    (1, 512, 7, 7, 3, 1, 1, 0),       # channel groups (the patch of 512 channels exceeds one workgroup)
+    (1, 520, 9, 6, 3, 2, 1, 4688),    # fp32: two groups, the last one carries the zero columns
+    (2, 2, 10, 10, 3, 1, 1, 27),      # ld not a multiple of 16 bytes: element-wise kernel
 ])
 def test_unfold_and_tokens_bit_exact(bk, dtype, B, C, H, W, k, stride, pad, ld):
     gen = torch.Generator().manual_seed(C * H + k)
@@ -414,6 +417,45 @@ def test_unfold_and_tokens_bit_exact(bk, dtype, B, C, H, W, k, stride, pad, ld):
     y = torch.randn(B, C, H, W, generator=gen).to(dtype)
     t = bk.bk_tokens_from_nchw(y.to(DEV)).cpu()
     assert np.array_equal(t.float().numpy(), oracle.tokens_from_nchw(y.float().numpy()))
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_grouped_conv_prep_bit_exact(bk, dtype):
+    """bk_conv_prep over 27 layers (more than one grouped launch), with layers
+    that only unfold or only transpose and shapes that take the element-wise
+    kernels, against the oracle's unfold and token-major transpose."""
+    gen = torch.Generator().manual_seed(11)
+    B = 3
+    shapes = [(3, 8, 17, 7, 2, 3), (8, 16, 9, 3, 1, 1), (16, 8, 9, 1, 2, 0), (5, 6, 10, 3, 1, 1),
+              (24, 16, 7, 3, 2, 1), (64, 64, 5, 3, 1, 1), (2, 5, 6, 3, 1, 0)] * 4
+    shapes = shapes[:27]
+    specs, refs = [], []
+    for l, (ci, co, h, k, s, pd) in enumerate(shapes):
+        ho = bk.conv_out_size(h, k, s, pd)
+        d = ci * k * k
+        ld = d + (l % 3) if l % 7 == 6 else (d + 7) // 8 * 8       # some ld not a multiple of 16 bytes
+        x = torch.randn(B, ci, h, h, generator=gen).to(dtype)
+        dy = torch.randn(B, co, ho, ho, generator=gen).to(dtype)
+        ux, uy = l % 5 != 3, l % 5 != 4                             # unfold only / transpose only
+        a = torch.full((B, ho * ho, ld), float("nan"), dtype=dtype, device=DEV)
+        g = torch.full((B, ho * ho, co), float("nan"), dtype=dtype, device=DEV)
+        specs.append({"x": x.to(DEV) if ux else None, "dy": dy.to(DEV) if uy else None, "a": a, "g": g, "k": k,
+                      "stride": s, "pad": pd, "ld": ld, "C": ci, "H": h, "W": h, "p": co})
+        refs.append((oracle.unfold(x.float().numpy(), k, k, s, pd, ld) if ux else None,
+                     oracle.tokens_from_nchw(dy.float().numpy()) if uy else None))
+    arr = bk.make_convs(specs)
+    bk.bk_conv_prep(arr, len(specs), bk.BK_BF16 if dtype == torch.bfloat16 else bk.BK_F32, B)
+    torch.cuda.synchronize()
+    for l, (sp, (ra, rg)) in enumerate(zip(specs, refs)):
+        a, g = sp["a"].cpu().float().numpy(), sp["g"].cpu().float().numpy()
+        if ra is not None:
+            assert np.array_equal(a, ra), l
+        else:
+            assert np.all(np.isnan(a)), l                          # no input: output untouched
+        if rg is not None:
+            assert np.array_equal(g, rg), l
+        else:
+            assert np.all(np.isnan(g)), l
 
 
 def test_conv_stack_matches_oracle(bk):

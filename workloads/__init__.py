@@ -7,7 +7,9 @@ inputs from here, so the two sides see bit-identical data.
 
 The stacks stand in for the paper's workloads (GPT-2 on E2E-length text, the
 long-sequence regime of Section 3.1, ViT-base at 224x224, GPT-2-large with its
-token embedding); the datasets and pretrained weights are not used.  Shapes
+token embedding, and the convolutions of ResNet-18 at 224x224 behind the
+layerwise decision of Section 3.2); the datasets and pretrained weights are
+not used.  Shapes
 follow Section 2.1 (a in R^{B x T x d}, dL/ds in R^{B x T x p}) and the
 per-layer dimensions of GPT-2 small/large and ViT-base.
 
@@ -18,7 +20,11 @@ Recipe (stated once, used everywhere):
     then the tensor is rounded (round-to-nearest-even) to the workload dtype;
   * token ids of an embedding layer follow a finite Zipf law,
     P(id = k-1) proportional to k^-s for k = 1..V, drawn with numpy's PCG64
-    seeded with 1000*w + 999.
+    seeded with 1000*w + 999;
+  * a convolution layer draws its input x [B, C_in, H, H] (k = 0) and its
+    output gradient [B, C_out, Ho, Ho] (k = 1) in the same way (NCHW); its
+    linear-layer view has T = Ho*Ho, d = C_in*k*k rounded up to a multiple of
+    8 (zero columns), p = C_out.
 """
 from __future__ import annotations
 
@@ -29,7 +35,7 @@ import numpy as np
 import torch
 
 __all__ = ["Layer", "Workload", "WORKLOADS", "get", "draw_linear", "draw_embedding",
-           "draw_layer", "zipf_ids", "make_stack", "workload_from_shapes"]
+           "draw_layer", "zipf_ids", "make_stack", "workload_from_shapes", "conv_layer", "draw_conv"]
 
 
 @dataclass(frozen=True)
@@ -39,10 +45,11 @@ class Layer:
     kind == "embed": a is the one-hot encoding of token ids over a vocabulary of
     size V == d, so only ids and g are stored.
     """
-    kind: str          # "linear" | "embed"
+    kind: str          # "linear" | "embed" | "conv"
     T: int
     d: int
     p: int
+    conv: tuple = ()   # kind == "conv": (C_in, k, stride, pad, H_in)
 
     @property
     def V(self) -> int:
@@ -82,6 +89,24 @@ def _gpt2_block(d: int, T: int) -> List[Layer]:
             Layer("linear", T, d, 4 * d), Layer("linear", T, 4 * d, d)]
 
 
+def conv_layer(cin: int, cout: int, k: int, stride: int, pad: int, hin: int) -> Layer:
+    """A k x k convolution on an hin x hin input, as the linear layer of its unfolding."""
+    ho = (hin + 2 * pad - k) // stride + 1
+    d = (cin * k * k + 7) // 8 * 8
+    return Layer("conv", ho * ho, d, cout, (cin, k, stride, pad, hin))
+
+
+def _resnet18_224() -> List[Layer]:
+    L = [conv_layer(3, 64, 7, 2, 3, 224)]
+    L += [conv_layer(64, 64, 3, 1, 1, 56) for _ in range(4)]
+    for cin, cout, h in ((64, 128, 56), (128, 256, 28), (256, 512, 14)):
+        L.append(conv_layer(cin, cout, 3, 2, 1, h))
+        L += [conv_layer(cout, cout, 3, 1, 1, h // 2) for _ in range(3)]
+        L.append(conv_layer(cin, cout, 1, 2, 0, h))        # downsample
+    L.append(Layer("linear", 1, 512, 1000))                # classifier
+    return L
+
+
 def _build() -> dict:
     w = {}
     w[1] = Workload(1, "single-linear-64x64-T16-B4-f32", 4, "f32",
@@ -107,6 +132,9 @@ def _build() -> dict:
                     (Layer("embed", 256, 50257, 1280),),
                     "abadi", R=1.0, sigma=0.8, g_scale=1e-2, zipf_s=1.1,
                     description="36 GPT-2-large blocks + 50257x1280 token embedding, Zipf(1.1) ids")
+    w[6] = Workload(6, "resnet18-conv-stack-224-B16-bf16", 16, "bf16", tuple(_resnet18_224()),
+                    "auto", gamma=0.01, sigma=1.0, g_scale=1e-2,
+                    description="ResNet-18 at 224x224: 20 convolutions (unfolded) + classifier")
     return w
 
 
@@ -164,9 +192,25 @@ def draw_embedding(wl: Workload, l: int, B: Optional[int] = None, device="cpu"):
     return ids.to(device), g.to(wl.torch_dtype)
 
 
+def draw_conv(wl: Workload, l: int, B: Optional[int] = None, device="cpu"):
+    """(x [B, C_in, H, H], dL/ds [B, C_out, Ho, Ho]) of convolution layer l (NCHW)."""
+    L = wl.layers[l]
+    cin, k, stride, pad, hin = L.conv
+    B = wl.B if B is None else B
+    ho = (hin + 2 * pad - k) // stride + 1
+    x = _randn((B, cin, hin, hin), _seed(wl.wid, l, 0), device)
+    dy = _randn((B, L.p, ho, ho), _seed(wl.wid, l, 1), device)
+    if wl.g_scale != 1.0:
+        dy.mul_(wl.g_scale)
+    return x.to(wl.torch_dtype), dy.to(wl.torch_dtype)
+
+
 def draw_layer(wl: Workload, l: int, B: Optional[int] = None, device="cpu"):
+    """(a or ids, g) of layer l; for a convolution the raw (x, dL/ds) in NCHW."""
     if wl.layers[l].kind == "embed":
         return draw_embedding(wl, l, B, device)
+    if wl.layers[l].kind == "conv":
+        return draw_conv(wl, l, B, device)
     return draw_linear(wl, l, B, device)
 
 
