@@ -139,7 +139,51 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {"agrad_dl_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "agrad_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
-                  "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip"}
+                  "agemm_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+                  "anarrow_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+                  "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
+                  "conv_prep_kernel": "paper_2210_00038_amd/csrc/conv_prep.hip"}
+
+
+def _narrow(L) -> bool:
+    return min(L.d, L.p) <= 64 and max(L.d, L.p) >= 128
+
+
+def norm_kernel(L, dtype: str = "bf16") -> str:
+    """Kernel that takes layer L's norm (the library's rule for 16-byte rows; a label only)."""
+    if L.kind == "embed":
+        return "ghost_norm_kernel"
+    if 2 * L.T * L.T < L.p * L.d:
+        return "ghost_norm_kernel"
+    if dtype != "bf16":
+        return "agemm_kernel"
+    return "anarrow_kernel" if _narrow(L) else "agemm_bf16_kernel"
+
+
+def grad_kernel(L, dtype: str = "bf16") -> str:
+    """Kernel that takes layer L's clipped gradient (same rule; a label only)."""
+    if L.kind == "embed":
+        return "embed_rows_kernel"
+    if dtype != "bf16":
+        return "agemm_kernel"
+    if L.T < 64:
+        return "agemm_bf16_kernel"
+    if _narrow(L):
+        return "anarrow_kernel"
+    return "agrad_dl_kernel" if L.T % 32 == 0 else "agrad_bf16_kernel"
+
+
+def dominant_kernel(w: wl.Workload, phase: str) -> str:
+    """Kernel with the largest share of a phase's paper-count flops."""
+    share = {}
+    for L in w.layers:
+        if phase == "norms":
+            k = norm_kernel(L, w.dtype)
+            f = 2.0 * L.T * L.T * (L.p + L.d) if k == "ghost_norm_kernel" else 2.0 * L.T * L.p * L.d
+        else:
+            k, f = grad_kernel(L, w.dtype), 2.0 * L.T * L.p * L.d
+        share[k] = share.get(k, 0.0) + f
+    return max(share, key=share.get)
 
 
 def source_hash(rel: str) -> str:
@@ -158,7 +202,7 @@ def measured_traffic(kernel: str, workload: str):
     except (OSError, ValueError):
         return None
     for e in rec.get("entries", []):
-        if e.get("kernel") == kernel and e.get("workload") == workload and \
+        if e.get("kernel") == kernel and e.get("workload") == workload and kernel in KERNEL_SOURCES and \
                 e.get("source_sha256_16") == source_hash(KERNEL_SOURCES[kernel]):
             return e.get("bytes_per_launch")
     return None
@@ -181,7 +225,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-6)")
+    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-7)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mixopt", action="store_true",
                     help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
@@ -279,33 +323,36 @@ def main():
     }
     if raw:
         phases = {"prep": {"ms": ph_ms[4], "gbs": work["prep_bytes"] / ph_ms[4] / 1e6}, **phases}
-    # Dominant kernel: the phase with the most time among the two big ones.
-    if phases["weighted_grads"]["ms"] >= phases["norms"]["ms"]:
-        ach = phases["weighted_grads"]["tflops"]
-        # bf16 layers with 32 | T take the LDS-DMA kernel, other T the register-staged one
-        gk = "agrad_dl_kernel" if all(L.T % 32 == 0 for L in w.layers if L.kind != "embed") \
-            else "agrad_bf16_kernel"
-        what = ("clip-weighted gradient, all layers in one launch" if gk == "agrad_dl_kernel" or
-                not any(L.T % 32 == 0 and L.T >= 64 for L in w.layers if L.kind != "embed")
-                else "clip-weighted gradient phase: one launch per kernel variant")
-        roof = {"kernel": f"{gk} ({what})",
-                "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                "frac": ach / peak_mfma, "traffic": measured_traffic(gk, w.name),
-                "per_launch": f"{work['gemm_flops'] / 1e9:.1f} GFLOP (sum over layers of 2 B T d p)"}
-    elif work["norm_flops"] / max(work["norm_bytes"], 1.0) > peak_mfma * 1e3 / PEAK_HBM_GBS:
-        # above the ridge point (long sequences): the norm kernels are MFMA-bound
-        ach = phases["norms"]["tflops"]
-        roof = {"kernel": "ghost_norm_kernel + agemm_bf16_kernel<inst> + reduce (all layers)",
-                "bound": "mfma", "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                "frac": ach / peak_mfma, "traffic": None,
-                "per_launch": f"{work['norm_flops'] / 1e9:.1f} GFLOP (paper count: 2BT^2(p+d) ghost, "
-                              f"2BTpd instantiated)"}
+    # Dominant phase (most time among preparation, norms and clipped
+    # gradients); its bound follows from its arithmetic intensity against the
+    # ridge point of MI355X (dense bf16 MFMA peak / HBM peak).
+    ridge = peak_mfma * 1e3 / PEAK_HBM_GBS                 # flop per byte
+    cand = {"weighted_grads": (work["gemm_flops"], work["gemm_bytes"]),
+            "norms": (work["norm_flops"], work["norm_bytes"])}
+    if raw:
+        cand["prep"] = (0.0, work["prep_bytes"])
+    dom = max(cand, key=lambda k: phases[k]["ms"])
+    flops, nbytes = cand[dom]
+    ms_dom = phases[dom]["ms"]
+    if dom == "prep":
+        gk, what = "conv_prep_kernel", "unfold + token-major transpose of every conv layer, one launch"
     else:
-        ach = phases["norms"]["gbs"]
-        roof = {"kernel": "ghost_norm_kernel + reduce (all layers)", "bound": "hbm", "achieved": ach,
-                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
-                "traffic": measured_traffic("ghost_norm_kernel", w.name),
-                "per_launch": f"{work['norm_bytes'] / 1e9:.3f} GB (a and g read once)"}
+        gk = dominant_kernel(w, dom)
+        kinds = {(grad_kernel if dom == "weighted_grads" else norm_kernel)(L, w.dtype) for L in w.layers}
+        what = ("clipped gradients" if dom == "weighted_grads" else "per-sample norms") + \
+               (", all layers in one launch" if len(kinds) == 1 else ", one launch per kernel variant")
+    if flops / max(nbytes, 1.0) > ridge:
+        ach = flops / ms_dom / 1e9
+        roof = {"kernel": f"{gk} ({what})", "bound": "mfma", "achieved": ach, "peak": peak_mfma,
+                "unit": "TFLOP/s", "frac": ach / peak_mfma,
+                "per_launch": f"{flops / 1e9:.1f} GFLOP (" + ("sum over layers of 2 B T d p" if dom == "weighted_grads"
+                              else "paper count: 2BT^2(p+d) ghost, 2BTpd instantiated") + ")"}
+    else:
+        ach = nbytes / ms_dom / 1e6
+        roof = {"kernel": f"{gk} ({what})", "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                "per_launch": f"{nbytes / 1e9:.3f} GB (inputs read once, outputs written once)"}
+    roof["traffic"] = measured_traffic(gk, w.name)
     for v in phases.values():
         for k in list(v):
             v[k] = round(float(v[k]), 4)

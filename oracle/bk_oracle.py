@@ -38,6 +38,12 @@ What is computed, and where the paper defines it
                            output channels, T = output height x width): the
                            activation a_i is the unfolded input, and the
                            output gradient is taken token-major [T, p].
+* lora_submodules / adapter_submodules -- App. E.2: a LoRA module
+                           x(W + LR) and an adapter tau(xD)U + x each split
+                           into two generalized linear sub-modules (d -> r and
+                           r -> p), whose (activation, output gradient) pairs
+                           enter the path like any other layer.  The frozen W
+                           and the residual x carry no trainable weight.
 * philox4x32_10 / noise -- Algorithm 1, Gaussian noise sigma R N(0, I).  The
                            paper does not fix a generator; the reading used
                            here is Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
@@ -65,7 +71,7 @@ __all__ = [
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
     "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
     "bk_layer_norm", "bk_stack", "per_sample_grads", "weighted_sum", "conv_out_size", "unfold",
-    "tokens_from_nchw",
+    "tokens_from_nchw", "lora_submodules", "adapter_submodules",
 ]
 
 F64 = np.float64
@@ -270,6 +276,36 @@ def tokens_from_nchw(y) -> np.ndarray:
     y = _f64(y)
     B, Cc, H, Wd = y.shape
     return y.reshape(B, Cc, H * Wd).transpose(0, 2, 1).copy()
+
+
+def lora_submodules(x, Lw, Rw, dv):
+    """LoRA (App. E.2): v = x(W + L R) with W frozen.  Sub-module 1 is
+    x -> u = x L (activation x [B,T,d], output gradient dL/du = dv R^T
+    [B,T,r]); sub-module 2 is u -> u R (activation u = x L [B,T,r], output
+    gradient dv [B,T,p]).  Returns [(a_1, g_1), (a_2, g_2)] in float64."""
+    x, Lw, Rw, dv = _f64(x), _f64(Lw), _f64(Rw), _f64(dv)
+    u = x @ Lw
+    du = dv @ Rw.T
+    return [(x, du), (u, dv)]
+
+
+def adapter_submodules(x, D, U, dv, act: str = "relu"):
+    """Adapter (App. E.2): A(x) = tau(x D) U + x.  Sub-module 1 is
+    x -> u = x D (activation x [B,T,p], output gradient
+    dL/du = (dv U^T) * tau'(u) [B,T,r]); sub-module 2 is tau(u) -> tau(u) U
+    (activation tau(u) [B,T,r], output gradient dv [B,T,p]).  The residual
+    x carries no weight.  tau = ReLU (tau'(0) taken as 0) or tanh."""
+    x, D, U, dv = _f64(x), _f64(D), _f64(U), _f64(dv)
+    u = x @ D
+    if act == "relu":
+        h, dh = np.maximum(u, 0.0), (u > 0).astype(F64)
+    elif act == "tanh":
+        h = np.tanh(u)
+        dh = 1.0 - h * h
+    else:
+        raise ValueError(act)
+    du = (dv @ U.T) * dh
+    return [(x, du), (h, dv)]
 
 
 def embed_weighted_grad(ids, g, C, V: int) -> np.ndarray:

@@ -449,7 +449,7 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 
     if (ks > 1) {
         store_partial_tile<kBM, kBN>(
-            args.tiles + ((size_t)L.ptile_off + ((size_t)sample * tiles + tile) * ks + slice) * (kBM * kBN),
+            args.tiles + L.ptile_off + (((size_t)sample * tiles + tile) * ks + slice) * (kBM * kBN),
             acc, 128 * wm, 64 * wn, lane, 1.f);
         return;
     }
@@ -495,6 +495,208 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
                 for (int i = 0; i < 16; ++i) {
                     const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
                     if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
+                }
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Narrow layers: one side of the d x p output is at most BN (32 or 64), as in
+// LoRA / adapter sub-modules (rank r) and convolutions with few output
+// channels.  The workgroup computes a 256 x BN tile of X^T diag(w) Y with X
+// the operand of the long side and Y the other: X = a, Y = g when p <= d,
+// else X = g, Y = a and the tile is G^T (the clip weight still scales whole
+// rows of the staged Y, which gives the same sum).  Four waves each own 64
+// rows x BN columns as 2 x BN/32 MFMA 32x32x16 accumulators; a k stage is
+// 64 rows, staged through two register sets (two stages in flight while the
+// waves write one to LDS and multiply).  Y's LDS rows are padded to 192
+// bytes so the four rows of a transposed read fall on distinct banks.  The
+// clipped gradient runs here only for T >= 64 (a stage then spans at most two
+// samples, whose weights come through scalar loads).
+// ---------------------------------------------------------------------------
+constexpr int kNM = 256;
+constexpr int kNSY = 192;
+
+template <bool INST, int BN>
+__global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, int n_wg) {
+    static_assert(BN == 32 || BN == 64, "narrow tile width");
+    constexpr int NY = BN / 32;           // accumulator columns per wave
+    constexpr int CPR = BN / 8;           // 16-byte chunks per staged Y row
+    constexpr int RPP = 256 / CPR;        // Y rows staged per pass of 256 threads
+    constexpr int NP = kBK / RPP;         // passes (Y chunks per thread)
+    __shared__ __attribute__((aligned(16))) char ldsA[kBK * kSA];
+    __shared__ __attribute__((aligned(16))) char ldsB[kBK * kNSY];
+    __shared__ float red[4];
+
+    const int wg = xcd_remap(blockIdx.x, n_wg);
+    int l = 0;
+    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const GemmLayer& L = args.L[l];
+    const bool sw = L.swap != 0;
+    const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
+    const int Md = sw ? p : d, Nd = sw ? d : p;
+    const int tiles = L.tm * tn;
+    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
+    const int sample = INST ? local / (tiles * ks) : 0;
+    const int rem = local - sample * tiles * ks;
+    const int tile = rem / ks, slice = rem - tile * ks;
+    const int mt = tile / tn, nt = tile - mt * tn;
+    const int m0 = mt * kNM, n0 = nt * BN;
+
+    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    const int64_t row0 = INST ? (int64_t)sample * nT : 0;
+    const uint32_t nrows = INST ? (uint32_t)nT : (uint32_t)args.B * (uint32_t)nT;
+    const uint32_t rowX = (uint32_t)Md * 2u, rowY = (uint32_t)Nd * 2u;
+    const bf16_t* X = reinterpret_cast<const bf16_t*>(sw ? L.g : L.a);
+    const bf16_t* Y = reinterpret_cast<const bf16_t*>(sw ? L.a : L.g);
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(X + row0 * Md, nrows * rowX);
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(Y + row0 * Nd, nrows * rowY);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // X tile: 64 rows x 32 chunks (rows ka + 8 j); Y tile: 64 rows x CPR
+    // chunks (rows kb + RPP j).  Rows past the last one fall outside the
+    // buffer resource and chunks past the last column get an out-of-range
+    // offset: both load as zeros.
+    const int ca = (tid & 31) * 8, ka = tid >> 5;
+    const int cb = (tid % CPR) * 8, kb = tid / CPR;
+    const uint32_t offA = (m0 + ca < Md) ? (uint32_t)ka * rowX + (uint32_t)(m0 + ca) * 2u : kOut;
+    const uint32_t offB = (n0 + cb < Nd) ? (uint32_t)kb * rowY + (uint32_t)(n0 + cb) * 2u : kOut;
+
+    f32x16_t acc[2][NY];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < NY; ++y)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
+
+    // Two register sets of staged rows: the loads of stages st + 1 and st + 2
+    // are in flight while stage st is written to LDS and multiplied.  Every
+    // fetch is issued (a stage past the slice loads zeros through the
+    // out-of-range offset, without memory traffic) and stages run in pairs,
+    // so the loop is straight-line and each wait covers exactly one set.
+    uint4 va0[8], vb0[NP], va1[8], vb1[NP];
+    float cw0[NP], cw1[NP];
+    const uint32_t nst_all = (nrows + kBK - 1) / kBK;
+    const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
+    const uint32_t nst = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
+    // Clip weights come through the scalar cache (C is read-only here), so
+    // their loads do not sit in the vector-memory count between two sets.
+    const __attribute__((address_space(4))) float* Cs = (const __attribute__((address_space(4))) float*)args.C;
+    auto fetch = [&](uint4 (&va)[8], uint4 (&vb)[NP], float (&cw)[NP], uint32_t st) {
+        const uint32_t k0 = st * kBK;
+        const bool live = st < nst;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            va[j] = buffer_load16(rA, (offA == kOut || !live) ? kOut : offA + (k0 + 8u * j) * rowX);
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+            vb[j] = buffer_load16(rB, (offB == kOut || !live) ? kOut : offB + (k0 + (uint32_t)RPP * j) * rowY);
+        if constexpr (!INST) {
+            // Clip weight of each staged row: C[k / T].  The host sends only
+            // T >= 64 here, so the 64 rows of a stage span at most two
+            // samples.  A stage past the slice (possibly with no rows at all:
+            // B T == 0) reads no C.
+            if (!live) {
+#pragma unroll
+                for (int j = 0; j < NP; ++j) cw[j] = 0.f;
+            } else {
+                const uint32_t q0 = __builtin_amdgcn_readfirstlane(k0 / (uint32_t)nT);
+                const uint32_t split = (q0 + 1u) * (uint32_t)nT - k0;
+                const float c0 = Cs[min(q0, (uint32_t)args.B - 1u)];
+                const float c1 = Cs[min(q0 + 1u, (uint32_t)args.B - 1u)];
+#pragma unroll
+                for (int j = 0; j < NP; ++j) cw[j] = ((uint32_t)(kb + RPP * j) < split) ? c0 : c1;
+            }
+        }
+    };
+    // Stage st from one register set; then that set's loads of stage st + 2.
+    auto stage = [&](uint4 (&va)[8], uint4 (&vb)[NP], float (&cw)[NP], uint32_t st) {
+        lds_barrier();
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            *reinterpret_cast<uint4*>(ldsA + (ka + 8 * j) * kSA + ca * 2) = va[j];
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+            uint4 v = vb[j];
+            if constexpr (!INST)
+                v = make_uint4(scale_bf16x2(v.x, cw[j]), scale_bf16x2(v.y, cw[j]), scale_bf16x2(v.z, cw[j]),
+                               scale_bf16x2(v.w, cw[j]));
+            *reinterpret_cast<uint4*>(ldsB + (kb + RPP * j) * kNSY + cb * 2) = v;
+        }
+        lds_barrier();
+        fetch(va, vb, cw, st + 2);
+        uint4 fa[2][2], fb[2][NY];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) fa[0][x] = frag_tr<kSA>(ldsA, 0, 64 * wave + 32 * x, lane);
+#pragma unroll
+        for (int y = 0; y < NY; ++y) fb[0][y] = frag_tr<kNSY>(ldsB, 0, 32 * y, lane);
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk + 1 < kBK / 16) {
+#pragma unroll
+                for (int x = 0; x < 2; ++x) fa[nxt][x] = frag_tr<kSA>(ldsA, 16 * (kk + 1), 64 * wave + 32 * x, lane);
+#pragma unroll
+                for (int y = 0; y < NY; ++y) fb[nxt][y] = frag_tr<kNSY>(ldsB, 16 * (kk + 1), 32 * y, lane);
+            }
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < NY; ++y) Mfma<bf16_t>::step(acc[x][y], fa[cur][x], fb[cur][y]);
+        }
+    };
+
+    fetch(va0, vb0, cw0, st_begin);
+    fetch(va1, vb1, cw1, st_begin + 1);
+    for (uint32_t st = st_begin; st < nst; st += 2) {
+        stage(va0, vb0, cw0, st);
+        stage(va1, vb1, cw1, st + 1);    // zeros when st + 1 == nst
+    }
+
+    // Element (m, n) of the tile is G[m][n], or G[n][m] when swapped.
+    const int r0 = 64 * wave;
+    if (ks > 1) {
+        float* P = args.tiles + L.ptile_off + (((size_t)sample * tiles + tile) * ks + slice) * (kNM * BN);
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < NY; ++y) {
+                const int n = 32 * y + (lane & 31);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) P[(r0 + 32 * x + acc_row(i, lane)) * BN + n] = acc[x][y][i];
+            }
+        return;
+    }
+    float* out = INST ? (L.G ? L.G + (size_t)sample * d * p : nullptr) : L.G;
+    if constexpr (INST) {
+        float s = 0.f;
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < NY; ++y) {
+                const bool col_ok = n0 + 32 * y + (lane & 31) < Nd;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const bool ok = col_ok && (m0 + r0 + 32 * x + acc_row(i, lane) < Md);
+                    s += ok ? acc[x][y][i] * acc[x][y][i] : 0.f;
+                }
+            }
+        const float tot = block_sum_256(s, red);
+        if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
+    }
+    if (out) {
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < NY; ++y) {
+                const int n = n0 + 32 * y + (lane & 31);
+                if (n >= Nd) continue;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int m = m0 + r0 + 32 * x + acc_row(i, lane);
+                    if (m < Md) out[sw ? (size_t)n * p + m : (size_t)m * p + n] = acc[x][y][i];
                 }
             }
     }
@@ -702,7 +904,7 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     if (st < nst) stage(std::integral_constant<int, 0>{});
 
     if (ks > 1) {
-        store_partial_tile<kGM, kGN>(args.tiles + ((size_t)L.ptile_off + (size_t)tile * ks + slice) * (kGM * kGN),
+        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)tile * ks + slice) * (kGM * kGN),
                                      acc, 128 * wm, 64 * wn, lane, 1.f);
         return;
     }
@@ -994,7 +1196,7 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     wait_vmcnt<0>();
 
     if (ks > 1) {
-        store_partial_tile<kGM, kGN>(args.tiles + ((size_t)L.ptile_off + (size_t)tile * ks + slice) * (kGM * kGN),
+        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)tile * ks + slice) * (kGM * kGN),
                                      acc, 128 * wm, 64 * wn, lane, c_last);
         return;
     }
@@ -1035,7 +1237,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
     const int mt = tile / L.tn, nt = tile - mt * L.tn;
     const int e = ch * kSplitRedWG + 4 * (int)threadIdx.x;
     const int m = mt * TM + e / TN, n = nt * TN + e % TN;
-    const float* src = args.tiles + ((size_t)L.ptile_off + (size_t)tg * max(L.ksplit, 1)) * (TM * TN) + e;
+    const float* src = args.tiles + L.ptile_off + (size_t)tg * max(L.ksplit, 1) * (TM * TN) + e;
     float4 sum = *reinterpret_cast<const float4*>(src);
     for (int q = 1; q < max(L.ksplit, 1); ++q) {
         const float4 v = *reinterpret_cast<const float4*>(src + (size_t)q * (TM * TN));
@@ -1045,38 +1247,54 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
         sum.w += v.w;
     }
     const float r[4] = {sum.x, sum.y, sum.z, sum.w};
-    const bool row_ok = m < L.d;
+    // Tile rows run along d, or along p for a swapped (narrow) layer.
+    const bool sw = L.swap != 0;
+    const int Md = sw ? L.p : L.d, Nd = sw ? L.d : L.p;
+    const bool row_ok = m < Md;
     float* out = L.G ? L.G + (size_t)sample * L.d * L.p : nullptr;
     if constexpr (INST) {
         float sq = 0.f;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sq += (row_ok && n + j < L.p) ? r[j] * r[j] : 0.f;
+        for (int j = 0; j < 4; ++j) sq += (row_ok && n + j < Nd) ? r[j] * r[j] : 0.f;
         const float tot = block_sum_256(sq, red);
         if (threadIdx.x == 0) args.part[(size_t)L.part_off + (size_t)tg * CH + ch] = tot;
     }
     if (out && row_ok) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            if (n + j < L.p) out[(size_t)m * L.p + n + j] = r[j];
+            if (n + j < Nd) out[sw ? (size_t)(n + j) * L.p + m : (size_t)m * L.p + n + j] = r[j];
     }
 }
 
 }  // namespace
 
-int gemm_tile_m(GemmVariant v) {
-    return (v == GemmVariant::Grad || v == GemmVariant::GradDL) ? kGM : v == GemmVariant::Wide ? kBM : kTile;
-}
-int gemm_tile_n(GemmVariant v) {
-    return (v == GemmVariant::Grad || v == GemmVariant::GradDL) ? kGN : v == GemmVariant::Wide ? kBN : kTile;
+GemmGeom gemm_geom(GemmVariant v, int64_t d, int64_t p) {
+    auto cdiv = [](int64_t a, int64_t b) { return (a + b - 1) / b; };
+    switch (v) {
+        case GemmVariant::Grad:
+        case GemmVariant::GradDL: return {cdiv(d, kGM), cdiv(p, kGN), (int64_t)kGM * kGN, false};
+        case GemmVariant::Wide: return {cdiv(d, kBM), cdiv(p, kBN), (int64_t)kBM * kBN, false};
+        case GemmVariant::Narrow32:
+        case GemmVariant::Narrow64: {
+            const int64_t bn = v == GemmVariant::Narrow32 ? 32 : 64;
+            const bool sw = d < p;
+            return {cdiv(sw ? p : d, kNM), cdiv(sw ? d : p, bn), kNM * bn, sw};
+        }
+        default: return {cdiv(d, kTile), cdiv(p, kTile), (int64_t)kTile * kTile, false};
+    }
 }
 
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned) {
     const int64_t es = bf16 ? 2 : 4;
     const bool vec = aligned && (d * es) % 16 == 0 && (p * es) % 16 == 0;
     if (!vec) return GemmVariant::Scalar;
-    // The wide kernels address a layer's rows (plus three stages of overrun)
-    // with 32-bit buffer offsets.
-    if (bf16 && (rows + 3 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) return GemmVariant::Wide;
+    // The wide and narrow kernels address a layer's rows (plus three stages
+    // of overrun) with 32-bit buffer offsets.
+    if (bf16 && (rows + 3 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) {
+        const int64_t lo = std::min(d, p), hi = std::max(d, p);
+        if (lo <= 64 && hi >= 128) return lo <= 32 ? GemmVariant::Narrow32 : GemmVariant::Narrow64;
+        return GemmVariant::Wide;
+    }
     return GemmVariant::Vec;
 }
 
@@ -1088,7 +1306,13 @@ hipError_t launch_split_reduce(const GemmArgs& args, int n_wg, bool inst_norm, G
         hipLaunchKernelGGL((split_reduce_kernel<kBM, kBN, true>), grid, block, 0, s, args);
     else if (!inst_norm && (v == GemmVariant::Grad || v == GemmVariant::GradDL))
         hipLaunchKernelGGL((split_reduce_kernel<kGM, kGN, false>), grid, block, 0, s, args);
-    else
+    else if (v == GemmVariant::Narrow32) {
+        if (inst_norm) hipLaunchKernelGGL((split_reduce_kernel<kNM, 32, true>), grid, block, 0, s, args);
+        else hipLaunchKernelGGL((split_reduce_kernel<kNM, 32, false>), grid, block, 0, s, args);
+    } else if (v == GemmVariant::Narrow64) {
+        if (inst_norm) hipLaunchKernelGGL((split_reduce_kernel<kNM, 64, true>), grid, block, 0, s, args);
+        else hipLaunchKernelGGL((split_reduce_kernel<kNM, 64, false>), grid, block, 0, s, args);
+    } else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -1111,6 +1335,16 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
     if (v == GemmVariant::Wide) {
         if (inst_norm) hipLaunchKernelGGL(agemm_bf16_kernel<true>, grid, block, 0, s, args, n_wg);
         else hipLaunchKernelGGL(agemm_bf16_kernel<false>, grid, block, 0, s, args, n_wg);
+        return hipGetLastError();
+    }
+    if (v == GemmVariant::Narrow32) {
+        if (inst_norm) hipLaunchKernelGGL((anarrow_kernel<true, 32>), grid, block, 0, s, args, n_wg);
+        else hipLaunchKernelGGL((anarrow_kernel<false, 32>), grid, block, 0, s, args, n_wg);
+        return hipGetLastError();
+    }
+    if (v == GemmVariant::Narrow64) {
+        if (inst_norm) hipLaunchKernelGGL((anarrow_kernel<true, 64>), grid, block, 0, s, args, n_wg);
+        else hipLaunchKernelGGL((anarrow_kernel<false, 64>), grid, block, 0, s, args, n_wg);
         return hipGetLastError();
     }
 #define BK_GEMM(T, I, V) hipLaunchKernelGGL((agemm_kernel<T, I, V>), grid, block, 0, s, args)

@@ -77,14 +77,16 @@ struct NormPlan {
     int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads;
                         // instantiation: bk::GemmVariant
     int64_t tiles = 0;  // instantiation: output tiles per sample
-    int64_t ksplit = 1; // instantiation: K slices per tile (wide kernel only)
+    int64_t ksplit = 1; // instantiation: K slices per tile (wide and narrow kernels)
+    int64_t tile_elems = 0;   // instantiation: floats of one K-split partial tile
 };
 
-// Tile shape and slice-reduction chunks of the split-capable kernels.
-constexpr int64_t kWideTile = 256 * 128;        // agemm_bf16_kernel
-constexpr int64_t kGradTile = 256 * 256;        // agrad_* kernels
-constexpr int64_t kWideChunks = kWideTile / bk::kSplitRedWG;
-constexpr int64_t kGradChunks = kGradTile / bk::kSplitRedWG;
+// Variants whose kernels can split a tile's contraction into K slices.
+bool inst_splits(int var) {
+    return var == (int)bk::GemmVariant::Wide || var == (int)bk::GemmVariant::Narrow32 ||
+           var == (int)bk::GemmVariant::Narrow64;
+}
+bool is_narrow(bk::GemmVariant v) { return v == bk::GemmVariant::Narrow32 || v == bk::GemmVariant::Narrow64; }
 
 // K slices of an instantiated norm on the wide kernel: when a layer gives
 // fewer than 128 workgroups (few samples, few tiles, long T), cut each
@@ -102,12 +104,21 @@ int64_t grad_ksplit(int64_t tiles, int64_t nst) {
     return std::min<int64_t>(256, cdiv(nst, 32));
 }
 
+// The same for the narrow kernels (64-row stages, far less work per stage):
+// a layer with fewer than 32 tiles gets slices of about 16 stages, at most 64.
+int64_t narrow_grad_ksplit(int64_t tiles, int64_t nst) {
+    if (tiles >= 32 || nst < 32) return 1;
+    return std::min<int64_t>(64, cdiv(nst, 16));
+}
+
 void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
     const size_t es = elem_bytes(dt);
     if (np.path == Path::Inst) {
         const auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
+        const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
         np.var = (int)v;
-        np.tiles = cdiv(L.d, bk::gemm_tile_m(v)) * cdiv(L.p, bk::gemm_tile_n(v));
+        np.tiles = geo.tm * geo.tn;
+        np.tile_elems = geo.tile_elems;
         np.npart = np.tiles;
     } else {
         const int64_t nsb = cdiv(L.T, bk::kSuper);
@@ -121,12 +132,12 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
     }
 }
 
-// Workgroup count, and the K split of instantiated norms on the wide kernel
-// (a split layer reports one partial per slice-reduction chunk).
+// Workgroup count, and the K split of instantiated norms on the wide and
+// narrow kernels (a split layer reports one partial per slice-reduction chunk).
 void finish_norm_plan(NormPlan& np, const bk_layer& L, int64_t B) {
-    if (np.path == Path::Inst && np.var == (int)bk::GemmVariant::Wide) {
+    if (np.path == Path::Inst && inst_splits(np.var)) {
         np.ksplit = inst_ksplit(B, np.tiles, L.T);
-        if (np.ksplit > 1) np.npart = np.tiles * kWideChunks;
+        if (np.ksplit > 1) np.npart = np.tiles * (np.tile_elems / bk::kSplitRedWG);
     }
     np.nwg = np.path == Path::Inst ? B * np.tiles * np.ksplit : B * np.npart;
 }
@@ -134,7 +145,7 @@ void finish_norm_plan(NormPlan& np, const bk_layer& L, int64_t B) {
 // Partial sums of a layer's norm (floats) and its K-split partial tiles (floats).
 size_t norm_part_floats(const NormPlan& np, int64_t B) { return (size_t)(B * np.npart); }
 size_t norm_tile_floats(const NormPlan& np, int64_t B) {
-    return np.ksplit > 1 ? (size_t)(B * np.tiles * np.ksplit * kWideTile) : 0;
+    return np.ksplit > 1 ? (size_t)(B * np.tiles * np.ksplit * np.tile_elems) : 0;
 }
 size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
     return align_up(norm_part_floats(np, B) * sizeof(float)) + norm_tile_floats(np, B) * sizeof(float);
@@ -229,10 +240,9 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
         const NormPlan np = norm_plan(layers[l], dt, B);
         items.push_back({l, np, off, toff});
         off += (int64_t)(align_up(norm_part_floats(np, B) * sizeof(float)) / sizeof(float));
-        toff += (int64_t)(norm_tile_floats(np, B) / kWideTile);
+        toff += (int64_t)norm_tile_floats(np, B);
     }
     float* tiles = part + off;
-    if (toff > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many partial tiles", fn);
 
     auto flush_ghost = [&](std::vector<const Item*>& v, bool embed, bool vec) -> bk_status {
         if (v.empty()) return BK_OK;
@@ -279,15 +289,17 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bk::GemmVariant(var)));
-            g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(var)));
+            const bk::GemmGeom geo = bk::gemm_geom(bk::GemmVariant(var), L.d, L.p);
+            g.tm = (int32_t)geo.tm;
+            g.tn = (int32_t)geo.tn;
+            g.swap = geo.swap ? 1 : 0;
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
             g.ksplit = (int32_t)np.ksplit;
-            g.ptile_off = (int32_t)v[k]->tile_off;
+            g.ptile_off = v[k]->tile_off;
             g.red_begin = (int32_t)red;
             wg += np.nwg;
-            if (np.ksplit > 1) red += B * np.tiles * kWideChunks;
+            if (np.ksplit > 1) red += B * np.tiles * (np.tile_elems / bk::kSplitRedWG);
         }
         if (wg > INT32_MAX || red > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
         hipError_t e = bk::launch_gemm(a, (int)wg, bf16, true, bk::GemmVariant(var), s);
@@ -299,7 +311,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
 
     // Group by (path, kernel variant), preserving layer order inside a group.
     for (int kind = 0; kind < 3; ++kind)
-        for (int var = 0; var < 3; ++var) {
+        for (int var = 0; var < (kind == 2 ? bk::kGemmVariants : 2); ++var) {
             std::vector<const Item*> batch;
             for (const Item& it : items) {
                 const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
@@ -334,23 +346,28 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     return BK_OK;
 }
 
-// Kernel variant of a linear layer's clipped gradient: the Wide layers with
-// T >= 64 run on the 256 x 256 kernels, with the weights on the accumulators
+// Kernel variant of a linear layer's clipped gradient: narrow layers with
+// T >= 64 run on the narrow kernel (shorter T on the wide one), the other
+// Wide layers with T >= 64 on the 256 x 256 kernels, with the weights on the accumulators
 // when the stage height divides T (and B fits the kernel's LDS table), else
 // on g.
 bk::GemmVariant grad_variant(const bk_layer& L, bool bf16, int64_t B) {
     const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
+    if (is_narrow(v)) return L.T < 64 ? bk::GemmVariant::Wide : v;   // narrow kernel: T >= 64
     if (v != bk::GemmVariant::Wide || L.T < 64) return v;
     return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL : bk::GemmVariant::Grad;
 }
 
 // Tiles and K slices of a linear layer's clipped gradient on variant v.
-struct GradPlan { int64_t tm, tn, ksplit; };
+struct GradPlan { int64_t tm, tn, ksplit, tile_elems; bool swap; };
 GradPlan grad_plan(const bk_layer& L, bk::GemmVariant v, int64_t B) {
-    GradPlan g{cdiv(L.d, bk::gemm_tile_m(v)), cdiv(L.p, bk::gemm_tile_n(v)), 1};
+    const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
+    GradPlan g{geo.tm, geo.tn, 1, geo.tile_elems, geo.swap};
     if (v == bk::GemmVariant::Grad || v == bk::GemmVariant::GradDL) {
         const int64_t rows = v == bk::GemmVariant::Grad ? 64 : bk::kDLStageRows;
         g.ksplit = grad_ksplit(g.tm * g.tn, cdiv(B * L.T, rows));
+    } else if (is_narrow(v)) {
+        g.ksplit = narrow_grad_ksplit(g.tm * g.tn, cdiv(B * L.T, 64));
     }
     return g;
 }
@@ -362,7 +379,7 @@ size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t
         if (L.kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, L.T, L.d));
         if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
         const GradPlan g = grad_plan(L, grad_variant(L, dt == BK_BF16, B), B);
-        if (g.ksplit > 1) tiles += (size_t)(g.tm * g.tn * g.ksplit * kGradTile) * sizeof(float);
+        if (g.ksplit > 1) tiles += (size_t)(g.tm * g.tn * g.ksplit * g.tile_elems) * sizeof(float);
     }
     return std::max(tot, tiles);
 }
@@ -397,7 +414,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     // Grouped launches by kernel variant.  Layers with few output tiles run
     // K-split (grad_plan); their partial tiles sit in the workspace (launches
     // follow each other on the stream, so each starts from offset 0).
-    for (int var = 0; var < 5; ++var) {
+    for (int var = 0; var < bk::kGemmVariants; ++var) {
         bk::GemmArgs a{};
         a.B = (int32_t)B;
         a.C = C;
@@ -406,7 +423,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         int64_t wg = 0, ptile = 0, red = 0;
         auto flush = [&]() -> bk_status {
             if (a.n == 0) return BK_OK;
-            if (wg > INT32_MAX || red > INT32_MAX || ptile > INT32_MAX)
+            if (wg > INT32_MAX || red > INT32_MAX)
                 return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
             hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, bk::GemmVariant(var), s);
             if (e == hipSuccess && red > 0)
@@ -434,12 +451,13 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.wg_begin = (int32_t)wg;
             g.part_off = 0;
             g.ksplit = (int32_t)gp.ksplit;
-            g.ptile_off = (int32_t)ptile;
+            g.swap = gp.swap ? 1 : 0;
+            g.ptile_off = ptile;
             g.red_begin = (int32_t)red;
             wg += gp.tm * gp.tn * gp.ksplit;
             if (gp.ksplit > 1) {
-                ptile += gp.tm * gp.tn * gp.ksplit;
-                red += gp.tm * gp.tn * kGradChunks;
+                ptile += gp.tm * gp.tn * gp.ksplit * gp.tile_elems;
+                red += gp.tm * gp.tn * (gp.tile_elems / bk::kSplitRedWG);
             }
             if (a.n == bk::kMaxGemm && (st = flush()) != BK_OK) return st;
         }
@@ -487,6 +505,11 @@ bk_status add_noise_layers(const char* fn, float* const* G, const int64_t* nel,
     a.std = std;
     a.seed = seed;
     a.step = step;
+    // Workgroup grain: 256 counter blocks each while the whole call has
+    // fewer than 2048 such groups, up to kNoiseBlocksPerWG for large calls.
+    int64_t total_q = 0;
+    for (int64_t l = 0; l < n; ++l) total_q += cdiv(nel[l], 4);
+    a.bpw = 256u * (uint32_t)std::min<int64_t>(bk::kNoiseBlocksPerWG / 256, std::max<int64_t>(1, cdiv(total_q, 256 * 2048)));
     int64_t wg = 0;
     auto flush = [&]() -> bk_status {
         if (a.n == 0) return BK_OK;
@@ -503,7 +526,7 @@ bk_status add_noise_layers(const char* fn, float* const* G, const int64_t* nel,
         L.n = nel[l];
         L.tensor_id = tensor_id[l];
         L.wg_begin = (uint32_t)wg;
-        wg += cdiv(cdiv(nel[l], 4), bk::kNoiseBlocksPerWG);
+        wg += cdiv(cdiv(nel[l], 4), (int64_t)a.bpw);
         if (a.n == bk::kMaxNoise) {
             bk_status st = flush();
             if (st != BK_OK) return st;
@@ -566,12 +589,14 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.T = (int32_t)L.T;
         g.d = (int32_t)L.d;
         g.p = (int32_t)L.p;
-        g.tm = (int32_t)cdiv(L.d, bk::gemm_tile_m(bk::GemmVariant(np.var)));
-        g.tn = (int32_t)cdiv(L.p, bk::gemm_tile_n(bk::GemmVariant(np.var)));
+        const bk::GemmGeom geo = bk::gemm_geom(bk::GemmVariant(np.var), L.d, L.p);
+        g.tm = (int32_t)geo.tm;
+        g.tn = (int32_t)geo.tn;
+        g.swap = geo.swap ? 1 : 0;
         g.ksplit = (int32_t)np.ksplit;
         a.tiles = part + align_up(norm_part_floats(np, B) * sizeof(float)) / sizeof(float);
         e = bk::launch_gemm(a, (int)np.nwg, dt == BK_BF16, true, bk::GemmVariant(np.var), s);
-        const int64_t red = np.ksplit > 1 ? B * np.tiles * kWideChunks : 0;
+        const int64_t red = np.ksplit > 1 ? B * np.tiles * (np.tile_elems / bk::kSplitRedWG) : 0;
         if (red > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
         if (e == hipSuccess && red > 0)
             e = bk::launch_split_reduce(a, (int)red, true, bk::GemmVariant(np.var), s);

@@ -50,8 +50,9 @@ struct GemmLayer {
     // ptile_off on, [sample][tile][slice]); a second kernel adds the slices in
     // order, its workgroups for this layer starting at red_begin.
     int32_t ksplit;     // 1: no split
-    int32_t ptile_off;
     int32_t red_begin;
+    int32_t swap;       // narrow kernels: the tile is G^T (rows along p, d < p)
+    int64_t ptile_off;  // first float of this layer's partial tiles
 };
 constexpr int kMaxGemm = 48;
 struct GemmArgs {
@@ -89,10 +90,10 @@ struct NoiseArgs {
     float std;
     uint64_t seed;
     uint32_t step;
-    uint32_t pad;
+    uint32_t bpw;       // Philox counter blocks per workgroup (256 .. kNoiseBlocksPerWG, 256 | bpw)
     NoiseLayer L[kMaxNoise];
 };
-constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by one workgroup
+constexpr int kNoiseBlocksPerWG = 4 * 256;   // most counter blocks handled by one workgroup
 
 // Kernel variant of the a^T g GEMMs for one layer:
 //  Scalar: element loads (rows not 16-byte multiples / unaligned), 128 x 128;
@@ -101,7 +102,10 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // Philox counter blocks handled by
 //  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads (T >= 64);
 //  GradDL: as Grad with LDS DMA and the weights on the accumulators
 //          (kDLStageRows divides T, B <= kDMaxB).
-enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4 };
+//  Narrow32 / Narrow64: bf16, one side of d x p at most 32 / 64, tiles of
+//          256 along the long side (operands swapped when d < p).
+enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4, Narrow32 = 5, Narrow64 = 6 };
+constexpr int kGemmVariants = 7;
 constexpr int kDMaxB = 4096;
 #ifndef BK_DL_KS
 #define BK_DL_KS 32
@@ -112,8 +116,13 @@ constexpr int kDMaxB = 4096;
 constexpr int kDLStageRows = BK_DL_KS;   // k rows per stage of the GradDL kernel
 constexpr int kDLBuffers = BK_DL_NB;     // its LDS stage buffers
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
-int gemm_tile_m(GemmVariant v);
-int gemm_tile_n(GemmVariant v);
+// Output tiles of a d x p layer on variant v: tm x tn tiles of tile_elems
+// floats (a K-split partial tile), rows along p when swap.
+struct GemmGeom {
+    int64_t tm, tn, tile_elems;
+    bool swap;
+};
+GemmGeom gemm_geom(GemmVariant v, int64_t d, int64_t p);
 
 // ---- weighted sum of stored per-sample gradients -------------------------------
 struct WsumLayer {

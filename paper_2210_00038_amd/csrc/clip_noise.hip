@@ -25,8 +25,17 @@ __global__ __launch_bounds__(256) void clip_kernel(const float* __restrict__ nor
                                                    float* __restrict__ C, float* __restrict__ total) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= B) return;
+    // Layers in ascending order; sixteen loads are issued ahead of their adds.
     double s = 0.0;
-    for (int64_t l = 0; l < L; ++l) s += (double)norm_sq[l * B + i];
+    int64_t l = 0;
+    for (; l + 16 <= L; l += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = norm_sq[(l + u) * B + i];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s += (double)v[u];
+    }
+    for (; l < L; ++l) s += (double)norm_sq[l * B + i];
     const double nrm = sqrt(s);
     double c;
     if (mode == 0) {                       // Abadi: min(R / ||g||, 1)
@@ -40,7 +49,7 @@ __global__ __launch_bounds__(256) void clip_kernel(const float* __restrict__ nor
 }
 
 // G[e] += std * z_e.  Workgroup w handles counter blocks
-// [w * kNoiseBlocksPerWG, (w + 1) * kNoiseBlocksPerWG) of its tensor.
+// [w * bpw, (w + 1) * bpw) of its tensor (bpw = args.bpw, a multiple of 256).
 __global__ __launch_bounds__(256) void noise_kernel(const NoiseArgs args) {
     const uint32_t wg = blockIdx.x;
     int l = 0;
@@ -49,9 +58,9 @@ __global__ __launch_bounds__(256) void noise_kernel(const NoiseArgs args) {
     float* G = L.G;
     const int64_t n = L.n;
     const int64_t nq = (n + 3) / 4;
-    const int64_t q_begin = (int64_t)(wg - L.wg_begin) * kNoiseBlocksPerWG;
+    const int64_t q_begin = (int64_t)(wg - L.wg_begin) * args.bpw;
     const bool vec = (reinterpret_cast<uintptr_t>(G) & 15u) == 0;
-    for (int k = 0; k < kNoiseBlocksPerWG / 256; ++k) {
+    for (int k = 0; k < (int)(args.bpw / 256); ++k) {
         const int64_t q = q_begin + k * 256 + threadIdx.x;
         if (q >= nq) break;
         const float4 z = normal4(args.seed, L.tensor_id, args.step, (uint64_t)q);

@@ -7,7 +7,7 @@ samples what the oracle can compute one piece at a time:
   * the per-sample norms of sampled layers (first, middle, last, every path
     kind present), against the oracle on the same inputs;
   * the clip factors and totals from the GPU's whole [L, B] norm table;
-  * sampled 32 x 32 blocks of the clipped gradients of the sampled layers
+  * sampled blocks (up to 32 x 32) of the clipped gradients of the sampled layers
     (run without noise), against the oracle's clipped gradient restricted to
     those rows and columns, and whole rows of the embedding gradient
     (most frequent ids and absent ids);
@@ -61,7 +61,7 @@ def _sample_layers(w):
     return sorted(pick | set(kinds.values()))
 
 
-@pytest.mark.parametrize("wid", [2, 3, 4, 5])
+@pytest.mark.parametrize("wid", [2, 3, 4, 5, 7])
 def test_full_stack_sampled_parity(bk, wid):
     w = wl.get(wid)
     print(f"workload {wid}: {w.name}, {len(w.layers)} layers, B={w.B}", flush=True)
@@ -112,8 +112,8 @@ def test_full_stack_sampled_parity(bk, wid):
             nz = counts[rows] > 0
             err = np.linalg.norm(got[nz] - ref[nz]) / np.linalg.norm(ref[nz])
         else:
-            rows = np.sort(rng.choice(L.d, 32, replace=False))
-            cols = np.sort(rng.choice(L.p, 32, replace=False))
+            rows = np.sort(rng.choice(L.d, min(32, L.d), replace=False))
+            cols = np.sort(rng.choice(L.p, min(32, L.p), replace=False))
             ref = oracle.weighted_grad(x[:, :, torch.from_numpy(rows)], g[:, :, torch.from_numpy(cols)], C)
             got = sel(Gg, rows, cols)
             err = np.linalg.norm(got - ref) / np.linalg.norm(ref)

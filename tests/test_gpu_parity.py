@@ -397,6 +397,69 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
 
 
+# ------------------------------------------- narrow layers (one side <= 64)
+@pytest.mark.parametrize("B,T,d,p", [
+    (3, 50, 768, 16),       # 256 x 32 tiles, rows along d
+    (3, 50, 16, 768),       # operands swapped: rows along p
+    (2, 130, 576, 64),      # 256 x 64 tiles (a convolution with 64 output channels)
+    (2, 33, 64, 520),       # swapped, ragged last tile
+    (4, 20, 8, 136),        # rank 8, T < one stage
+    (2, 4096, 256, 24),     # long T: the instantiated norm splits K
+    (8, 2048, 40, 1000),    # clipped gradient splits K (4 tiles x 16 slices), swapped
+])
+def test_narrow_layers_match_oracle(bk, B, T, d, p):
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B * T + d + p, g_scale=1e-2)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(T)) + 0.1
+    C[0] = 0.0
+    ad, gd = a.to(DEV), g.to(DEV)
+    ref_n = oracle.linear_norm_sq(a, g)
+    assert _rel(bk.bk_inst_norm(ad, gd).cpu().numpy(), ref_n) <= NORM_TOL[torch.bfloat16]
+    G = bk.bk_weighted_grad(ad, gd, C.to(DEV)).cpu().numpy()
+    assert _frob(G, oracle.weighted_grad(a, g, C)) <= GRAD_TOL[torch.bfloat16]
+    if B * d * p <= 4 * 1024 * 1024:
+        norm, P = bk.bk_per_sample_grads(ad, gd)
+        P = P.cpu().numpy()
+        ref_P = oracle.per_sample_grads(a, g)
+        for i in range(B):
+            assert _frob(P[i], ref_P[i]) <= GRAD_TOL[torch.bfloat16], i
+        assert _rel(norm.cpu().numpy(), ref_n) <= NORM_TOL[torch.bfloat16]
+
+
+# ------------------------------------------- LoRA / adapter sub-modules (App. E.2)
+@pytest.mark.parametrize("module,d,r,T,B", [
+    ("lora", 768, 16, 128, 4),      # the rank-16 LoRA of the GPT-2-small shapes: both instantiate
+    ("lora", 96, 1, 24, 3),         # rank one
+    ("lora", 200, 12, 40, 5),       # r and d not multiples of 8
+    ("lora", 256, 1024, 16, 2),     # the paper's largest rank: both sub-modules ghost
+    ("adapter", 768, 64, 100, 3),   # adapter p -> r -> p, ReLU, ragged T
+    ("adapter", 130, 8, 33, 4),
+])
+def test_lora_adapter_stack_matches_oracle(bk, module, d, r, T, B):
+    """Sub-modules of LoRA x(W + LR) / adapter relu(xD)U + x, decomposed by the
+    oracle from drawn x, weights and output gradients, rounded to bf16, through
+    the whole path (both sub-modules of two modules in one stack)."""
+    gen = torch.Generator().manual_seed(d + r + T)
+    layers, ins = [], []
+    for _ in range(2):
+        x = torch.randn(B, T, d, generator=gen, dtype=torch.float64)
+        A1 = torch.randn(d, r, generator=gen, dtype=torch.float64) / np.sqrt(d)
+        A2 = torch.randn(r, d, generator=gen, dtype=torch.float64) / np.sqrt(r)
+        dv = torch.randn(B, T, d, generator=gen, dtype=torch.float64) * 1e-2
+        subs = (oracle.lora_submodules(x, A1, A2, dv) if module == "lora"
+                else oracle.adapter_submodules(x, A1, A2, dv, "relu"))
+        for a, g in subs:
+            ins.append((torch.from_numpy(a).to(torch.bfloat16), torch.from_numpy(g).to(torch.bfloat16)))
+            layers.append(wl.Layer("linear", T, a.shape[2], g.shape[2]))
+    norms, C, tot, G = _run_stack(bk, layers, ins, B, torch.bfloat16, bk.BK_CLIP_AUTO, 1.0, 0.01, 0.0, seed=5)
+    ref = oracle.bk_stack(layers, ins, "auto", 1.0, 0.01, 0.0, seed=5, with_noise=False)
+    want_path = "ghost" if 2 * T * T < d * r else "inst"
+    assert ref["paths"] == [want_path] * 4
+    assert _rel(norms, ref["norms"]) <= NORM_TOL[torch.bfloat16]
+    assert _rel(C, ref["C"]) <= NORM_TOL[torch.bfloat16]
+    for l in range(len(layers)):
+        assert _frob(G[l], ref["G"][l]) <= GRAD_TOL[torch.bfloat16], l
+
+
 # ------------------------------------------- convolution layers via unfold
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("B,C,H,W,k,stride,pad,ld", [

@@ -7,9 +7,9 @@ inputs from here, so the two sides see bit-identical data.
 
 The stacks stand in for the paper's workloads (GPT-2 on E2E-length text, the
 long-sequence regime of Section 3.1, ViT-base at 224x224, GPT-2-large with its
-token embedding, and the convolutions of ResNet-18 at 224x224 behind the
-layerwise decision of Section 3.2); the datasets and pretrained weights are
-not used.  Shapes
+token embedding, the convolutions of ResNet-18 at 224x224 behind the
+layerwise decision of Section 3.2, and LoRA on GPT-2 small as in App. E.2);
+the datasets and pretrained weights are not used.  Shapes
 follow Section 2.1 (a in R^{B x T x d}, dL/ds in R^{B x T x p}) and the
 per-layer dimensions of GPT-2 small/large and ViT-base.
 
@@ -96,6 +96,13 @@ def conv_layer(cin: int, cout: int, k: int, stride: int, pad: int, hin: int) -> 
     return Layer("conv", ho * ho, d, cout, (cin, k, stride, pad, hin))
 
 
+def _lora(d: int, r: int, T: int, blocks: int) -> List[Layer]:
+    # App. E.2: each LoRA module x(W + LR) trains two sub-modules, x -> xL
+    # (d -> r) and xL -> xLR (r -> d); here on the query and value maps
+    return [Layer("linear", T, d_in, d_out) for _ in range(blocks) for _ in ("q", "v")
+            for d_in, d_out in ((d, r), (r, d))]
+
+
 def _resnet18_224() -> List[Layer]:
     L = [conv_layer(3, 64, 7, 2, 3, 224)]
     L += [conv_layer(64, 64, 3, 1, 1, 56) for _ in range(4)]
@@ -135,6 +142,10 @@ def _build() -> dict:
     w[6] = Workload(6, "resnet18-conv-stack-224-B16-bf16", 16, "bf16", tuple(_resnet18_224()),
                     "auto", gamma=0.01, sigma=1.0, g_scale=1e-2,
                     description="ResNet-18 at 224x224: 20 convolutions (unfolded) + classifier")
+    w[7] = Workload(7, "gpt2-small-lora-r16-qv-T128-B32-bf16", 32, "bf16", tuple(_lora(768, 16, 128, 12)),
+                    "auto", gamma=0.01, sigma=1.0, g_scale=1e-2,
+                    description="LoRA rank 16 on the query and value projections of 12 GPT-2-small "
+                                "blocks: 24 x (768 -> 16, 16 -> 768)")
     return w
 
 
