@@ -44,6 +44,21 @@ What is computed, and where the paper defines it
                            r -> p), whose (activation, output gradient) pairs
                            enter the path like any other layer.  The frozen W
                            and the residual x carry no trainable weight.
+* bias_sums / bias_norm_sq -- the bias b of a layer s = a W + b (the forward and
+                           back-propagation figure of Section 2): its per-sample
+                           gradient is sum_t dL_i/ds_t, instantiated (Section 5
+                           notes that book-keeping covers the weights only).
+* norm_affine_sums / norm_affine_norm_sq -- the elementwise affine parameters
+                           of LayerNorm / GroupNorm / InstanceNorm (y = gamma *
+                           xhat + beta; per-sample instantiation in the codebase
+                           notes of the appendix): dL_i/dgamma = sum_t g_t * xhat_t,
+                           dL_i/dbeta = sum_t g_t, over the tokens (or spatial
+                           positions) t.
+* logical_batch          -- gradient accumulation (footnote on physical and
+                           logical batch sizes in Section 3; appendix codebase
+                           notes): clip per physical batch, sum the clipped
+                           gradients over the physical batches, add the noise
+                           once per logical batch.
 * philox4x32_10 / noise -- Algorithm 1, Gaussian noise sigma R N(0, I).  The
                            paper does not fix a generator; the reading used
                            here is Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
@@ -71,7 +86,8 @@ __all__ = [
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
     "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
     "bk_layer_norm", "bk_stack", "per_sample_grads", "weighted_sum", "conv_out_size", "unfold",
-    "tokens_from_nchw", "lora_submodules", "adapter_submodules",
+    "tokens_from_nchw", "lora_submodules", "adapter_submodules", "bias_sums", "bias_norm_sq",
+    "norm_affine_sums", "norm_affine_norm_sq", "logical_batch", "BIAS_TENSOR",
 ]
 
 F64 = np.float64
@@ -308,6 +324,31 @@ def adapter_submodules(x, D, U, dv, act: str = "relu"):
     return [(x, du), (h, dv)]
 
 
+def bias_sums(g) -> np.ndarray:
+    """Per-sample gradient of a bias: s_i = sum_t g_it  ([B,T,p] -> [B,p])."""
+    return _f64(g).sum(axis=1)
+
+
+def bias_norm_sq(g) -> np.ndarray:
+    """||s_i||^2 of the per-sample bias gradient -> [B]."""
+    s = bias_sums(g)
+    return np.einsum("bp,bp->b", s, s)
+
+
+def norm_affine_sums(xhat, g):
+    """Per-sample gradients of y = gamma * xhat + beta over tokens t:
+    u_i = sum_t g_it * xhat_it (gamma) and s_i = sum_t g_it (beta), both [B,p]."""
+    xhat, g = _f64(xhat), _f64(g)
+    return (g * xhat).sum(axis=1), g.sum(axis=1)
+
+
+def norm_affine_norm_sq(xhat, g, beta: bool = True) -> np.ndarray:
+    """||u_i||^2 (+ ||s_i||^2 with a beta) -> [B]."""
+    u, s = norm_affine_sums(xhat, g)
+    n = np.einsum("bp,bp->b", u, u)
+    return n + np.einsum("bp,bp->b", s, s) if beta else n
+
+
 def embed_weighted_grad(ids, g, C, V: int) -> np.ndarray:
     """G[v, :] = sum_i C_i sum_{t: x_it = v} g_it  -> [V, p] (every row present)."""
     ids = _ids(ids)
@@ -422,10 +463,19 @@ def add_noise(G, std: float, seed: int, tensor_id: int, step: int) -> np.ndarray
 # Whole path (Algorithm 1 from "norms" to "noise", BK-MixGhostClip choice of
 # norm per layer from Algorithm "BKAL-mixed")
 # --------------------------------------------------------------------------
-def bk_layer_norm(layer_kind: str, x, g, V: int = 0) -> np.ndarray:
+BIAS_TENSOR = 1 << 31      # noise stream of a bias / beta: tensor id BIAS_TENSOR | layer
+
+
+def bk_layer_norm(layer_kind: str, x, g, V: int = 0, bias: bool = False) -> np.ndarray:
+    """Per-sample squared gradient norm of one layer: the weights (by their
+    definition, ghost and instantiated alike), plus its bias when it has one;
+    for a "norm" layer (affine of a normalization) gamma, plus beta with bias."""
     if layer_kind == "embed":
         return embed_norm_sq(x, g, V)
-    return linear_norm_sq(x, g)
+    if layer_kind == "norm":
+        return norm_affine_norm_sq(x, g, bias)
+    n = linear_norm_sq(x, g)
+    return n + bias_norm_sq(g) if bias else n
 
 
 def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed: int,
@@ -436,21 +486,53 @@ def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed
     gradients G_l (before noise) and, if with_noise, G_hat_l with tensor_id = l.
     mixopt: BK-MixOpt -- a linear layer that instantiates (2 T^2 >= p d) keeps
     its per-sample gradients and forms G_l as their weighted sum (App. B.5);
-    every other layer takes the book-keeping GEMM a^T diag(C) g."""
-    norms = np.stack([bk_layer_norm(L.kind, x, g, L.d) for L, (x, g) in zip(layers, inputs)])
+    every other layer takes the book-keeping GEMM a^T diag(C) g.
+    A layer with a true .bias attribute also has a bias (a "norm" layer: a
+    beta); its clipped gradient sum_i C_i s_i is returned in Gb[l] (None
+    otherwise) and noised with tensor id BIAS_TENSOR | l.  A "norm" layer's
+    G_l is its gamma gradient sum_i C_i u_i."""
+    bias = [bool(getattr(L, "bias", False)) for L in layers]
+    norms = np.stack([bk_layer_norm(L.kind, x, g, L.d, b) for L, (x, g), b in zip(layers, inputs, bias)])
     total = aggregate(norms)
     C = clip_factors(total, mode, R, gamma)
-    G, Ghat = [], []
+    G, Ghat, Gb, Gbhat = [], [], [], []
     for l, (L, (x, g)) in enumerate(zip(layers, inputs)):
         if L.kind == "embed":
             Gl = embed_weighted_grad(x, g, C, L.d)
+        elif L.kind == "norm":
+            Gl = weighted_sum(norm_affine_sums(x, g)[0], C)
         elif mixopt and not use_ghost(L.T, L.d, L.p):
             Gl = weighted_sum(per_sample_grads(x, g), C)
         else:
             Gl = weighted_grad(x, g, C)
         G.append(Gl)
+        Gbl = weighted_sum(bias_sums(g), C) if bias[l] else None
+        Gb.append(Gbl)
         if with_noise:
             Ghat.append(add_noise(Gl, std, seed, l, step))
-    return {"norms": norms, "total": total, "C": C, "G": G, "Ghat": Ghat,
-            "paths": [("embed" if L.kind == "embed" else ("ghost" if use_ghost(L.T, L.d, L.p) else "inst"))
-                      for L in layers]}
+            Gbhat.append(add_noise(Gbl, std, seed, BIAS_TENSOR | l, step) if bias[l] else None)
+    return {"norms": norms, "total": total, "C": C, "G": G, "Ghat": Ghat, "Gb": Gb, "Gbhat": Gbhat,
+            "paths": [("embed" if L.kind == "embed" else "norm" if L.kind == "norm" else
+                       ("ghost" if use_ghost(L.T, L.d, L.p) else "inst")) for L in layers]}
+
+
+def logical_batch(layers, batches, mode: str, R: float, gamma: float, std: float, seed: int,
+                  step: int = 0):
+    """Gradient accumulation: `batches` is a list of physical batches (each a
+    list of per-layer inputs as for bk_stack).  Each physical batch is clipped
+    on its own (its samples' norms and factors); the clipped gradients add up
+    over the physical batches; the noise is drawn once, for the logical batch.
+    Returns dict with per-batch C, the summed G / Gb and the noised Ghat / Gbhat."""
+    G = Gb = None
+    Cs = []
+    for inputs in batches:
+        r = bk_stack(layers, inputs, mode, R, gamma, 0.0, seed, step, with_noise=False)
+        Cs.append(r["C"])
+        if G is None:
+            G, Gb = r["G"], r["Gb"]
+        else:
+            G = [x + y for x, y in zip(G, r["G"])]
+            Gb = [None if x is None else x + y for x, y in zip(Gb, r["Gb"])]
+    Ghat = [add_noise(Gl, std, seed, l, step) for l, Gl in enumerate(G)]
+    Gbhat = [None if x is None else add_noise(x, std, seed, BIAS_TENSOR | l, step) for l, x in enumerate(Gb)]
+    return {"C": Cs, "G": G, "Gb": Gb, "Ghat": Ghat, "Gbhat": Gbhat}
