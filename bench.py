@@ -55,9 +55,22 @@ def algorithmic_work(w: wl.Workload, mixopt: bool = False):
     B = w.B
     out = {"norm_flops": 0.0, "norm_bytes": 0.0, "gemm_flops": 0.0, "gemm_bytes": 0.0,
            "noise_elems": 0.0, "prep_bytes": 0.0, "ghost_layers": 0, "inst_layers": 0,
-           "embed_layers": 0, "conv_layers": 0}
+           "embed_layers": 0, "conv_layers": 0, "affine_layers": 0, "bias_terms": 0}
     for L0 in w.layers:
         L = L0
+        if L0.bias or L0.kind == "norm":
+            # per-sample sums (App. notes on normalization layers; biases, Section 5):
+            # g (and xhat) read once, B p sums written and read back, p written
+            nin = 2 if L0.kind == "norm" else 1
+            nsum = (1 if L0.bias else 0) + (1 if L0.kind == "norm" else 0)
+            out["norm_bytes"] += B * L0.T * L0.p * es * nin + 4.0 * B * L0.p * nsum
+            out["gemm_bytes"] += (4.0 * B * L0.p + 4.0 * L0.p) * nsum
+            out["gemm_flops"] += 2.0 * B * L0.p * nsum
+            out["noise_elems"] += float(L0.p) * nsum
+            out["affine_layers"] += 1 if L0.kind == "norm" else 0
+            out["bias_terms"] += 1 if L0.bias else 0
+            if L0.kind == "norm":
+                continue
         if L0.kind == "conv":
             cin, k, stride, pad, hin = L0.conv
             out["conv_layers"] += 1
@@ -98,7 +111,7 @@ def make_inputs(w: wl.Workload, dev):
             t = (torch.empty(w.B, L.T, L.d, dtype=w.torch_dtype, device=dev),
                  torch.empty(w.B, L.T, L.p, dtype=w.torch_dtype, device=dev))
         ins.append(t)
-    Gs = [torch.empty(L.d, L.p, device=dev) for L in w.layers]
+    Gs = [torch.empty((L.p,) if L.kind == "norm" else (L.d, L.p), device=dev) for L in w.layers]
     return ins, raw, Gs
 
 
@@ -121,12 +134,20 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
         if kind == "conv":
             cin, k, stride, pad, _ = L.conv
             x, g, kind = oracle.unfold(x, k, k, stride, pad, L.d), oracle.tokens_from_nchw(g), "linear"
-        n = oracle.bk_layer_norm(kind, x, g, L.d)
+        n = oracle.bk_layer_norm(kind, x, g, L.d, L.bias)
         C = oracle.clip_factors(n, w.clip, w.R, w.gamma)
-        G = (oracle.embed_weighted_grad(x, g, C, L.d) if L.kind == "embed" else oracle.weighted_grad(x, g, C))
+        if kind == "embed":
+            G = oracle.embed_weighted_grad(x, g, C, L.d)
+        elif kind == "norm":
+            G = oracle.weighted_sum(oracle.norm_affine_sums(x, g)[0], C)
+        else:
+            G = oracle.weighted_grad(x, g, C)
         oracle.add_noise(G, w.noise_std, w.wid, l, 0)
+        if L.bias:
+            oracle.add_noise(oracle.weighted_sum(oracle.bias_sums(g), C), w.noise_std, w.wid,
+                             oracle.BIAS_TENSOR | l, 0)
         t_used += time.perf_counter() - t0
-        done += 2.0 * w.B * L.T * L.p * true_d(L)
+        done += 2.0 * w.B * L.T * L.p * true_d(L) if L.kind != "norm" else 0.0
         nl += 1
         if t_used >= budget_s:
             break
@@ -225,10 +246,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-7)")
+    ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mixopt", action="store_true",
                     help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
+    ap.add_argument("--accumulate", type=int, default=1,
+                    help="physical batches per logical batch (gradient accumulation; noise once per step)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (reference for the HBM byte counters)")
     args = ap.parse_args()
@@ -252,11 +275,22 @@ def main():
     n, B = len(w.layers), w.B
 
     ins, raw, Gs = make_inputs(w, dev)
-    keep = [args.mixopt and L.kind != "embed" and not bk.bk_use_ghost(L.T, L.d, L.p) for L in w.layers]
-    Ps = [torch.empty(B, L.d, L.p, device=dev) if k else None for L, k in zip(w.layers, keep)]
-    specs = [{"kind": bk.BK_EMBEDDING if L.kind == "embed" else bk.BK_LINEAR, "x": x, "g": g, "G": G,
-              "V": L.d, "mixopt": args.mixopt, "P": P} for L, (x, g), G, P in zip(w.layers, ins, Gs, Ps)]
-    arr = bk.make_layers(specs)
+    K = max(1, args.accumulate)
+    keep = [args.mixopt and L.kind in ("linear", "conv") and not bk.bk_use_ghost(L.T, L.d, L.p)
+            for L in w.layers]
+    Ps = [torch.empty(B, L.p, device=dev) if L.kind == "norm" else
+          (torch.empty(B, L.d, L.p, device=dev) if k else None) for L, k in zip(w.layers, keep)]
+    Gbs = [torch.empty(L.p, device=dev) if L.bias else None for L in w.layers]
+    Pbs = [torch.empty(B, L.p, device=dev) if L.bias else None for L in w.layers]
+    kinds = {"embed": bk.BK_EMBEDDING, "norm": bk.BK_NORM_AFFINE}
+
+    def layer_array(accumulate: bool):
+        return bk.make_layers([{"kind": kinds.get(L.kind, bk.BK_LINEAR), "x": x, "g": g, "G": G, "V": L.d,
+                                "mixopt": args.mixopt, "P": P, "bias": L.bias, "Gb": Gb, "Pb": Pb,
+                                "accumulate": accumulate}
+                               for L, (x, g), G, P, Gb, Pb in zip(w.layers, ins, Gs, Ps, Gbs, Pbs)])
+    arr = layer_array(False)
+    arr_acc = layer_array(True)      # physical batches 2..K of a logical batch add to G
     norm_sq = torch.empty(n, B, device=dev)
     C = torch.empty(B, device=dev)
     tot = torch.empty(B, device=dev)
@@ -266,9 +300,12 @@ def main():
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     import ctypes
-    g_ptrs = (ctypes.c_void_p * n)(*[G.data_ptr() for G in Gs])
-    g_nel = (ctypes.c_int64 * n)(*[G.numel() for G in Gs])
-    g_tid = (ctypes.c_uint32 * n)(*range(n))
+    noised = [(G, l) for l, G in enumerate(Gs)] + [(Gb, bk.BK_BIAS_TENSOR | l) for l, Gb in enumerate(Gbs)
+                                                   if Gb is not None]
+    nn_ = len(noised)
+    g_ptrs = (ctypes.c_void_p * nn_)(*[G.data_ptr() for G, _ in noised])
+    g_nel = (ctypes.c_int64 * nn_)(*[G.numel() for G, _ in noised])
+    g_tid = (ctypes.c_uint32 * nn_)(*[t for _, t in noised])
 
     convs = bk.make_convs([{"x": x, "dy": dy, "a": ins[l][0], "g": ins[l][1], "k": w.layers[l].conv[1],
                             "stride": w.layers[l].conv[2], "pad": w.layers[l].conv[3], "ld": w.layers[l].d}
@@ -279,26 +316,31 @@ def main():
             bk._check(bk.lib.bk_conv_prep(convs, len(raw), dt, B, sp), "bk_conv_prep")
 
     def step(ev=None):
-        if ev: ev[5].record(stream)
-        prep()
-        if ev: ev[0].record(stream)
-        bk._check(bk.lib.bk_layer_norms(arr, n, dt, B, norm_sq.data_ptr(), ws_n.data_ptr(),
-                                        ws_n.numel(), sp), "bk_layer_norms")
-        if ev: ev[1].record(stream)
-        bk._check(bk.lib.bk_clip_factors(norm_sq.data_ptr(), n, B, mode, w.R, w.gamma, C.data_ptr(),
-                                         tot.data_ptr(), sp), "bk_clip_factors")
-        if ev: ev[2].record(stream)
-        bk._check(bk.lib.bk_weighted_grads(arr, n, C.data_ptr(), dt, B, ws_g.data_ptr(), ws_g.numel(), sp),
-                  "bk_weighted_grads")
-        if ev: ev[3].record(stream)
-        bk._check(bk.lib.bk_add_noise_grouped(g_ptrs, g_nel, g_tid, n, w.noise_std, w.wid, 0, sp),
+        """One logical batch: K physical batches (prep, norms, clip, clipped
+        gradients added to G after the first), then the noise once."""
+        t = (lambda: ev.append(torch.cuda.Event(enable_timing=True)) or ev[-1].record(stream)) if ev is not None \
+            else (lambda: None)
+        for k in range(K):
+            t()
+            prep()
+            t()
+            bk._check(bk.lib.bk_layer_norms(arr, n, dt, B, norm_sq.data_ptr(), ws_n.data_ptr(),
+                                            ws_n.numel(), sp), "bk_layer_norms")
+            t()
+            bk._check(bk.lib.bk_clip_factors(norm_sq.data_ptr(), n, B, mode, w.R, w.gamma, C.data_ptr(),
+                                             tot.data_ptr(), sp), "bk_clip_factors")
+            t()
+            bk._check(bk.lib.bk_weighted_grads(arr_acc if k else arr, n, C.data_ptr(), dt, B, ws_g.data_ptr(),
+                                               ws_g.numel(), sp), "bk_weighted_grads")
+        t()
+        bk._check(bk.lib.bk_add_noise_grouped(g_ptrs, g_nel, g_tid, nn_, w.noise_std, w.wid, 0, sp),
                   "bk_add_noise_grouped")
-        if ev: ev[4].record(stream)
+        t()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    evs = [[] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -307,10 +349,19 @@ def main():
     elapsed = time.perf_counter() - t0
     assert torch.isfinite(C).all().item(), "non-finite clip factors"
 
-    ph = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] + [e[5].elapsed_time(e[0])]
-                   for e in evs])   # ms
-    ph_ms = ph.mean(axis=0)
+    # events: per physical batch [prep, norms, clip, grads], then noise
+    def phase_ms(e):
+        out = np.zeros(5)
+        for k in range(K):
+            b = 4 * k
+            for j, slot in enumerate((4, 0, 1, 2)):          # prep, norms, clip, grads
+                out[slot] += e[b + j].elapsed_time(e[b + j + 1])
+        out[3] = e[4 * K].elapsed_time(e[4 * K + 1])
+        return out
+    ph_ms = np.array([phase_ms(e) for e in evs]).mean(axis=0)
     work = algorithmic_work(w, args.mixopt)
+    work = {k: (v * K if k in ("norm_flops", "norm_bytes", "gemm_flops", "gemm_bytes", "prep_bytes") else v)
+            for k, v in work.items()}
     ms_step = elapsed * 1e3 / args.steps
     peak_mfma = PEAK_MFMA_TFLOPS[w.dtype]
     phases = {
@@ -357,14 +408,16 @@ def main():
         for k in list(v):
             v[k] = round(float(v[k]), 4)
     res = {
-        "metric": METRIC, "value": B / (ms_step / 1e3), "unit": "samples/s", "n_gpus": 1,
+        "metric": METRIC, "value": K * B / (ms_step / 1e3), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "variant": "BK-MixOpt" if args.mixopt else "BK",
+                   "accumulate": K, "logical_batch": K * B,
                    "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
                    "clip": w.clip, "sigma": w.sigma, "paths": {"ghost": work["ghost_layers"],
                    "inst": work["inst_layers"], "embed": work["embed_layers"],
-                   "conv": work["conv_layers"]}},
+                   "conv": work["conv_layers"], "affine": work["affine_layers"],
+                   "bias": work["bias_terms"]}},
         "roofline": roof,
         "phases": phases,
         "mfma_frac": {"ghost_norm_paper_flops": phases["norms"].get("tflops", 0) / peak_mfma,

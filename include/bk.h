@@ -73,33 +73,63 @@ typedef enum { BK_F32 = 0, BK_BF16 = 1 } bk_dtype;
  *                  is pure normalisation, and C_i = 0 when ||g_i|| = 0 there) */
 typedef enum { BK_CLIP_ABADI = 0, BK_CLIP_AUTO = 1 } bk_clip;
 
-typedef enum { BK_LINEAR = 0, BK_EMBEDDING = 1 } bk_layer_kind;
+/* BK_NORM_AFFINE: the elementwise affine y = gamma * xhat + beta of a
+ * LayerNorm / GroupNorm / InstanceNorm over p features (channels), whose
+ * per-sample gradients are instantiated (the appendix notes on the supported
+ * layers): dL_i/dgamma = sum_t g_it * xhat_it, dL_i/dbeta = sum_t g_it, t over
+ * tokens or spatial positions. */
+typedef enum { BK_LINEAR = 0, BK_EMBEDDING = 1, BK_NORM_AFFINE = 2 } bk_layer_kind;
 
 /* Layer flags (bk_layer.flags).
  *   BK_LAYER_MIXOPT: BK-MixOpt (Section 3.2; the MixOpt branch of Algorithm
  *   "BKAL-mixed").  A linear layer that instantiates its per-sample gradients
  *   for the norm (bk_use_ghost == 0) keeps them in P, and its clipped gradient
  *   is their weighted sum sum_i C_i P_i (App. B.5) instead of the GEMM
- *   a^T diag(C) g.  Ghost-norm and embedding layers ignore the flag. */
-enum { BK_LAYER_MIXOPT = 1 };
+ *   a^T diag(C) g.  Ghost-norm, embedding and affine layers ignore the flag.
+ *   BK_LAYER_BIAS: a linear layer s = a W + b with a bias (Section 5: book-
+ *   keeping covers the weights; the bias gradient sum_t g_it is instantiated
+ *   per sample), or the beta of a BK_NORM_AFFINE layer.  Its squared norm
+ *   adds to the layer's per-sample norm; bk_layer_norms keeps the per-sample
+ *   sums in Pb [B, p] and bk_weighted_grads writes sum_i C_i Pb_i to Gb [p].
+ *   Embedding layers take no bias.
+ *   BK_LAYER_ACCUMULATE: gradient accumulation over physical batches (the
+ *   paper's logical vs physical batch size): bk_weighted_grads adds this
+ *   step's clipped gradients to G (and Gb) instead of overwriting them, each
+ *   element in one fixed-order addition.  Each physical batch is clipped on
+ *   its own; the caller draws the noise once per logical batch (noise_std 0
+ *   in bk_private_grad on all but the last physical batch). */
+enum { BK_LAYER_MIXOPT = 1, BK_LAYER_BIAS = 2, BK_LAYER_ACCUMULATE = 4 };
 
-/* One generalized linear layer of a stack (used by the grouped calls).
- *   kind == BK_LINEAR   : x = a [B, T, d] of dtype dt, g [B, T, p], G [d, p]
- *   kind == BK_EMBEDDING: x = token ids int64 [B, T] (values in [0, d)),
- *                         d = vocabulary size V, g [B, T, p], G [V, p]
- * G may be NULL in calls that only compute norms.  P (device, float32
- * [B, d, p]) is used only by a BK_LAYER_MIXOPT linear layer that
+/* One layer of a stack (used by the grouped calls).
+ *   kind == BK_LINEAR     : x = a [B, T, d] of dtype dt, g [B, T, p], G [d, p]
+ *   kind == BK_EMBEDDING  : x = token ids int64 [B, T] (values in [0, d)),
+ *                           d = vocabulary size V, g [B, T, p], G [V, p]
+ *   kind == BK_NORM_AFFINE: x = xhat [B, T, p] (the normalized input, dtype
+ *                           dt), d = p, g [B, T, p], G [p] (gamma gradient),
+ *                           P [B, p] float32 (per-sample gamma gradients,
+ *                           written by bk_layer_norms, read by
+ *                           bk_weighted_grads; required)
+ * G may be NULL in calls that only compute norms.  For a linear layer P
+ * (device, float32 [B, d, p]) is used only by a BK_LAYER_MIXOPT layer that
  * instantiates: bk_layer_norms writes the per-sample gradients there and
- * bk_weighted_grads of the same step reads them; otherwise it may be NULL. */
+ * bk_weighted_grads of the same step reads them; otherwise it may be NULL.
+ * Gb [p] and Pb [B, p] (float32) are used only with BK_LAYER_BIAS.  All of
+ * P, Pb, G, Gb are caller-owned device buffers, 4-byte aligned. */
 typedef struct bk_layer {
     int32_t kind;
-    int32_t flags;           /* 0 or BK_LAYER_MIXOPT */
+    int32_t flags;           /* BK_LAYER_* bits */
     int64_t T, d, p;
     const void* x;
     const void* g;
     float* G;
     float* P;
+    float* Gb;
+    float* Pb;
 } bk_layer;
+
+/* Noise stream of the bias (or beta) gradient of layer l: tensor id
+ * BK_BIAS_TENSOR | l. */
+#define BK_BIAS_TENSOR 0x80000000u
 
 /* Operation ids for bk_workspace_size. */
 typedef enum {
@@ -278,7 +308,8 @@ bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, b
 /* The whole path of Algorithm 1 from the per-layer norms to the noise, with
  * the layerwise norm choice of Algorithm "BKAL-mixed" (BK-MixGhostClip):
  * bk_layer_norms -> bk_clip_factors -> bk_weighted_grads -> bk_add_noise_grouped
- * on every layers[l].G with tensor_id = l.  norm_sq [n,B], C [B] out, total_sq [B]
+ * on every layers[l].G with tensor_id = l and every bias / beta gradient
+ * layers[l].Gb with tensor_id = BK_BIAS_TENSOR | l.  norm_sq [n,B], C [B] out, total_sq [B]
  * out (may be NULL).  noise_std = sigma R; 0 skips the noise. */
 size_t bk_private_grad_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
                                       int64_t B);

@@ -21,7 +21,8 @@ import torch
 
 __all__ = [
     "BK_OK", "BK_ERR_INVALID_VALUE", "BK_ERR_NOT_SUPPORTED", "BK_ERR_WORKSPACE", "BK_ERR_LAUNCH",
-    "BK_F32", "BK_BF16", "BK_CLIP_ABADI", "BK_CLIP_AUTO", "BK_LINEAR", "BK_EMBEDDING", "BK_LAYER_MIXOPT",
+    "BK_F32", "BK_BF16", "BK_CLIP_ABADI", "BK_CLIP_AUTO", "BK_LINEAR", "BK_EMBEDDING", "BK_NORM_AFFINE",
+    "BK_LAYER_MIXOPT", "BK_LAYER_BIAS", "BK_LAYER_ACCUMULATE", "BK_BIAS_TENSOR",
     "BK_OP_GHOST_NORM", "BK_OP_INST_NORM", "BK_OP_EMBED_GHOST_NORM", "BK_OP_WEIGHTED_GRAD",
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
     "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
@@ -37,8 +38,9 @@ __all__ = [
 BK_OK, BK_ERR_INVALID_VALUE, BK_ERR_NOT_SUPPORTED, BK_ERR_WORKSPACE, BK_ERR_LAUNCH = range(5)
 BK_F32, BK_BF16 = 0, 1
 BK_CLIP_ABADI, BK_CLIP_AUTO = 0, 1
-BK_LINEAR, BK_EMBEDDING = 0, 1
-BK_LAYER_MIXOPT = 1
+BK_LINEAR, BK_EMBEDDING, BK_NORM_AFFINE = 0, 1, 2
+BK_LAYER_MIXOPT, BK_LAYER_BIAS, BK_LAYER_ACCUMULATE = 1, 2, 4
+BK_BIAS_TENSOR = 0x80000000
 (BK_OP_GHOST_NORM, BK_OP_INST_NORM, BK_OP_EMBED_GHOST_NORM, BK_OP_WEIGHTED_GRAD,
  BK_OP_EMBED_WEIGHTED_GRAD) = range(5)
 
@@ -65,7 +67,8 @@ class bk_layer(ctypes.Structure):
     """Mirror of ``struct bk_layer`` in include/bk.h."""
     _fields_ = [("kind", ctypes.c_int32), ("flags", ctypes.c_int32), ("T", ctypes.c_int64),
                 ("d", ctypes.c_int64), ("p", ctypes.c_int64), ("x", ctypes.c_void_p),
-                ("g", ctypes.c_void_p), ("G", ctypes.c_void_p), ("P", ctypes.c_void_p)]
+                ("g", ctypes.c_void_p), ("G", ctypes.c_void_p), ("P", ctypes.c_void_p),
+                ("Gb", ctypes.c_void_p), ("Pb", ctypes.c_void_p)]
 
 
 class bk_conv(ctypes.Structure):
@@ -410,10 +413,13 @@ def bk_philox_raw(seed: int, tensor_id: int, step: int, q0: int, nq: int, out=No
 # -------------------------------------------------------------------- grouped
 def make_layers(specs: Sequence[dict]):
     """ctypes bk_layer array from dicts {kind, x, g, G (optional), V (embedding),
-    mixopt (optional bool), P (optional float32 [B,d,p], BK-MixOpt store)}.
+    mixopt (optional bool), P (optional float32 [B,d,p], BK-MixOpt store; [B,p] gamma
+    store of an affine layer), bias (optional bool) with Gb [p] and Pb [B,p],
+    accumulate (optional bool)}.
 
-    x is a [B,T,d] for a linear layer or int64 ids [B,T] for an embedding; the
-    tensors must stay alive while the array is used."""
+    x is a [B,T,d] for a linear layer, int64 ids [B,T] for an embedding, or the
+    normalized input [B,T,p] of an affine layer; the tensors must stay alive
+    while the array is used."""
     arr = (bk_layer * max(1, len(specs)))()
     for k, s in enumerate(specs):
         x, g = _dev(s["x"], "x"), _dev(s["g"], "g")
@@ -426,7 +432,8 @@ def make_layers(specs: Sequence[dict]):
         else:
             d = x.shape[2]
         arr[k].kind = kind
-        arr[k].flags = BK_LAYER_MIXOPT if s.get("mixopt") else 0
+        arr[k].flags = ((BK_LAYER_MIXOPT if s.get("mixopt") else 0) | (BK_LAYER_BIAS if s.get("bias") else 0) |
+                        (BK_LAYER_ACCUMULATE if s.get("accumulate") else 0))
         arr[k].T = g.shape[1]
         arr[k].d = d
         arr[k].p = g.shape[2]
@@ -434,6 +441,8 @@ def make_layers(specs: Sequence[dict]):
         arr[k].g = _ptr(g)
         arr[k].G = _ptr(G)
         arr[k].P = _ptr(s.get("P"))
+        arr[k].Gb = _ptr(s.get("Gb"))
+        arr[k].Pb = _ptr(s.get("Pb"))
     return arr
 
 

@@ -129,6 +129,33 @@ __device__ __forceinline__ uint4 frag(const char* lds, int ms, int j, int lane) 
     }
 }
 
+// The 16 values of one 32x32 accumulator column n (rows r0 + acc_row(i, lane),
+// those below rmax) into out[m sm + n sn], times `scale`; with `add` they are
+// added to what out holds, the 16 old values being loaded before any store so
+// that the loads overlap (gradient accumulation).
+__device__ __forceinline__ void put_col16(float* out, size_t sm, size_t sn, int r0, int rmax, int n, int lane,
+                                          const f32x16_t& v, float scale, bool add) {
+    if (add) {
+        float o[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int m = r0 + acc_row(i, lane);
+            o[i] = m < rmax ? out[(size_t)m * sm + (size_t)n * sn] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int m = r0 + acc_row(i, lane);
+            if (m < rmax) out[(size_t)m * sm + (size_t)n * sn] = o[i] + v[i] * scale;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int m = r0 + acc_row(i, lane);
+            if (m < rmax) out[(size_t)m * sm + (size_t)n * sn] = v[i] * scale;
+        }
+    }
+}
+
 template <typename T, bool INST, bool VEC>
 __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
     using Cfg = GemmCfg<T>;
@@ -233,17 +260,13 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
         }
     } else {
         float* G = L.G;
+        const bool add = L.accum != 0;
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int n = n0 + (2 * wn + y) * 32 + (lane & 31);
-                if (n >= p) continue;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int m = m0 + (2 * wm + x) * 32 + acc_row(i, lane);
-                    if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
-                }
+                if (n < p) put_col16(G, (size_t)p, 1, m0 + (2 * wm + x) * 32, d, n, lane, acc[x][y], 1.f, add);
             }
     }
 }
@@ -485,17 +508,13 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
         }
     } else {
         float* G = L.G;
+        const bool add = L.accum != 0;
 #pragma unroll
         for (int x = 0; x < 4; ++x)
 #pragma unroll
             for (int y = 0; y < 2; ++y) {
                 const int n = n0 + 64 * wn + 32 * y + (lane & 31);
-                if (n >= p) continue;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
-                    if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
-                }
+                if (n < p) put_col16(G, (size_t)p, 1, m0 + 128 * wm + 32 * x, d, n, lane, acc[x][y], 1.f, add);
             }
     }
 }
@@ -687,17 +706,14 @@ __global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, in
         if (tid == 0) args.part[(size_t)L.part_off + (size_t)sample * tiles + tile] = tot;
     }
     if (out) {
+        const bool add = !INST && L.accum != 0;
+        const size_t sm = sw ? 1 : (size_t)p, sn = sw ? (size_t)p : 1;
 #pragma unroll
         for (int x = 0; x < 2; ++x)
 #pragma unroll
             for (int y = 0; y < NY; ++y) {
                 const int n = n0 + 32 * y + (lane & 31);
-                if (n >= Nd) continue;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int m = m0 + r0 + 32 * x + acc_row(i, lane);
-                    if (m < Md) out[sw ? (size_t)n * p + m : (size_t)m * p + n] = acc[x][y][i];
-                }
+                if (n < Nd) put_col16(out, sm, sn, m0 + r0 + 32 * x, Md, n, lane, acc[x][y], 1.f, add);
             }
     }
 }
@@ -909,17 +925,13 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
         return;
     }
     float* G = L.G;
+    const bool add = L.accum != 0;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) {
             const int n = n0 + 64 * wn + 32 * y + (lane & 31);
-            if (n >= p) continue;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
-                if (m < d) G[(size_t)m * p + n] = acc[x][y][i];
-            }
+            if (n < p) put_col16(G, (size_t)p, 1, m0 + 128 * wm + 32 * x, d, n, lane, acc[x][y], 1.f, add);
         }
 }
 
@@ -1201,17 +1213,13 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         return;
     }
     float* G = L.G;
+    const bool add = L.accum != 0;
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) {
             const int n = n0 + 64 * wn + 32 * y + (lane & 31);
-            if (n >= p) continue;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int m = m0 + 128 * wm + 32 * x + acc_row(i, lane);
-                if (m < d) G[(size_t)m * p + n] = acc[x][y][i] * c_last;
-            }
+            if (n < p) put_col16(G, (size_t)p, 1, m0 + 128 * wm + 32 * x, d, n, lane, acc[x][y], c_last, add);
         }
 }
 
@@ -1260,9 +1268,13 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
         if (threadIdx.x == 0) args.part[(size_t)L.part_off + (size_t)tg * CH + ch] = tot;
     }
     if (out && row_ok) {
+        const bool add = !INST && L.accum != 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            if (n + j < Nd) out[sw ? (size_t)(n + j) * L.p + m : (size_t)m * L.p + n + j] = r[j];
+            if (n + j < Nd) {
+                float* q = out + (sw ? (size_t)(n + j) * L.p + m : (size_t)m * L.p + n + j);
+                *q = add ? *q + r[j] : r[j];
+            }
     }
 }
 

@@ -45,7 +45,7 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 size_t elem_bytes(bk_dtype dt) { return dt == BK_BF16 ? 2 : 4; }
 
-enum class Path { Ghost, Inst, Embed };
+enum class Path { Ghost, Inst, Embed, Affine };   // Affine: no weight term (BK_NORM_AFFINE)
 
 // Everything the kernels index with 32-bit integers stays below 2^31.
 bk_status check_dims(const char* fn, int64_t B, int64_t T, int64_t d, int64_t p) {
@@ -79,6 +79,7 @@ struct NormPlan {
     int64_t tiles = 0;  // instantiation: output tiles per sample
     int64_t ksplit = 1; // instantiation: K slices per tile (wide and narrow kernels)
     int64_t tile_elems = 0;   // instantiation: floats of one K-split partial tile
+    int64_t aff_chunks = 0;   // per-sample partials of the bias / affine sums (second run)
 };
 
 // Variants whose kernels can split a tile's contraction into K slices.
@@ -113,7 +114,10 @@ int64_t narrow_grad_ksplit(int64_t tiles, int64_t nst) {
 
 void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
     const size_t es = elem_bytes(dt);
-    if (np.path == Path::Inst) {
+    if (np.path == Path::Affine) {
+        np.npart = 0;
+        np.var = 0;
+    } else if (np.path == Path::Inst) {
         const auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
         const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
         np.var = (int)v;
@@ -140,10 +144,12 @@ void finish_norm_plan(NormPlan& np, const bk_layer& L, int64_t B) {
         if (np.ksplit > 1) np.npart = np.tiles * (np.tile_elems / bk::kSplitRedWG);
     }
     np.nwg = np.path == Path::Inst ? B * np.tiles * np.ksplit : B * np.npart;
+    const bool affine = L.kind == BK_NORM_AFFINE || (L.kind == BK_LINEAR && (L.flags & BK_LAYER_BIAS));
+    np.aff_chunks = affine ? cdiv(L.p, bk::kAffineCols) : 0;
 }
 
 // Partial sums of a layer's norm (floats) and its K-split partial tiles (floats).
-size_t norm_part_floats(const NormPlan& np, int64_t B) { return (size_t)(B * np.npart); }
+size_t norm_part_floats(const NormPlan& np, int64_t B) { return (size_t)(B * (np.npart + np.aff_chunks)); }
 size_t norm_tile_floats(const NormPlan& np, int64_t B) {
     return np.ksplit > 1 ? (size_t)(B * np.tiles * np.ksplit * np.tile_elems) : 0;
 }
@@ -155,6 +161,8 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
     if (L.kind == BK_EMBEDDING) {
         np.path = Path::Embed;
+    } else if (L.kind == BK_NORM_AFFINE) {
+        np.path = Path::Affine;
     } else {
         np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
     }
@@ -172,13 +180,31 @@ bool keeps_grads(const bk_layer& L) {
     return L.kind == BK_LINEAR && (L.flags & BK_LAYER_MIXOPT) && bk_use_ghost(L.T, L.d, L.p) != 1;
 }
 
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
 bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, bool need_G) {
-    if (L.kind != BK_LINEAR && L.kind != BK_EMBEDDING)
+    if (L.kind != BK_LINEAR && L.kind != BK_EMBEDDING && L.kind != BK_NORM_AFFINE)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld has unknown kind %d", fn, (long long)l, L.kind);
-    if ((L.flags & ~BK_LAYER_MIXOPT) != 0)
+    if ((L.flags & ~(BK_LAYER_MIXOPT | BK_LAYER_BIAS | BK_LAYER_ACCUMULATE)) != 0)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: unknown flags 0x%x", fn, (long long)l, L.flags);
     bk_status s = check_dims(fn, B, L.T, L.d, L.p);
     if (s != BK_OK) return s;
+    const bool bias = (L.flags & BK_LAYER_BIAS) != 0;
+    if (bias && L.kind == BK_EMBEDDING)
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: an embedding takes no bias", fn, (long long)l);
+    if (L.kind == BK_NORM_AFFINE) {
+        if (L.d != L.p)
+            return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: affine layer needs d == p", fn, (long long)l);
+        if (B * L.p > 0 && (!L.P || !aligned4(L.P)))
+            return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: affine layer needs P [B,p] (4-byte aligned)", fn,
+                        (long long)l);
+    }
+    if (bias && B * L.p > 0 && (!L.Pb || !aligned4(L.Pb)))
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: BK_LAYER_BIAS needs Pb [B,p] (4-byte aligned)", fn,
+                    (long long)l);
+    if (bias && need_G && L.p > 0 && (!L.Gb || !aligned4(L.Gb)))
+        return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: BK_LAYER_BIAS needs Gb [p] (4-byte aligned)", fn,
+                    (long long)l);
     if (keeps_grads(L) && B * L.d * L.p > 0) {
         if (!L.P)
             return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: BK_LAYER_MIXOPT needs P [B,d,p]", fn,
@@ -327,6 +353,44 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             if (st != BK_OK) return st;
         }
 
+    // Per-sample bias / affine sums of the layers that have them (their
+    // partials follow the layer's weight partials).
+    {
+        bk::AffineArgs a{};
+        a.B = (int32_t)B;
+        a.part = part;
+        int64_t wg = 0;
+        auto flush = [&]() -> bk_status {
+            if (a.n == 0) return BK_OK;
+            if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+            hipError_t e = bk::launch_affine(a, (int)wg, bf16, s);
+            a.n = 0;
+            wg = 0;
+            return e == hipSuccess ? BK_OK : hip_fail(e, "bias / affine sums launch");
+        };
+        for (const Item& it : items) {
+            if (it.np.aff_chunks == 0) continue;
+            const bk_layer& L = layers[it.l];
+            const bool affine = L.kind == BK_NORM_AFFINE;
+            const size_t es = elem_bytes(dt);
+            bk::AffineLayer& f = a.L[a.n++];
+            f.x = affine ? L.x : nullptr;
+            f.g = L.g;
+            f.P = affine ? L.P : nullptr;
+            f.Pb = (L.flags & BK_LAYER_BIAS) ? L.Pb : nullptr;
+            f.T = (int32_t)L.T;
+            f.p = (int32_t)L.p;
+            f.chunks = (int32_t)it.np.aff_chunks;
+            f.wg_begin = (int32_t)wg;
+            f.part_off = (int32_t)(it.part_off + B * it.np.npart);
+            f.vec = (aligned16(L.g) && (!affine || aligned16(L.x)) && (L.p * (int64_t)es) % 16 == 0 &&
+                     L.p % 8 == 0) ? 1 : 0;
+            wg += B * it.np.aff_chunks;
+            if (a.n == bk::kMaxAffine && (st = flush()) != BK_OK) return st;
+        }
+        if ((st = flush()) != BK_OK) return st;
+    }
+
     // Finish every layer's norms with the fixed-order reduction.
     for (int64_t l0 = 0; l0 < n; l0 += bk::kMaxReduce) {
         const int64_t cnt = std::min<int64_t>(bk::kMaxReduce, n - l0);
@@ -339,6 +403,8 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             r.L[k].out = norm_sq + (l0 + k) * B;
             r.L[k].part_off = (int32_t)it.part_off;
             r.L[k].npart = (int32_t)it.np.npart;
+            r.L[k].part_off2 = (int32_t)(it.part_off + B * it.np.npart);
+            r.L[k].npart2 = (int32_t)it.np.aff_chunks;
         }
         hipError_t e = bk::launch_reduce(r, (int)(cnt * B), s);
         if (e != hipSuccess) return hip_fail(e, "norm reduction launch");
@@ -385,13 +451,14 @@ size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t
 }
 
 // Appends one weighted-sum job (P [B, n] -> G [n]) to a grouped launch.
-bk_status add_wsum_layer(bk::WsumArgs& w, int64_t& wg, const float* P, float* G, int64_t n) {
+bk_status add_wsum_layer(bk::WsumArgs& w, int64_t& wg, const float* P, float* G, int64_t n, bool accum) {
     bk::WsumLayer& L = w.L[w.n++];
     L.P = P;
     L.G = G;
     L.n = n;
     L.wg_begin = (uint32_t)wg;
     L.vec = (aligned16(P) && aligned16(G) && n % 4 == 0) ? 1u : 0u;
+    L.accum = accum ? 1u : 0u;
     wg += cdiv(n, bk::kWsumPerWG);
     return BK_OK;
 }
@@ -452,6 +519,7 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.part_off = 0;
             g.ksplit = (int32_t)gp.ksplit;
             g.swap = gp.swap ? 1 : 0;
+            g.accum = (L.flags & BK_LAYER_ACCUMULATE) ? 1 : 0;
             g.ptile_off = ptile;
             g.red_begin = (int32_t)red;
             wg += gp.tm * gp.tn * gp.ksplit;
@@ -463,7 +531,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         }
         if ((st = flush()) != BK_OK) return st;
     }
-    // BK-MixOpt layers: weighted sums of their stored per-sample gradients.
+    // Weighted sums of stored per-sample gradients: BK-MixOpt weights, the
+    // gammas of affine layers, and every bias / beta.
     {
         bk::WsumArgs w{};
         w.B = (int32_t)B;
@@ -479,9 +548,16 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         };
         for (int64_t l = 0; l < n; ++l) {
             const bk_layer& L = layers[l];
-            if (!keeps_grads(L) || L.d * L.p == 0) continue;
-            if ((st = add_wsum_layer(w, wg, L.P, L.G, L.d * L.p)) != BK_OK) return st;
-            if (w.n == bk::kMaxWsum && (st = flush()) != BK_OK) return st;
+            const bool acc = (L.flags & BK_LAYER_ACCUMULATE) != 0;
+            if ((keeps_grads(L) || L.kind == BK_NORM_AFFINE) && L.d * L.p > 0) {
+                const int64_t ne = L.kind == BK_NORM_AFFINE ? L.p : L.d * L.p;
+                if ((st = add_wsum_layer(w, wg, L.P, L.G, ne, acc)) != BK_OK) return st;
+                if (w.n == bk::kMaxWsum && (st = flush()) != BK_OK) return st;
+            }
+            if ((L.flags & BK_LAYER_BIAS) && L.p > 0) {
+                if ((st = add_wsum_layer(w, wg, L.Pb, L.Gb, L.p, acc)) != BK_OK) return st;
+                if (w.n == bk::kMaxWsum && (st = flush()) != BK_OK) return st;
+            }
         }
         if ((st = flush()) != BK_OK) return st;
     }
@@ -492,7 +568,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
         uint64_t* keys = reinterpret_cast<uint64_t*>(w);
         int32_t* first = reinterpret_cast<int32_t*>(w + align_up((size_t)(B * L.T) * sizeof(uint64_t)));
         hipError_t e = bk::launch_embed_grad(static_cast<const int64_t*>(L.x), L.g, C, bf16, B, L.T,
-                                             L.p, L.d, L.G, keys, first, s);
+                                             L.p, L.d, L.G, keys, first,
+                                             (L.flags & BK_LAYER_ACCUMULATE) != 0, s);
         if (e != hipSuccess) return hip_fail(e, "embedding gradient launch");
     }
     return BK_OK;
@@ -720,7 +797,7 @@ bk_status bk_weighted_sum(const float* P, const float* C, int64_t B, int64_t n, 
     w.B = (int32_t)B;
     w.C = C;
     int64_t wg = 0;
-    add_wsum_layer(w, wg, P, G, n);
+    add_wsum_layer(w, wg, P, G, n, false);
     hipError_t e = bk::launch_wsum(w, (int)wg, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? BK_OK : hip_fail(e, "weighted sum launch");
 }
@@ -937,7 +1014,8 @@ bk_status bk_private_grad(const bk_layer* layers, int64_t n, bk_dtype dt, int64_
     for (int64_t l = 0; l < n; ++l)
         if ((st = check_layer(fn, layers[l], l, B, true)) != BK_OK) return st;
     if (B > 0 && !C) return fail(BK_ERR_INVALID_VALUE, "%s: NULL clip factor output", fn);
-    if (n > UINT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many layers", fn);
+    // tensor ids l and BK_BIAS_TENSOR | l must not collide
+    if (n > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: too many layers", fn);
     const size_t need = bk_private_grad_workspace_size(layers, n, dt, B);
     if (ws_bytes < need || (need > 0 && !ws))
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
@@ -947,15 +1025,21 @@ bk_status bk_private_grad(const bk_layer* layers, int64_t n, bk_dtype dt, int64_
     if (e != hipSuccess) return hip_fail(e, "clip launch");
     if ((st = weighted_grads(fn, layers, n, C, dt, B, ws, ws_bytes, s)) != BK_OK) return st;
     if (noise_std == 0.f) return BK_OK;
-    std::vector<float*> G((size_t)n);
-    std::vector<int64_t> nel((size_t)n);
-    std::vector<uint32_t> tid((size_t)n);
+    std::vector<float*> G;
+    std::vector<int64_t> nel;
+    std::vector<uint32_t> tid;
     for (int64_t l = 0; l < n; ++l) {
-        G[(size_t)l] = layers[l].G;
-        nel[(size_t)l] = layers[l].d * layers[l].p;
-        tid[(size_t)l] = (uint32_t)l;
+        const bk_layer& L = layers[l];
+        G.push_back(L.G);
+        nel.push_back(L.kind == BK_NORM_AFFINE ? L.p : L.d * L.p);
+        tid.push_back((uint32_t)l);
+        if (L.flags & BK_LAYER_BIAS) {        // bias / beta: its own noise stream
+            G.push_back(L.Gb);
+            nel.push_back(L.p);
+            tid.push_back(BK_BIAS_TENSOR | (uint32_t)l);
+        }
     }
-    return add_noise_layers(fn, G.data(), nel.data(), tid.data(), n, noise_std, seed, step, s);
+    return add_noise_layers(fn, G.data(), nel.data(), tid.data(), (int64_t)G.size(), noise_std, seed, step, s);
 }
 
 const char* bk_status_string(bk_status s) {

@@ -52,6 +52,7 @@ struct GemmLayer {
     int32_t ksplit;     // 1: no split
     int32_t red_begin;
     int32_t swap;       // narrow kernels: the tile is G^T (rows along p, d < p)
+    int32_t accum;      // clipped gradient: add to G instead of writing it
     int64_t ptile_off;  // first float of this layer's partial tiles
 };
 constexpr int kMaxGemm = 48;
@@ -69,6 +70,8 @@ struct ReduceLayer {
     float* out;         // [B]
     int32_t part_off;
     int32_t npart;      // partials per sample
+    int32_t part_off2;  // a second run (bias / affine sums), added after the first
+    int32_t npart2;
 };
 constexpr int kMaxReduce = 200;
 struct ReduceArgs {
@@ -131,6 +134,8 @@ struct WsumLayer {
     int64_t n;
     uint32_t wg_begin;
     uint32_t vec;       // P, G 16-byte aligned and 4 | n
+    uint32_t accum;     // add to G instead of writing it
+    uint32_t pad;
 };
 constexpr int kMaxWsum = 100;
 struct WsumArgs {
@@ -202,6 +207,31 @@ hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_
                              uint32_t* out, hipStream_t s);
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
                              int64_t B, int64_t T, int64_t p, int64_t V, float* G,
-                             uint64_t* keys, int32_t* first, hipStream_t s);
+                             uint64_t* keys, int32_t* first, bool accum, hipStream_t s);
+
+// ---- per-sample bias and normalization-affine sums ---------------------------
+// For each sample i and feature c: s_i[c] = sum_t g[i,t,c] (a bias or a beta)
+// and, with x set, u_i[c] = sum_t g[i,t,c] x[i,t,c] (a gamma).  One workgroup
+// per (layer, sample, chunk of kAffineCols features) writes the sums and one
+// partial of the squared norm, sum_c u^2 + s^2, at part[part_off + i chunks + k].
+constexpr int kAffineCols = 256;
+struct AffineLayer {
+    const void* x;      // xhat [B,T,p] (gamma terms), or nullptr
+    const void* g;      // [B,T,p]
+    float* P;           // [B,p] gamma sums (with x)
+    float* Pb;          // [B,p] bias / beta sums, or nullptr
+    int32_t T, p;
+    int32_t chunks;     // ceil(p / kAffineCols)
+    int32_t wg_begin;
+    int32_t part_off;
+    int32_t vec;        // x and g rows 16-byte aligned, 8 | p
+};
+constexpr int kMaxAffine = 64;
+struct AffineArgs {
+    int32_t n, B;
+    float* part;
+    AffineLayer L[kMaxAffine];
+};
+hipError_t launch_affine(const AffineArgs& args, int n_wg, bool bf16, hipStream_t s);
 
 }  // namespace bk

@@ -16,6 +16,8 @@ __global__ __launch_bounds__(256) void reduce_kernel(const ReduceArgs args) {
     const float* p = args.part + L.part_off + (int64_t)i * L.npart;
     double s = 0.0;
     for (int k = 0; k < L.npart; ++k) s += (double)p[k];
+    const float* p2 = args.part + L.part_off2 + (int64_t)i * L.npart2;
+    for (int k = 0; k < L.npart2; ++k) s += (double)p2[k];
     L.out[i] = (float)s;
 }
 

@@ -62,12 +62,13 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(const uint64_t* __restr
                                                          const int32_t* __restrict__ first, int n,
                                                          const T* __restrict__ g,
                                                          const float* __restrict__ C, int T_, int p,
-                                                         float* __restrict__ G) {
+                                                         float* __restrict__ G, int accum) {
     const int64_t v = blockIdx.x;
     float* row = G + v * (int64_t)p;
     const int s0 = first[v];
-    if (s0 < 0) {
-        for (int c = threadIdx.x; c < p; c += 256) row[c] = 0.f;
+    if (s0 < 0) {                          // absent id: zero row (kept as it is when accumulating)
+        if (!accum)
+            for (int c = threadIdx.x; c < p; c += 256) row[c] = 0.f;
         return;
     }
     for (int c0 = 0; c0 < p; c0 += 256) {
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(const uint64_t* __restr
             const float w = C[r / (uint32_t)T_];
             if (c < p) acc += w * load_elem<T>(g + (int64_t)r * p + c);
         }
-        if (c < p) row[c] = acc;
+        if (c < p) row[c] = accum ? row[c] + acc : acc;
     }
 }
 
@@ -88,7 +89,7 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(const uint64_t* __restr
 
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
                              int64_t B, int64_t T, int64_t p, int64_t V, float* G, uint64_t* keys,
-                             int32_t* first, hipStream_t s) {
+                             int32_t* first, bool accum, hipStream_t s) {
     const int n = (int)(B * T);
     if (n > kSortMax) return hipErrorInvalidValue;
     int P = 1;
@@ -99,10 +100,10 @@ hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, 
     if (V <= 0) return hipSuccess;
     if (bf16)
         hipLaunchKernelGGL(embed_rows_kernel<bf16_t>, dim3((unsigned)V), dim3(256), 0, s, keys, first, n,
-                           reinterpret_cast<const bf16_t*>(g), C, (int)(T > 0 ? T : 1), (int)p, G);
+                           reinterpret_cast<const bf16_t*>(g), C, (int)(T > 0 ? T : 1), (int)p, G, accum ? 1 : 0);
     else
         hipLaunchKernelGGL(embed_rows_kernel<float>, dim3((unsigned)V), dim3(256), 0, s, keys, first, n,
-                           reinterpret_cast<const float*>(g), C, (int)(T > 0 ? T : 1), (int)p, G);
+                           reinterpret_cast<const float*>(g), C, (int)(T > 0 ? T : 1), (int)p, G, accum ? 1 : 0);
     return hipGetLastError();
 }
 

@@ -1,7 +1,7 @@
 // Weighted sum of stored per-sample gradients (App. B.5), BK-MixOpt's
 // clipped gradient on the layers that instantiate:
 //   G[e] = sum_i C[i] P[i n + e],  i ascending, one float32 fused
-// multiply-add per sample (deterministic).
+// multiply-add per sample (deterministic); with accum the sum is added to G.
 // One launch covers a group of layers; each thread owns 4 consecutive
 // elements (16-byte loads when the layer's buffers allow) and streams the B
 // per-sample values of them.  HBM-bound: (B + 1) * 4 bytes per element.
@@ -30,7 +30,15 @@ __global__ __launch_bounds__(256) void wsum_kernel(const WsumArgs args) {
             acc.z = fmaf(c, v.z, acc.z);
             acc.w = fmaf(c, v.w, acc.w);
         }
-        *reinterpret_cast<float4*>(L.G + e0) = acc;
+        float4* q = reinterpret_cast<float4*>(L.G + e0);
+        if (L.accum) {
+            const float4 o = *q;
+            acc.x += o.x;
+            acc.y += o.y;
+            acc.z += o.z;
+            acc.w += o.w;
+        }
+        *q = acc;
     } else {
         const int m = (int)min<int64_t>(4, n - e0);
         float acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -43,7 +51,7 @@ __global__ __launch_bounds__(256) void wsum_kernel(const WsumArgs args) {
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            if (j < m) L.G[e0 + j] = acc[j];
+            if (j < m) L.G[e0 + j] = L.accum ? L.G[e0 + j] + acc[j] : acc[j];
     }
 }
 

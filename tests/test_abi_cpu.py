@@ -121,7 +121,7 @@ def test_grouped_validation():
     for k in range(2):
         arr[k].kind, arr[k].T, arr[k].d, arr[k].p = bk.BK_LINEAR, 8, 16, 16
         arr[k].x = arr[k].g = arr[k].G = 0x10000
-    arr[1].flags = 2                                        # not a known flag
+    arr[1].flags = 8                                        # not a known flag
     st = bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
     assert st == bk.BK_ERR_INVALID_VALUE and "flags" in bk.bk_last_error()
     arr[1].flags = 0
@@ -210,3 +210,35 @@ def test_grouped_conv_prep_validation():
     two = (bk.bk_conv * 2)(mk()[0], mk(ld=1)[0])
     assert L.bk_conv_prep(two, 2, bk.BK_BF16, 2, None) == bk.BK_ERR_INVALID_VALUE
     assert b"layer 1" in L.bk_last_error()
+
+
+def test_bias_affine_accumulate_validation():
+    """BK_LAYER_BIAS needs Pb (and Gb for gradients), an affine layer needs
+    d == p and P, an embedding takes no bias; BK_LAYER_ACCUMULATE needs nothing."""
+    def one(**kw):
+        arr = (bk.bk_layer * 1)()
+        arr[0].kind, arr[0].T, arr[0].d, arr[0].p = kw.get("kind", bk.BK_LINEAR), 8, kw.get("d", 16), 16
+        arr[0].x = arr[0].g = arr[0].G = 0x10000
+        arr[0].flags = kw.get("flags", 0)
+        for f in ("P", "Gb", "Pb"):
+            setattr(arr[0], f, kw.get(f))
+        return arr
+    norms = lambda a: bk.lib.bk_layer_norms(a, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    grads = lambda a: bk.lib.bk_weighted_grads(a, 1, FAKE, bk.BK_BF16, 4, FAKE, 1 << 20, None)
+    assert norms(one(flags=bk.BK_LAYER_BIAS)) == bk.BK_ERR_INVALID_VALUE and "Pb" in bk.bk_last_error()
+    assert grads(one(flags=bk.BK_LAYER_BIAS, Pb=0x10000)) == bk.BK_ERR_INVALID_VALUE and "Gb" in bk.bk_last_error()
+    assert norms(one(flags=bk.BK_LAYER_BIAS, Pb=0x10001)) == bk.BK_ERR_INVALID_VALUE       # misaligned
+    assert norms(one(kind=bk.BK_EMBEDDING, flags=bk.BK_LAYER_BIAS, Pb=0x10000, Gb=0x10000)) == \
+        bk.BK_ERR_INVALID_VALUE and "no bias" in bk.bk_last_error()
+    assert norms(one(kind=bk.BK_NORM_AFFINE, d=12, P=0x10000)) == bk.BK_ERR_INVALID_VALUE and \
+        "d == p" in bk.bk_last_error()
+    assert norms(one(kind=bk.BK_NORM_AFFINE)) == bk.BK_ERR_INVALID_VALUE and "P [B,p]" in bk.bk_last_error()
+    assert norms(one(kind=7)) == bk.BK_ERR_INVALID_VALUE
+    # workspace grows by one partial per sample and 256-feature chunk for the bias sums
+    plain = bk.bk_layer_norms_workspace_size(one(), 1, bk.BK_BF16, 4)
+    biased = bk.bk_layer_norms_workspace_size(one(flags=bk.BK_LAYER_BIAS, Pb=0x10000), 1, bk.BK_BF16, 4)
+    assert biased >= plain + 4 * 4 - 256
+    assert bk.bk_layer_norms_workspace_size(one(kind=bk.BK_NORM_AFFINE, P=0x10000), 1, bk.BK_BF16, 4) >= 16
+    # no samples: nothing to check beyond the flags, nothing launched
+    assert bk.lib.bk_layer_norms(one(flags=bk.BK_LAYER_BIAS | bk.BK_LAYER_ACCUMULATE), 1, bk.BK_BF16, 0,
+                                 None, None, 0, None) == bk.BK_OK

@@ -193,3 +193,57 @@ def test_conv_stack_full_sampled_parity(bk):
         assert err <= GRAD_TOL, l
     del raw, ins, G0
     torch.cuda.empty_cache()
+
+
+def test_gpt2_bias_layernorm_full_sampled(bk):
+    """GPT-2 small with every bias and LayerNorm affine (73 layers, B = 32,
+    T = 128), one bk_private_grad call as bench.py runs it: sampled layer
+    norms, gamma / beta / bias gradients against the oracle; and accumulation
+    of two identical physical batches, which must give exactly twice the
+    single-batch clipped gradients (each pass is deterministic)."""
+    w = wl.get(8)
+    n, B = len(w.layers), w.B
+    print(f"workload 8: {w.name}, {n} layers, B={B}", flush=True)
+    ins = [wl.draw_layer(w, l, device=DEV) for l in range(n)]
+    kinds = {"norm": bk.BK_NORM_AFFINE}
+    Gs = [torch.empty((L.p,) if L.kind == "norm" else (L.d, L.p), device=DEV) for L in w.layers]
+    Gbs = [torch.empty(L.p, device=DEV) for L in w.layers]
+    Ps = [torch.empty(B, L.p, device=DEV) if L.kind == "norm" else None for L in w.layers]
+    Pbs = [torch.empty(B, L.p, device=DEV) for L in w.layers]
+    mk = lambda acc: bk.make_layers([{"kind": kinds.get(L.kind, bk.BK_LINEAR), "x": x, "g": g, "G": G, "P": P,
+                                      "bias": True, "Gb": Gb, "Pb": Pb, "accumulate": acc}
+                                     for L, (x, g), G, P, Gb, Pb in zip(w.layers, ins, Gs, Ps, Gbs, Pbs)])
+    norm_sq, C = torch.empty(n, B, device=DEV), torch.empty(B, device=DEV)
+    bk.bk_private_grad(mk(False), n, bk.BK_BF16, B, bk.BK_CLIP_AUTO, w.R, w.gamma, 0.0, 8, 0, norm_sq, C, None)
+    torch.cuda.synchronize()
+    G1 = [G.clone() for G in Gs]
+    Gb1 = [G.clone() for G in Gbs]
+    norms, Cc = norm_sq.cpu().numpy().astype(np.float64), C.cpu().numpy()
+    ref_C = oracle.clip_factors(oracle.aggregate(norms), w.clip, w.R, w.gamma)
+    assert np.max(np.abs(Cc - ref_C) / ref_C) <= 1e-5
+    for l in (0, 1, 2, 5, n - 1):                    # ln_1, qkv, attn out, mlp down, final ln
+        L = w.layers[l]
+        x, g = (t.cpu() for t in ins[l])
+        ref_n = oracle.bk_layer_norm(L.kind, x, g, L.d, True)
+        rel = np.max(np.abs(norms[l] - ref_n) / ref_n)
+        print(f"  layer {l} ({L.kind} {L.d}x{L.p}): norm rel err {rel:.2e}", flush=True)
+        assert rel <= NORM_TOL, l
+        if L.kind == "norm":
+            ref_G = oracle.weighted_sum(oracle.norm_affine_sums(x, g)[0], Cc)
+            got = G1[l].cpu().numpy()
+        else:
+            rows = np.sort(np.random.default_rng(l).choice(L.d, 32, replace=False))
+            cols = np.sort(np.random.default_rng(l + 1).choice(L.p, 32, replace=False))
+            ref_G = oracle.weighted_grad(x[:, :, torch.from_numpy(rows)], g[:, :, torch.from_numpy(cols)], Cc)
+            got = G1[l].cpu().numpy()[rows][:, cols]
+        ref_b = oracle.weighted_sum(oracle.bias_sums(g), Cc)
+        assert np.linalg.norm(got - ref_G) / np.linalg.norm(ref_G) <= GRAD_TOL, l
+        assert np.linalg.norm(Gb1[l].cpu().numpy() - ref_b) / np.linalg.norm(ref_b) <= GRAD_TOL, l
+    # a second, identical physical batch accumulated onto the first
+    bk.bk_private_grad(mk(True), n, bk.BK_BF16, B, bk.BK_CLIP_AUTO, w.R, w.gamma, 0.0, 8, 0, norm_sq, C, None)
+    torch.cuda.synchronize()
+    for l in range(n):
+        assert torch.equal(Gs[l], 2 * G1[l]), l
+        assert torch.equal(Gbs[l], 2 * Gb1[l]), l
+    del ins, Gs, Gbs, G1, Gb1
+    torch.cuda.empty_cache()

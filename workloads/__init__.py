@@ -24,7 +24,9 @@ Recipe (stated once, used everywhere):
   * a convolution layer draws its input x [B, C_in, H, H] (k = 0) and its
     output gradient [B, C_out, Ho, Ho] (k = 1) in the same way (NCHW); its
     linear-layer view has T = Ho*Ho, d = C_in*k*k rounded up to a multiple of
-    8 (zero columns), p = C_out.
+    8 (zero columns), p = C_out;
+  * a LayerNorm affine layer draws its normalized input xhat [B, T, p] (k = 0)
+    and output gradient (k = 1) like a linear layer with d = p.
 """
 from __future__ import annotations
 
@@ -45,11 +47,12 @@ class Layer:
     kind == "embed": a is the one-hot encoding of token ids over a vocabulary of
     size V == d, so only ids and g are stored.
     """
-    kind: str          # "linear" | "embed" | "conv"
+    kind: str          # "linear" | "embed" | "conv" | "norm" (affine of a LayerNorm, d = p)
     T: int
     d: int
     p: int
     conv: tuple = ()   # kind == "conv": (C_in, k, stride, pad, H_in)
+    bias: bool = False # a bias (linear / conv) or a beta (norm)
 
     @property
     def V(self) -> int:
@@ -94,6 +97,14 @@ def conv_layer(cin: int, cout: int, k: int, stride: int, pad: int, hin: int) -> 
     ho = (hin + 2 * pad - k) // stride + 1
     d = (cin * k * k + 7) // 8 * 8
     return Layer("conv", ho * ho, d, cout, (cin, k, stride, pad, hin))
+
+
+def _gpt2_full_block(d: int, T: int) -> List[Layer]:
+    # every trainable tensor of a block: ln_1, attention qkv and output,
+    # ln_2, MLP up and down, with the biases of the four linear maps
+    return [Layer("norm", T, d, d, bias=True), Layer("linear", T, d, 3 * d, bias=True),
+            Layer("linear", T, d, d, bias=True), Layer("norm", T, d, d, bias=True),
+            Layer("linear", T, d, 4 * d, bias=True), Layer("linear", T, 4 * d, d, bias=True)]
 
 
 def _lora(d: int, r: int, T: int, blocks: int) -> List[Layer]:
@@ -146,6 +157,12 @@ def _build() -> dict:
                     "auto", gamma=0.01, sigma=1.0, g_scale=1e-2,
                     description="LoRA rank 16 on the query and value projections of 12 GPT-2-small "
                                 "blocks: 24 x (768 -> 16, 16 -> 768)")
+    w[8] = Workload(8, "gpt2-small-full-T128-B32-bf16+bias+ln", 32, "bf16",
+                    tuple(l for _ in range(12) for l in _gpt2_full_block(768, 128)) +
+                    (Layer("norm", 128, 768, 768, bias=True),),
+                    "auto", gamma=0.01, sigma=1.0, g_scale=1e-2,
+                    description="12 GPT-2-small blocks with the biases of their 48 linear maps and "
+                                "their 24 LayerNorm affines, plus the final LayerNorm")
     return w
 
 
@@ -217,7 +234,7 @@ def draw_conv(wl: Workload, l: int, B: Optional[int] = None, device="cpu"):
 
 
 def draw_layer(wl: Workload, l: int, B: Optional[int] = None, device="cpu"):
-    """(a or ids, g) of layer l; for a convolution the raw (x, dL/ds) in NCHW."""
+    """(a or ids or xhat, g) of layer l; for a convolution the raw (x, dL/ds) in NCHW."""
     if wl.layers[l].kind == "embed":
         return draw_embedding(wl, l, B, device)
     if wl.layers[l].kind == "conv":
