@@ -64,10 +64,10 @@ __global__ __launch_bounds__(256) void affine_sums_kernel(const AffineArgs args)
     const int p = L.p, T = L.T;
     const int c0 = k * kAffineCols;
     const int tid = threadIdx.x, r = tid >> 5, cl = (tid & 31) * 8;
-    const bool gam = L.x != nullptr;
+    const bool gam = L.gamma != 0;
     const bool vec = L.vec != 0;
     const E* g = static_cast<const E*>(L.g) + (size_t)i * T * p;
-    const E* x = gam ? static_cast<const E*>(L.x) + (size_t)i * T * p : nullptr;
+    const E* x = gam && T > 0 ? static_cast<const E*>(L.x) + (size_t)i * T * p : nullptr;
 
     float s[8], u[8];
 #pragma unroll

@@ -385,6 +385,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             f.part_off = (int32_t)(it.part_off + B * it.np.npart);
             f.vec = (aligned16(L.g) && (!affine || aligned16(L.x)) && (L.p * (int64_t)es) % 16 == 0 &&
                      L.p % 8 == 0) ? 1 : 0;
+            f.gamma = affine ? 1 : 0;
             wg += B * it.np.aff_chunks;
             if (a.n == bk::kMaxAffine && (st = flush()) != BK_OK) return st;
         }

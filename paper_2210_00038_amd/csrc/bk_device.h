@@ -140,8 +140,10 @@ constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint32_t hi0 = __umulhi(kPhiloxM0, c.x), lo0 = kPhiloxM0 * c.x;
-        const uint32_t hi1 = __umulhi(kPhiloxM1, c.z), lo1 = kPhiloxM1 * c.z;
+        // each 32x32 -> 64-bit product in one multiply (v_mad_u64_u32)
+        const uint64_t p0 = (uint64_t)kPhiloxM0 * c.x, p1 = (uint64_t)kPhiloxM1 * c.z;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
         c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
         k0 += kPhiloxW0;
         k1 += kPhiloxW1;
@@ -160,13 +162,14 @@ __device__ __forceinline__ float word_to_uniform(uint32_t w) {
     return (float)(2u * (w >> 9) + 1u) * 5.9604644775390625e-08f;
 }
 
-// Box-Muller: (r cos 2 pi u1, r sin 2 pi u1), r = sqrt(-2 ln u0).
+// Box-Muller: (r cos 2 pi u1, r sin 2 pi u1), r = sqrt(-2 ln u0), with the
+// hardware transcendentals: v_log_f32 (log2; ln u = log2 u ln 2), v_sqrt_f32
+// (the argument is >= 2^-23, no denormals), and v_sin_f32 / v_cos_f32, whose
+// input is in turns, so u1 in (0, 1) needs no range reduction.
 __device__ __forceinline__ float2 box_muller(uint32_t w0, uint32_t w1) {
     const float u0 = word_to_uniform(w0), u1 = word_to_uniform(w1);
-    const float r = sqrtf(-2.0f * logf(u0));
-    float s, c;
-    sincospif(2.0f * u1, &s, &c);
-    return make_float2(r * c, r * s);
+    const float r = __builtin_amdgcn_sqrtf(-2.0f * 0.693147180559945309f * __builtin_amdgcn_logf(u0));
+    return make_float2(r * __builtin_amdgcn_cosf(u1), r * __builtin_amdgcn_sinf(u1));
 }
 
 // The four standard normals of counter block q.

@@ -216,15 +216,17 @@ hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, 
 // partial of the squared norm, sum_c u^2 + s^2, at part[part_off + i chunks + k].
 constexpr int kAffineCols = 256;
 struct AffineLayer {
-    const void* x;      // xhat [B,T,p] (gamma terms), or nullptr
+    const void* x;      // xhat [B,T,p] (gamma terms; may be null when T == 0)
     const void* g;      // [B,T,p]
-    float* P;           // [B,p] gamma sums (with x)
+    float* P;           // [B,p] gamma sums (gamma set)
     float* Pb;          // [B,p] bias / beta sums, or nullptr
     int32_t T, p;
     int32_t chunks;     // ceil(p / kAffineCols)
     int32_t wg_begin;
     int32_t part_off;
     int32_t vec;        // x and g rows 16-byte aligned, 8 | p
+    int32_t gamma;      // the layer has gamma terms (an affine layer)
+    int32_t pad;
 };
 constexpr int kMaxAffine = 64;
 struct AffineArgs {

@@ -62,26 +62,41 @@ __global__ __launch_bounds__(256) void noise_kernel(const NoiseArgs args) {
     const int64_t nq = (n + 3) / 4;
     const int64_t q_begin = (int64_t)(wg - L.wg_begin) * args.bpw;
     const bool vec = (reinterpret_cast<uintptr_t>(G) & 15u) == 0;
-    for (int k = 0; k < (int)(args.bpw / 256); ++k) {
+    // The thread's G blocks are loaded first and its normals drawn while the
+    // loads are in flight; then each block gets its noise and is stored.
+    constexpr int NI = kNoiseBlocksPerWG / 256;
+    const int ni = (int)(args.bpw / 256);
+    float4 v[NI], z[NI];
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
         const int64_t q = q_begin + k * 256 + threadIdx.x;
-        if (q >= nq) break;
-        const float4 z = normal4(args.seed, L.tensor_id, args.step, (uint64_t)q);
+        if (k < ni && q < nq && vec && 4 * q + 3 < n) v[k] = *reinterpret_cast<const float4*>(G + 4 * q);
+    }
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
+        const int64_t q = q_begin + k * 256 + threadIdx.x;
+        if (k < ni && q < nq) z[k] = normal4(args.seed, L.tensor_id, args.step, (uint64_t)q);
+    }
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
+        const int64_t q = q_begin + k * 256 + threadIdx.x;
+        if (k >= ni || q >= nq) break;
         const int64_t e = 4 * q;
         if (vec && e + 3 < n) {
-            float4* p4 = reinterpret_cast<float4*>(G + e);
-            float4 v = *p4;
-            v.x += args.std * z.x;
-            v.y += args.std * z.y;
-            v.z += args.std * z.z;
-            v.w += args.std * z.w;
-            *p4 = v;
+            float4 w = v[k];
+            w.x += args.std * z[k].x;
+            w.y += args.std * z[k].y;
+            w.z += args.std * z[k].z;
+            w.w += args.std * z[k].w;
+            *reinterpret_cast<float4*>(G + e) = w;
         } else {
-            const float zz[4] = {z.x, z.y, z.z, z.w};
+            const float zz[4] = {z[k].x, z[k].y, z[k].z, z[k].w};
             for (int j = 0; j < 4 && e + j < n; ++j) G[e + j] += args.std * zz[j];
         }
     }
 }
 
+// Raw Philox words of counter blocks q0 .. q0 + nq - 1 (a test hook).
 __global__ __launch_bounds__(256) void philox_raw_kernel(uint64_t seed, uint32_t tid, uint32_t step,
                                                          uint64_t q0, int64_t nq, uint32_t* out) {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

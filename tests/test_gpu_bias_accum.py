@@ -157,3 +157,22 @@ def test_accumulation_over_physical_batches(bk, dtype):
         if L.bias:
             Gb = bufs.Gb[l].cpu().numpy()
             assert _frob(Gb - (ref["Gbhat"][l] - ref["Gb"][l]), ref["Gb"][l]) <= TOL[dtype], l
+
+
+@pytest.mark.parametrize("B,T", [(0, 16), (3, 0)])
+def test_empty_batches_with_bias_affine_accumulate(bk, B, T):
+    """No samples or no tokens: norms are zero, written gradients are zero,
+    accumulated gradients keep their values, and nothing faults."""
+    layers = [_L("linear", T, 64, 96, bias=True), _L("norm", T, 40, 40, bias=True), _L("linear", T, 256, 24)]
+    layers[1].d = layers[1].p
+    for acc in (False, True):
+        bufs = _Bufs(bk, layers, max(B, 1))
+        for G in bufs.G + [g for g in bufs.Gb if g is not None]:
+            G.fill_(3.0)
+        ins = [(torch.zeros(B, T, L.d, dtype=torch.bfloat16), torch.zeros(B, T, L.p, dtype=torch.bfloat16))
+               for L in layers]
+        norms, C = _run(bk, layers, ins, bufs, B, torch.bfloat16, bk.BK_CLIP_AUTO, 1.0, 0.01, 0.0, 1, acc)
+        assert norms.size == 0 or np.all(norms == 0.0)
+        want = 3.0 if acc else 0.0
+        for G in bufs.G + [g for g in bufs.Gb if g is not None]:
+            assert torch.all(G == want).item()
