@@ -170,11 +170,15 @@ struct UnfoldJob {
     void* a;
     int C, H, W, kh, kw, stride, pad, Ho, Wo, ld;
     int cc, ngroups, Wp, table_off;   // channels per group, groups, patch row length, table offset
+    int vw;                           // input elements per load (1, 2 or 4; W % vw == 0)
+    int pad_;
 };
 struct TokensJob {
     const void* y;
     void* out;
     int C, HW, tiles_t, tiles_c;
+    int vin;                          // 16-byte loads along HW (HW a multiple of 16 / element size)
+    int pad_;
 };
 constexpr int kMaxPrepJobs = 24;
 struct PrepArgs {

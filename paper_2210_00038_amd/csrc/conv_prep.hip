@@ -19,8 +19,9 @@
 // whose ld is not a multiple of VE, take the one-element-per-thread kernel.
 //
 // tokens: [B, C, HW] -> [B, HW, C] through a 64 x 64 LDS tile, read along
-// HW and written as 16-byte rows along C (C a multiple of VE); other C take a
-// 32 x 33 tile with scalar stores.
+// HW (16 bytes at a time when HW is a multiple of VE) and written as 16-byte
+// rows along C (C a multiple of VE); other C take a 32 x 33 tile with scalar
+// stores.
 #include "bk_device.h"
 #include "bk_kernels.h"
 
@@ -84,6 +85,15 @@ __device__ __forceinline__ int small_div(int n, int dv, float rdv) {
     return q;
 }
 
+// N consecutive elements (N * sizeof(E) bytes, that aligned) in one load.
+template <typename E, int N>
+__device__ __forceinline__ void load_vec(const E* src, E (&v)[4]) {
+    struct alignas(N * sizeof(E)) Pack { E e[N]; };
+    const Pack p = *reinterpret_cast<const Pack*>(src);
+#pragma unroll
+    for (int j = 0; j < N; ++j) v[j] = p.e[j];
+}
+
 // One unfold workgroup: channel group g of output row oh of sample b.
 template <typename E>
 __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int oh, int g,
@@ -102,31 +112,47 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
     const int ncols = (c0 + cg == C) ? ld - col0 : cg * khkw;
     const int zslot = cc * kh * Wp;
 
-    // input rows (c, i) of this output row, zero outside the image; the
-    // patch is walked flat (element e = row Wp + wp) so every lane loads
-    const int nel = cg * kh * Wp;
-    const float rWp = 1.0f / (float)Wp, rkh = 1.0f / (float)kh;
+    // input rows (c, i) of this output row: the patch is zeroed, then the
+    // in-image part of each row (columns w < Wv of the input row, at patch
+    // column pad + w) is copied J.vw elements per load, walked flat over
+    // (row, vector) so every lane loads
+    const int nz = cc * kh * Wp + 1;
+    for (int e = tid; e < nz; e += kUnfoldThreads) patch[e] = E{};
+    __syncthreads();
+    const int vw = J.vw;
+    const int Wv = min(W, Wp - pad);                  // image columns inside the patch row
+    const int nv = Wv > 0 ? (Wv + vw - 1) / vw : 0;   // loads per row
+    const int nrows = cg * kh, nel = nrows * nv;
+    const float rnv = 1.0f / (float)max(nv, 1), rkh = 1.0f / (float)kh;
     const E* xb = x + (b * C + c0) * (int64_t)H * W;
     for (int e0 = tid; e0 < nel; e0 += kFillUnroll * kUnfoldThreads) {
-        E v[kFillUnroll];
+        E v[kFillUnroll][4];
+        int dst[kFillUnroll], cnt[kFillUnroll];
 #pragma unroll
         for (int u = 0; u < kFillUnroll; ++u) {
             const int e = e0 + u * kUnfoldThreads;
-            v[u] = E{};
+            cnt[u] = 0;
+            dst[u] = 0;
             if (e < nel) {
-                const int r = small_div(e, Wp, rWp), wp = e - r * Wp;
+                const int r = small_div(e, nv, rnv), w0 = (e - r * nv) * vw;
                 const int cr = small_div(r, kh, rkh), i = r - cr * kh;
-                const int h = oh * stride + i - pad, w = wp - pad;
-                if (h >= 0 && h < H && w >= 0 && w < W) v[u] = xb[((int64_t)cr * H + h) * W + w];
+                const int h = oh * stride + i - pad;
+                if (h >= 0 && h < H) {
+                    const E* src = xb + ((int64_t)cr * H + h) * W + w0;     // w0 + vw <= W
+                    if (vw == 4) load_vec<E, 4>(src, v[u]);
+                    else if (vw == 2) load_vec<E, 2>(src, v[u]);
+                    else v[u][0] = *src;
+                    cnt[u] = min(vw, Wv - w0);
+                    dst[u] = r * Wp + pad + w0;
+                }
             }
         }
 #pragma unroll
-        for (int u = 0; u < kFillUnroll; ++u) {
-            const int e = e0 + u * kUnfoldThreads;
-            if (e < nel) patch[e] = v[u];
-        }
+        for (int u = 0; u < kFillUnroll; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (j < cnt[u]) patch[dst[u] + j] = v[u][j];
     }
-    if (tid == 0) patch[zslot] = E{};
     for (int col = tid; col < ncols; col += kUnfoldThreads) {
         const int gc = col0 + col;
         int off = -1;
@@ -173,13 +199,27 @@ __device__ __forceinline__ void tokens_block(const TokensJob& J, int64_t b, int 
     const int tid = threadIdx.x;
     const E* src = static_cast<const E*>(J.y) + b * C * HW;
     E* dst = static_cast<E*>(J.out) + b * C * HW;
+    if (J.vin) {
+        // 16-byte loads: VE consecutive tokens of one channel (HW % VE == 0)
+        constexpr int CPT = 64 / VE;                   // chunks per channel row of the tile
 #pragma unroll
-    for (int it = 0; it < 16; ++it) {
-        const int idx = it * 256 + tid, cl = idx >> 6, tl = idx & 63;
-        const int64_t c = c0 + cl, t = t0 + tl;
-        E v{};
-        if (c < C && t < HW) v = src[c * HW + t];
-        tile[tl * LDR + cl] = v;
+        for (int it = 0; it < CPT / 4; ++it) {
+            const int idx = it * 256 + tid, cl = idx / CPT, tc = (idx % CPT) * VE;
+            const int64_t c = c0 + cl, t = t0 + tc;
+            Vec16<E> v{};
+            if (c < C && t < HW) v = *reinterpret_cast<const Vec16<E>*>(src + c * HW + t);
+#pragma unroll
+            for (int j = 0; j < VE; ++j) tile[(tc + j) * LDR + cl] = v.v[j];
+        }
+    } else {
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+            const int idx = it * 256 + tid, cl = idx >> 6, tl = idx & 63;
+            const int64_t c = c0 + cl, t = t0 + tl;
+            E v{};
+            if (c < C && t < HW) v = src[c * HW + t];
+            tile[tl * LDR + cl] = v;
+        }
     }
     __syncthreads();
     constexpr int CPR = 64 / VE;                        // 16-byte chunks per tile row
@@ -291,8 +331,12 @@ hipError_t add_unfold(PrepBuilder& P, const void* x, void* a, const UnfoldShape&
         if (e != hipSuccess) return e;
     }
     UnfoldJob& J = P.A.u[P.A.nu];
+    // widest input load that divides the row length and the base alignment
+    int vw = 1;
+    for (int cand : {4, 2})
+        if (s.W % cand == 0 && reinterpret_cast<uintptr_t>(x) % (cand * sizeof(E)) == 0) { vw = cand; break; }
     J = UnfoldJob{x, a, (int)s.C, (int)s.H, (int)s.W, (int)s.kh, (int)s.kw, (int)s.stride, (int)s.pad,
-                  (int)s.Ho, (int)s.Wo, (int)s.ld, p.cc, p.ngroups, p.Wp, (int)p.table_off};
+                  (int)s.Ho, (int)s.Wo, (int)s.ld, p.cc, p.ngroups, p.Wp, (int)p.table_off, vw, 0};
     P.blocks += nblk;
     P.A.blk_end[P.A.nu++] = (int)P.blocks;
     P.lds = std::max<int>(P.lds, (int)p.lds);
@@ -316,7 +360,8 @@ hipError_t add_tokens(PrepBuilder& P, const void* y, void* out, int64_t B, int64
         if (e != hipSuccess) return e;
     }
     TokensJob& J = P.A.t[P.A.nt];
-    J = TokensJob{y, out, (int)C, (int)HW, (int)tt, (int)tc};
+    const int vin = (HW % Vec16<E>::N == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0) ? 1 : 0;
+    J = TokensJob{y, out, (int)C, (int)HW, (int)tt, (int)tc, vin, 0};
     P.blocks += nblk;
     P.A.blk_end[P.A.nu + P.A.nt++] = (int)P.blocks;
     P.lds = std::max<int>(P.lds, tokens_lds<E>());

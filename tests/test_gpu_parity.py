@@ -470,6 +470,8 @@ def test_lora_adapter_stack_matches_oracle(bk, module, d, r, T, B):
     (1, 512, 7, 7, 3, 1, 1, 0),       # channel groups (the patch of 512 channels exceeds one workgroup)
     (1, 520, 9, 6, 3, 2, 1, 4688),    # fp32: two groups, the last one carries the zero columns
     (2, 2, 10, 10, 3, 1, 1, 27),      # ld not a multiple of 16 bytes: element-wise kernel
+    (2, 16, 12, 12, 3, 1, 1, 0),      # 4-element input loads; 16-byte token loads (HW = 144)
+    (2, 8, 14, 20, 3, 2, 0, 0),       # last input load clipped to the patch row (Wp - pad < W)
 ])
 def test_unfold_and_tokens_bit_exact(bk, dtype, B, C, H, W, k, stride, pad, ld):
     gen = torch.Generator().manual_seed(C * H + k)
