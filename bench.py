@@ -207,6 +207,30 @@ def dominant_kernel(w: wl.Workload, phase: str) -> str:
     return max(share, key=share.get)
 
 
+def plain_gemm_ms(w: wl.Workload, ins, reps: int = 10) -> float:
+    """hipBLASLt (torch.mm) time of the plain gradients a_flat^T g_flat of every
+    linear / unfolded-conv layer of the stack (bf16 in; no weights, no noise),
+    the denominator of the stack overhead together with the library's own GEMM."""
+    flat = [(x.reshape(-1, x.shape[-1]), g.reshape(-1, g.shape[-1])) for L, (x, g) in zip(w.layers, ins)
+            if L.kind in ("linear", "conv")]
+    if not flat:
+        return float("nan")
+
+    def run():
+        for a, g in flat:
+            torch.mm(a.t(), g)
+    for _ in range(2):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def source_hash(rel: str) -> str:
     import hashlib
     with open(os.path.join(ROOT, rel), "rb") as f:
@@ -423,6 +447,13 @@ def main():
         "mfma_frac": {"ghost_norm_paper_flops": phases["norms"].get("tflops", 0) / peak_mfma,
                       "weighted_gemm": phases["weighted_grads"]["tflops"] / peak_mfma},
     }
+    if w.dtype == "bf16" and K == 1:
+        # stack overhead against the plain gradient GEMMs: the faster of
+        # hipBLASLt on a_flat^T g_flat and the library's own clipped GEMM
+        hb = plain_gemm_ms(w, ins)
+        own = phases["weighted_grads"]["ms"]
+        res["plain_gemm"] = {"hipblaslt_ms": round(hb, 4), "own_ms": own,
+                             "stack_over_plain": round(ms_step / min(hb, own), 3)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)
