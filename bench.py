@@ -115,17 +115,21 @@ def make_inputs(w: wl.Workload, dev):
     return ins, raw, Gs
 
 
-def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
-    """The float64 oracle on the host: whole path on the first layers of the
-    stack (all B samples), until ~budget_s of work; scaled to the whole stack
-    by the fraction of its gradient flops done."""
-    import oracle
+def _cpu_model() -> str:
     try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
-    total = algorithmic_work(w)["gemm_flops"] + 1e-9
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
+def _oracle_pass(w: wl.Workload, budget_s: float):
+    """The float64 oracle on the first layers of the stack (all B samples)
+    until ~budget_s of work; returns (seconds, gradient flops done, layers)."""
+    import oracle
     done, t_used, nl = 0.0, 0.0, 0
     for l, L in enumerate(w.layers):
         x, g = wl.draw_layer(w, l)
@@ -151,10 +155,28 @@ def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
         nl += 1
         if t_used >= budget_s:
             break
-    t_full = t_used * total / done
+    return t_used, done, nl
+
+
+def cpu_baseline(w: wl.Workload, budget_s: float = 12.0, single_budget_s: float = 6.0):
+    """The float64 oracle on the host with its BLAS on every thread it is
+    given, then again on one thread; each pass covers the first layers of the
+    stack (all B samples, input generation excluded) for ~its budget of work
+    and is scaled to the whole stack by the fraction of its gradient flops."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    total = algorithmic_work(w)["gemm_flops"] + 1e-9
+    t_used, done, nl = _oracle_pass(w, budget_s)
+    with threadpool_limits(limits=1):
+        t1, done1, nl1 = _oracle_pass(w, single_budget_s)
+    t_full, t_full1 = t_used * total / done, t1 * total / done1
     return {"value": w.B / t_full, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {nl} of {len(w.layers)} layers, all {w.B} samples, full path in float64 "
-                      f"({t_used:.1f} s), scaled by gradient flops to the whole stack"}
+                      f"({t_used:.1f} s), scaled by gradient flops to the whole stack",
+            "s_per_step": round(t_full, 3),
+            "single_thread": {"value": w.B / t_full1, "s_per_step": round(t_full1, 3), "cores": 1,
+                              "sample": f"first {nl1} layers ({t1:.1f} s), scaled the same way"},
+            "host": {"cpu_model": _cpu_model(), "os_cpu_count": os.cpu_count()}}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -272,6 +294,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-plain-gemm", action="store_true",
+                    help="skip the hipBLASLt plain-GEMM denominator (keeps a kernel trace to the library)")
     ap.add_argument("--mixopt", action="store_true",
                     help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
     ap.add_argument("--accumulate", type=int, default=1,
@@ -383,6 +407,7 @@ def main():
         out[3] = e[4 * K].elapsed_time(e[4 * K + 1])
         return out
     ph_ms = np.array([phase_ms(e) for e in evs]).mean(axis=0)
+    step_ev = np.array([e[0].elapsed_time(e[-1]) for e in evs])
     work = algorithmic_work(w, args.mixopt)
     work = {k: (v * K if k in ("norm_flops", "norm_bytes", "gemm_flops", "gemm_bytes", "prep_bytes") else v)
             for k, v in work.items()}
@@ -443,11 +468,14 @@ def main():
                    "conv": work["conv_layers"], "affine": work["affine_layers"],
                    "bias": work["bias_terms"]}},
         "roofline": roof,
+        "step_ms_events": {"p10": round(float(np.percentile(step_ev, 10)), 4),
+                           "median": round(float(np.median(step_ev)), 4),
+                           "p90": round(float(np.percentile(step_ev, 90)), 4)},
         "phases": phases,
         "mfma_frac": {"ghost_norm_paper_flops": phases["norms"].get("tflops", 0) / peak_mfma,
                       "weighted_gemm": phases["weighted_grads"]["tflops"] / peak_mfma},
     }
-    if w.dtype == "bf16" and K == 1:
+    if w.dtype == "bf16" and K == 1 and not args.no_plain_gemm:
         # stack overhead against the plain gradient GEMMs: the faster of
         # hipBLASLt on a_flat^T g_flat and the library's own clipped GEMM
         hb = plain_gemm_ms(w, ins)
