@@ -299,7 +299,13 @@ bk_status bk_layer_norms(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t
                          float* norm_sq, void* ws, size_t ws_bytes, void* stream);
 
 /* Clipped gradients of every layer into layers[l].G (BK_LAYER_MIXOPT
- * instantiated layers: the weighted sum of their P). */
+ * instantiated layers: the weighted sum of their P).  The workspace holds
+ * float32 partial tiles of K-split GEMM tiles: those of layers with few
+ * output tiles, and those of the last, partly filled round of workgroups of
+ * a large launch (at most (compute units) x 256 KiB for each).  Its size
+ * depends on the compute-unit count of the device current at the query
+ * (256 when no device can be asked); query with the launching device
+ * current. */
 size_t bk_weighted_grads_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt,
                                         int64_t B);
 bk_status bk_weighted_grads(const bk_layer* layers, int64_t n, const float* C, bk_dtype dt,

@@ -136,6 +136,10 @@ __device__ __forceinline__ uint4 frag(const char* lds, int ms, int j, int lane) 
 __device__ __forceinline__ void put_col16(float* out, size_t sm, size_t sn, int r0, int rmax, int n, int lane,
                                           const f32x16_t& v, float scale, bool add) {
     if (add) {
+        // The product is rounded before the add (no fused multiply-add), so
+        // that adding to G gives the same value as writing v * scale and
+        // adding G's old value afterwards.
+#pragma clang fp contract(off)
         float o[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -1014,17 +1018,24 @@ constexpr int kDStage = 2 * kDOp;
 constexpr int kDKK = kDKS / 16;                  // 16-row MFMA steps per stage
 constexpr int kDPW = kDKS / 8;                   // DMA instructions per wave per stage
 
-__global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, int n_wg) {
+__global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, int n_remap) {
     __shared__ __attribute__((aligned(16))) char lds[kDNB * kDStage];
     __shared__ float ctab[kDMaxB + 1];
 
-    const int wg = xcd_remap(blockIdx.x, n_wg);
+    // The first n_remap workgroups in contiguous runs per XCD; the tail (the
+    // K slices of the last round's tiles) in launch order, so that it is
+    // dispatched last.
+    const int wg = (int)blockIdx.x < n_remap ? xcd_remap(blockIdx.x, n_remap) : (int)blockIdx.x;
     int l = 0;
     while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
-    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
-    const int tile = local / ks, slice = local - tile * ks;
+    const int local = wg - L.wg_begin, sf = L.split_from;
+    // Tiles below split_from whole, the others in ksplit slices.
+    const int ks = local < sf ? 1 : max(L.ksplit, 1);
+    const int rel = local < sf ? 0 : (local - sf) / ks;              // split tile, from split_from
+    const int tile = local < sf ? local : sf + rel;
+    const int slice = local < sf ? 0 : (local - sf) - rel * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
@@ -1208,7 +1219,7 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     wait_vmcnt<0>();
 
     if (ks > 1) {
-        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)tile * ks + slice) * (kGM * kGN),
+        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)rel * ks + slice) * (kGM * kGN),
                                      acc, 128 * wm, 64 * wn, lane, c_last);
         return;
     }
@@ -1225,7 +1236,8 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 
 // Sum of the K slices of split layers, slice 0 first.  Workgroup -> layer by
 // red_begin; inside a layer, tile group (sample * tiles + tile for the
-// instantiated norm, tile otherwise) and one kSplitRedWG-element chunk of it.
+// instantiated norm, tile - split_from otherwise) and one kSplitRedWG-element
+// chunk of it.
 // Clipped gradient: the sum goes to G.  Instantiated norm: its squares (of
 // elements inside the matrix) are summed into one norm partial per chunk,
 // and with G set (BK-MixOpt) the sum is also kept in G [B,d,p].
@@ -1241,18 +1253,27 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
     const int tg = job / CH, ch = job - tg * CH;
     const int tiles = L.tm * L.tn;
     const int sample = INST ? tg / tiles : 0;
-    const int tile = tg - sample * tiles;
+    const int tile = tg - sample * tiles + L.split_from;
     const int mt = tile / L.tn, nt = tile - mt * L.tn;
     const int e = ch * kSplitRedWG + 4 * (int)threadIdx.x;
     const int m = mt * TM + e / TN, n = nt * TN + e % TN;
-    const float* src = args.tiles + L.ptile_off + (size_t)tg * max(L.ksplit, 1) * (TM * TN) + e;
+    const int ks = max(L.ksplit, 1);
+    const float* src = args.tiles + L.ptile_off + (size_t)tg * ks * (TM * TN) + e;
+    // Slices in batches of 8 loads issued together, added in slice order.
     float4 sum = *reinterpret_cast<const float4*>(src);
-    for (int q = 1; q < max(L.ksplit, 1); ++q) {
-        const float4 v = *reinterpret_cast<const float4*>(src + (size_t)q * (TM * TN));
-        sum.x += v.x;
-        sum.y += v.y;
-        sum.z += v.z;
-        sum.w += v.w;
+    for (int q0 = 1; q0 < ks; q0 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (q0 + j < ks) v[j] = *reinterpret_cast<const float4*>(src + (size_t)(q0 + j) * (TM * TN));
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (q0 + j < ks) {
+                sum.x += v[j].x;
+                sum.y += v[j].y;
+                sum.z += v[j].z;
+                sum.w += v[j].w;
+            }
     }
     const float r[4] = {sum.x, sum.y, sum.z, sum.w};
     // Tile rows run along d, or along p for a swapped (narrow) layer.
@@ -1330,7 +1351,7 @@ hipError_t launch_split_reduce(const GemmArgs& args, int n_wg, bool inst_norm, G
 }
 
 hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,
-                       hipStream_t s) {
+                       hipStream_t s, int n_remap) {
     if (n_wg <= 0) return hipSuccess;
     const dim3 grid(n_wg), block(256);
     const bool vec = v != GemmVariant::Scalar;
@@ -1341,7 +1362,8 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
     }
     if (v == GemmVariant::GradDL) {
         if (inst_norm) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(agrad_dl_kernel, grid, dim3(512), 0, s, args, n_wg);
+        const int nr = n_remap > 0 && n_remap < n_wg ? n_remap : n_wg;
+        hipLaunchKernelGGL(agrad_dl_kernel, grid, dim3(512), 0, s, args, nr);
         return hipGetLastError();
     }
     if (v == GemmVariant::Wide) {

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cstdarg>
 #include <cstdio>
@@ -425,8 +426,17 @@ bk::GemmVariant grad_variant(const bk_layer& L, bool bf16, int64_t B) {
     return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL : bk::GemmVariant::Grad;
 }
 
-// Tiles and K slices of a linear layer's clipped gradient on variant v.
-struct GradPlan { int64_t tm, tn, ksplit, tile_elems; bool swap; };
+// Tiles and K slices of a linear layer's clipped gradient on variant v
+// (split_from > 0: only the tiles from split_from on are K-split).
+struct GradPlan {
+    int64_t tm, tn, ksplit, tile_elems;
+    bool swap;
+    int64_t split_from = 0;
+    bool tail = false;   // the K-split tiles are a GradDL launch's tail (plan_dl_tail)
+    int64_t tiles() const { return tm * tn; }
+    int64_t split_tiles() const { return ksplit > 1 ? tm * tn - split_from : 0; }
+    int64_t wgs() const { return split_from + (tm * tn - split_from) * ksplit; }
+};
 GradPlan grad_plan(const bk_layer& L, bk::GemmVariant v, int64_t B) {
     const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
     GradPlan g{geo.tm, geo.tn, 1, geo.tile_elems, geo.swap};
@@ -439,16 +449,94 @@ GradPlan grad_plan(const bk_layer& L, bk::GemmVariant v, int64_t B) {
     return g;
 }
 
-size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
-    size_t tot = 0, tiles = 0;
-    for (int64_t l = 0; l < n; ++l) {
-        const bk_layer& L = layers[l];
-        if (L.kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, L.T, L.d));
-        if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
-        const GradPlan g = grad_plan(L, grad_variant(L, dt == BK_BF16, B), B);
-        if (g.ksplit > 1) tiles += (size_t)(g.tm * g.tn * g.ksplit * g.tile_elems) * sizeof(float);
+// Compute units of the current device (256, MI355X's, when there is none to
+// ask, e.g. for a workspace query on a host without a GPU).
+int64_t device_cus() {
+    constexpr int kMaxDev = 64;
+    static std::atomic<int> cache[kMaxDev];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 256;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+        return 256;
+    cache[dev].store(v, std::memory_order_relaxed);
+    return v;
+}
+
+// One grouped clipped-gradient launch: layers of one kernel variant, in
+// launch order.
+struct GradEntry { int64_t l; GradPlan gp; };
+struct GradGroup { bk::GemmVariant v; std::vector<GradEntry> e; };
+
+constexpr int64_t kTailMinStages = 8;    // stages per slice of a split tail tile, at least
+constexpr int64_t kTailMaxSplit = 16;    // K slices per tail tile, at most
+
+// The GradDL kernel holds one workgroup per CU, so a launch of N tiles of
+// equal work runs in ceil(N / cus) rounds.  When the last round is at most
+// half full (r = N mod cus tiles), those r tiles are cut into s = cus / r K
+// slices each and moved behind every other tile in launch order: the slices
+// are dispatched last and fill the CUs together once the full rounds are
+// done.  They are taken from the layer with the most tiles, which goes last.
+void plan_dl_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) {
+    if (g.e.empty()) return;
+    const int64_t T0 = layers[g.e[0].l].T;
+    int64_t N = 0;
+    size_t best = 0;
+    for (size_t k = 0; k < g.e.size(); ++k) {
+        if (g.e[k].gp.ksplit != 1 || layers[g.e[k].l].T != T0) return;   // unequal work
+        N += g.e[k].gp.tiles();
+        if (g.e[k].gp.tiles() > g.e[best].gp.tiles()) best = k;
     }
-    return std::max(tot, tiles);
+    const int64_t r = N % cus;
+    if (r == 0 || 2 * r > cus || g.e[best].gp.tiles() < r) return;
+    const int64_t nst = cdiv(B * T0, bk::kDLStageRows);
+    const int64_t sp = std::min({cus / r, nst / kTailMinStages, kTailMaxSplit});
+    if (sp < 2) return;
+    std::rotate(g.e.begin() + (std::ptrdiff_t)best, g.e.begin() + (std::ptrdiff_t)best + 1, g.e.end());
+    GradPlan& gp = g.e.back().gp;
+    gp.ksplit = sp;
+    gp.split_from = gp.tiles() - r;
+    gp.tail = true;
+}
+
+// The grouped launches of bk_weighted_grads: by kernel variant, at most
+// kMaxGemm layers each.
+std::vector<GradGroup> grad_groups(const bk_layer* layers, int64_t n, bool bf16, int64_t B) {
+    std::vector<GradGroup> out;
+    for (int var = 0; var < bk::kGemmVariants; ++var) {
+        for (int64_t l = 0; l < n; ++l) {
+            const bk_layer& L = layers[l];
+            if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
+            const auto v = grad_variant(L, bf16, B);
+            if ((int)v != var) continue;
+            if (out.empty() || out.back().v != v || (int64_t)out.back().e.size() == bk::kMaxGemm)
+                out.push_back(GradGroup{v, {}});
+            out.back().e.push_back(GradEntry{l, grad_plan(L, v, B)});
+        }
+    }
+    int64_t cus = 0;
+    for (GradGroup& g : out)
+        if (g.v == bk::GemmVariant::GradDL) {
+            if (cus == 0) cus = device_cus();
+            plan_dl_tail(g, layers, B, cus);
+        }
+    return out;
+}
+
+size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    size_t tot = 0;
+    for (int64_t l = 0; l < n; ++l)
+        if (layers[l].kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T, layers[l].d));
+    // Grouped launches follow each other on the stream: each one's partial
+    // tiles start at the workspace's beginning.
+    for (const GradGroup& g : grad_groups(layers, n, dt == BK_BF16, B)) {
+        size_t tiles = 0;
+        for (const GradEntry& e : g.e)
+            tiles += (size_t)(e.gp.split_tiles() * e.gp.ksplit * e.gp.tile_elems) * sizeof(float);
+        tot = std::max(tot, tiles);
+    }
+    return tot;
 }
 
 // Appends one weighted-sum job (P [B, n] -> G [n]) to a grouped launch.
@@ -480,32 +568,20 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     const bool bf16 = dt == BK_BF16;
 
     // Grouped launches by kernel variant.  Layers with few output tiles run
-    // K-split (grad_plan); their partial tiles sit in the workspace (launches
-    // follow each other on the stream, so each starts from offset 0).
-    for (int var = 0; var < bk::kGemmVariants; ++var) {
+    // K-split (grad_plan), and so do the tiles of a GradDL launch's last,
+    // partly filled round (plan_dl_tail); the partial tiles sit in the
+    // workspace (launches follow each other on the stream, so each starts
+    // from offset 0).
+    for (const GradGroup& grp : grad_groups(layers, n, bf16, B)) {
         bk::GemmArgs a{};
         a.B = (int32_t)B;
         a.C = C;
         a.part = nullptr;
         a.tiles = static_cast<float*>(ws);
-        int64_t wg = 0, ptile = 0, red = 0;
-        auto flush = [&]() -> bk_status {
-            if (a.n == 0) return BK_OK;
-            if (wg > INT32_MAX || red > INT32_MAX)
-                return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
-            hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, bk::GemmVariant(var), s);
-            if (e == hipSuccess && red > 0)
-                e = bk::launch_split_reduce(a, (int)red, false, bk::GemmVariant(var), s);
-            a.n = 0;
-            wg = ptile = red = 0;
-            return e == hipSuccess ? BK_OK : hip_fail(e, "clipped gradient launch");
-        };
-        for (int64_t l = 0; l < n; ++l) {
-            const bk_layer& L = layers[l];
-            if (L.kind != BK_LINEAR || L.d * L.p == 0 || keeps_grads(L)) continue;
-            const auto v = grad_variant(L, bf16, B);
-            if ((int)v != var) continue;
-            const GradPlan gp = grad_plan(L, v, B);
+        int64_t wg = 0, ptile = 0, red = 0, remap = 0;
+        for (const GradEntry& e : grp.e) {
+            const bk_layer& L = layers[e.l];
+            const GradPlan& gp = e.gp;
             bk::GemmLayer& g = a.L[a.n++];
             g.a = L.x;
             g.g = L.g;
@@ -519,18 +595,22 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
             g.wg_begin = (int32_t)wg;
             g.part_off = 0;
             g.ksplit = (int32_t)gp.ksplit;
+            g.split_from = (int32_t)gp.split_from;
             g.swap = gp.swap ? 1 : 0;
             g.accum = (L.flags & BK_LAYER_ACCUMULATE) ? 1 : 0;
             g.ptile_off = ptile;
             g.red_begin = (int32_t)red;
-            wg += gp.tm * gp.tn * gp.ksplit;
+            if (gp.tail) remap = wg + gp.split_from;   // the last layer; its slices run last
+            wg += gp.wgs();
             if (gp.ksplit > 1) {
-                ptile += gp.tm * gp.tn * gp.ksplit * gp.tile_elems;
-                red += gp.tm * gp.tn * (gp.tile_elems / bk::kSplitRedWG);
+                ptile += gp.split_tiles() * gp.ksplit * gp.tile_elems;
+                red += gp.split_tiles() * (gp.tile_elems / bk::kSplitRedWG);
             }
-            if (a.n == bk::kMaxGemm && (st = flush()) != BK_OK) return st;
         }
-        if ((st = flush()) != BK_OK) return st;
+        if (wg > INT32_MAX || red > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
+        hipError_t e = bk::launch_gemm(a, (int)wg, bf16, false, grp.v, s, (int)remap);
+        if (e == hipSuccess && red > 0) e = bk::launch_split_reduce(a, (int)red, false, grp.v, s);
+        if (e != hipSuccess) return hip_fail(e, "clipped gradient launch");
     }
     // Weighted sums of stored per-sample gradients: BK-MixOpt weights, the
     // gammas of affine layers, and every bias / beta.

@@ -47,7 +47,20 @@ def test_workspace_sizes():
     assert ws >= 16 * 36 * 4                    # 8 super blocks -> 36 pairs
     ws = bk.bk_workspace_size(bk.BK_OP_INST_NORM, bk.BK_BF16, 16, 1024, 768, 768)
     assert ws >= 16 * 36 * 4                    # 6 x 6 output tiles
-    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 768, 768) == 0
+    # 3 x 3 tiles of 256 x 256 fill under half of 256 CUs (the host-side CU
+    # count when no device answers): each tile in 16 K slices of fp32 partials
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 768, 768) == \
+        9 * 16 * 256 * 256 * 4
+    # 11 x 11 tiles: the last round (121 tiles) is under half of 256 CUs
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 2816, 2816) == \
+        121 * 2 * 256 * 256 * 4
+    # 17 x 16 = 272 tiles: 16 left over, each in 16 slices
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 4352, 4096) == \
+        16 * 16 * 256 * 256 * 4
+    # 12 x 12 = 144 tiles, over half of 256: no split
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 3072, 3072) == 0
+    # T not a multiple of 32 (the other 256 x 256 kernel): no tail split
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1000, 768, 768) == 0
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) >= \
         16 * 256 * 8 + 50257 * 4
     assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, 7, 1, 1, 1, 1) == 0        # bad dtype
@@ -242,3 +255,20 @@ def test_bias_affine_accumulate_validation():
     # no samples: nothing to check beyond the flags, nothing launched
     assert bk.lib.bk_layer_norms(one(flags=bk.BK_LAYER_BIAS | bk.BK_LAYER_ACCUMULATE), 1, bk.BK_BF16, 0,
                                  None, None, 0, None) == bk.BK_OK
+
+
+def test_grouped_noise_validation():
+    """The grouped noise entry point checks its arrays and std before any
+    launch; n = 0 and std = 0 launch nothing."""
+    ptrs = (ctypes.c_void_p * 2)(0x10000, None)
+    nel = (ctypes.c_int64 * 2)(4, 4)
+    tids = (ctypes.c_uint32 * 2)(0, 1)
+    for fn in (bk.lib.bk_add_noise_grouped,):
+        assert fn(None, nel, tids, 2, 1.0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+        assert fn(ptrs, nel, tids, -1, 1.0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+        assert fn(ptrs, nel, tids, 2, float("nan"), 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+        assert fn(ptrs, nel, tids, 2, -0.5, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
+        assert fn(ptrs, nel, tids, 2, 1.0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE   # tensor 1 NULL
+        assert "NULL" in bk.bk_last_error()
+        assert fn(ptrs, nel, tids, 0, 1.0, 0, 0, None) == bk.BK_OK
+    assert bk.lib.bk_add_noise_grouped(ptrs, nel, tids, 1, 0.0, 0, 0, None) == bk.BK_OK

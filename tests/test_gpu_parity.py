@@ -397,6 +397,47 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
 
 
+# A grouped launch of the LDS-DMA kernel (one workgroup per CU) whose last
+# round of tiles is under half full: those tiles run in K slices, dispatched
+# after every whole tile, and are summed in slice order.
+@pytest.mark.parametrize("shapes,B,T,zero", [
+    ([(768, 4096)] * 6, 4, 512, [1]),         # 288 tiles: 32 split from the middle of a layer
+    ([(512, 4096)] * 9, 4, 256, []),          # 288 tiles: one whole 32-tile layer split
+    ([(768, 768)], 3, 256, [0]),              # 9 tiles, no whole round: all split
+])
+def test_weighted_grads_tail_split(bk, shapes, B, T, zero):
+    gen = torch.Generator().manual_seed(B * T + len(shapes))
+    ins = [((torch.randn(B, T, d, generator=gen)).to(torch.bfloat16),
+            (torch.randn(B, T, p, generator=gen) * 1e-2).to(torch.bfloat16)) for d, p in shapes]
+    C = torch.rand(B, generator=gen) + 0.1
+    C[zero] = 0.0
+    dev = [(a.to(DEV), g.to(DEV)) for a, g in ins]
+    Gs = [torch.empty(d, p, device=DEV) for d, p in shapes]
+    specs = [{"kind": bk.BK_LINEAR, "x": a, "g": g, "G": G} for (a, g), G in zip(dev, Gs)]
+    arr = bk.make_layers(specs)
+    n = len(shapes)
+    tiles = sum((d // 256) * (p // 256) for d, p in shapes)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    ws = bk.bk_weighted_grads_workspace_size(arr, n, bk.BK_BF16, B)
+    if tiles % cus and 2 * (tiles % cus) <= cus:
+        assert ws > 0                      # the tail is split
+    Cd = C.to(DEV)
+    bk.bk_weighted_grads(arr, n, Cd, bk.BK_BF16, B)
+    first = [G.clone() for G in Gs]
+    for (a, g), G in zip(ins, first):
+        assert _frob(G.cpu().numpy(), oracle.weighted_grad(a, g, C)) <= GRAD_TOL[torch.bfloat16]
+    # bitwise reproducible, and an accumulating call adds exactly what a
+    # writing call writes (the product by the weight is rounded before the add)
+    bk.bk_weighted_grads(arr, n, Cd, bk.BK_BF16, B)
+    assert all(torch.equal(G, F) for G, F in zip(Gs, first))
+    G0 = [torch.randn(G.shape, generator=gen).to(DEV) for G in Gs]
+    for G, g0 in zip(Gs, G0):
+        G.copy_(g0)
+    acc = bk.make_layers([dict(sp, accumulate=True) for sp in specs])
+    bk.bk_weighted_grads(acc, n, Cd, bk.BK_BF16, B)
+    assert all(torch.equal(G, g0 + F) for G, g0, F in zip(Gs, G0, first))
+
+
 # ------------------------------------------- narrow layers (one side <= 64)
 @pytest.mark.parametrize("B,T,d,p", [
     (3, 50, 768, 16),       # 256 x 32 tiles, rows along d
