@@ -185,6 +185,7 @@ KERNEL_SOURCES = {"agrad_dl_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "agemm_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "anarrow_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
+                  "split_reduce_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "conv_prep_kernel": "paper_2210_00038_amd/csrc/conv_prep.hip"}
 
 
@@ -263,6 +264,9 @@ def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` on `workload` from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary, scaled by the copy-kernel
     calibration; None when absent or when the kernel source has changed."""
+    if " + " in kernel:           # launches of one phase: their bytes add up
+        parts = [measured_traffic(k, workload) for k in kernel.split(" + ")]
+        return None if any(v is None for v in parts) else sum(parts)
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
@@ -441,6 +445,12 @@ def main():
         kinds = {(grad_kernel if dom == "weighted_grads" else norm_kernel)(L, w.dtype) for L in w.layers}
         what = ("clipped gradients" if dom == "weighted_grads" else "per-sample norms") + \
                (", all layers in one launch" if len(kinds) == 1 else ", one launch per kernel variant")
+        if dom == "weighted_grads" and len(kinds) == 1 and all(L.kind != "embed" for L in w.layers) and \
+                bk.bk_weighted_grads_workspace_size(arr, n, dt, B) > 0:
+            # K-split tiles (few-tile layers, or the last round of a launch):
+            # the phase time includes the fixed-order reduction of their slices
+            gk += " + split_reduce_kernel"
+            what += ", plus the reduction of its K-split tiles"
     if flops / max(nbytes, 1.0) > ridge:
         ach = flops / ms_dom / 1e9
         roof = {"kernel": f"{gk} ({what})", "bound": "mfma", "achieved": ach, "peak": peak_mfma,

@@ -56,8 +56,7 @@ __global__ __launch_bounds__(256) void affine_sums_kernel(const AffineArgs args)
     __shared__ float ru[8][kAffineCols];
     __shared__ float red[4];
     const uint32_t wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= (uint32_t)args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const AffineLayer& L = args.L[l];
     const int local = (int)wg - L.wg_begin;
     const int i = local / L.chunks, k = local - i * L.chunks;

@@ -172,8 +172,7 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
     __shared__ float red[4];
 
     const int wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int tiles = L.tm * tn;
@@ -364,8 +363,7 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     __shared__ float red[4];
 
     const int wg = xcd_remap(blockIdx.x, n_wg);
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int tiles = L.tm * tn;
@@ -552,8 +550,7 @@ __global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, in
     __shared__ float red[4];
 
     const int wg = xcd_remap(blockIdx.x, n_wg);
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const bool sw = L.swap != 0;
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
@@ -746,8 +743,7 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     __shared__ __attribute__((aligned(16))) char lds[2 * kGStage];
 
     const int wg = xcd_remap(blockIdx.x, n_wg);
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
@@ -1026,8 +1022,7 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // K slices of the last round's tiles) in launch order, so that it is
     // dispatched last.
     const int wg = (int)blockIdx.x < n_remap ? xcd_remap(blockIdx.x, n_remap) : (int)blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int local = wg - L.wg_begin, sf = L.split_from;
@@ -1246,8 +1241,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
     __shared__ float red[4];
     constexpr int CH = TM * TN / kSplitRedWG;
     const int wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].red_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].red_begin; });
     const GemmLayer& L = args.L[l];
     const int job = wg - L.red_begin;
     const int tg = job / CH, ch = job - tg * CH;

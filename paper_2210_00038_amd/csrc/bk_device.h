@@ -118,6 +118,22 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Sum of one float per thread over a 256-thread workgroup; result valid in
 // thread 0.  `red` must hold 4 floats of LDS.
+// Descriptor of workgroup `wg` in a grouped launch: the last l < n with
+// begin(l) <= wg, begin(l) being descriptor l's first workgroup
+// (non-decreasing in l, begin(0) = 0).  Binary search: a handful of
+// dependent scalar loads of the kernel arguments instead of one per
+// preceding descriptor.
+template <typename Begin>
+__device__ __forceinline__ int find_desc(int n, int64_t wg, Begin begin) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)begin(mid) <= wg) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
     v = wave_sum(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -65,8 +65,7 @@ __global__ __launch_bounds__(256) void clip_kernel(const float* __restrict__ nor
 // [w * bpw, (w + 1) * bpw) of its tensor (bpw = args.bpw, a multiple of 256).
 __global__ __launch_bounds__(256) void noise_kernel(const NoiseArgs args) {
     const uint32_t wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const NoiseLayer& L = args.L[l];
     float* G = L.G;
     const int64_t n = L.n;

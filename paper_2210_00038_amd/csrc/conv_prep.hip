@@ -241,8 +241,7 @@ template <typename E>
 __global__ __launch_bounds__(kUnfoldThreads) void conv_prep_kernel(PrepArgs A) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int blk = blockIdx.x;
-    int j = 0;
-    while (blk >= A.blk_end[j]) ++j;
+    const int j = find_desc(A.nu + A.nt, blk, [&](int k) { return k ? A.blk_end[k - 1] : 0; });
     const int local = blk - (j ? A.blk_end[j - 1] : 0);
     if (j < A.nu) {
         const UnfoldJob& J = A.u[j];

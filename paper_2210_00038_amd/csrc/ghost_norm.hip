@@ -274,8 +274,7 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     __shared__ float red[4];
 
     const int wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GhostLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, nsb = L.nsb, npairs = L.npairs;
     const int local = wg - L.wg_begin;

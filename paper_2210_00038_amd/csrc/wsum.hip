@@ -13,8 +13,7 @@ namespace {
 
 __global__ __launch_bounds__(256) void wsum_kernel(const WsumArgs args) {
     const uint32_t wg = blockIdx.x;
-    int l = 0;
-    while (l + 1 < args.n && wg >= args.L[l + 1].wg_begin) ++l;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const WsumLayer& L = args.L[l];
     const int64_t n = L.n;
     const int64_t e0 = (int64_t)(wg - L.wg_begin) * kWsumPerWG + 4 * (int64_t)threadIdx.x;
