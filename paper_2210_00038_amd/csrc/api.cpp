@@ -81,6 +81,7 @@ struct NormPlan {
     int64_t ksplit = 1; // instantiation: K slices per tile (wide and narrow kernels)
     int64_t tile_elems = 0;   // instantiation: floats of one K-split partial tile
     int64_t aff_chunks = 0;   // per-sample partials of the bias / affine sums (second run)
+    bool fused_bias = false;  // ghost layer whose kernel also forms the bias sums (no second run)
 };
 
 // Variants whose kernels can split a tile's contraction into K slices.
@@ -146,7 +147,11 @@ void finish_norm_plan(NormPlan& np, const bk_layer& L, int64_t B) {
     }
     np.nwg = np.path == Path::Inst ? B * np.tiles * np.ksplit : B * np.npart;
     const bool affine = L.kind == BK_NORM_AFFINE || (L.kind == BK_LINEAR && (L.flags & BK_LAYER_BIAS));
-    np.aff_chunks = affine ? cdiv(L.p, bk::kAffineCols) : 0;
+    // A ghost layer on the 16-byte path with one 128-row block per sample
+    // sums its bias terms while its g passes through LDS for the Gram.
+    np.fused_bias = np.path == Path::Ghost && np.var == 1 && L.T > 0 && L.T <= bk::kSuper &&
+                    L.kind == BK_LINEAR && (L.flags & BK_LAYER_BIAS) && L.p > 0;
+    np.aff_chunks = affine && !np.fused_bias ? cdiv(L.p, bk::kAffineCols) : 0;
 }
 
 // Partial sums of a layer's norm (floats) and its K-split partial tiles (floats).
@@ -290,6 +295,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.npairs = (int32_t)v[k]->np.npart;
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
+            g.Pb = v[k]->np.fused_bias ? L.Pb : nullptr;
             wg += v[k]->np.nwg;
         }
         if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);

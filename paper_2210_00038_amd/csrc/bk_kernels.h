@@ -26,6 +26,10 @@ struct GhostLayer {
     int32_t wg_begin;   // first workgroup of this layer in the launch
     int32_t part_off;   // first partial (float) of this layer in the workspace
     int32_t pad;
+    // Linear layer with a bias, 16-byte rows and T <= 128: the per-sample
+    // bias sums [B,p] go here and their squared norm joins the partials; else
+    // nullptr.
+    float* Pb;
 };
 constexpr int kMaxGhost = 64;
 struct GhostArgs {

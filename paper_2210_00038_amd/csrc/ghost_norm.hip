@@ -158,9 +158,18 @@ constexpr int kRingBytes = 64 * 1024;        // LDS ring of gram_dl
 // row r sits at column c ^ (r / 2 mod 8) (CW = 128: a 256-byte bank line
 // holds two rows) or c ^ (r mod 16) (CW = 256), so that the 16 rows read by
 // 16 lanes land on distinct 16-byte bank groups.
+// Column sums (DIAG with a single 128-row block, i.e. T <= 128): with cs set,
+// each chunk's columns are also summed over the block's rows from LDS, cs[k] =
+// sum_t X[t, k] is written and bsq accumulates cs[k]^2 (threads that finish
+// columns).  Thread t sums 16-byte column t % C16 over every (256 / C16)-th
+// row; lanes of a wave holding the same column are added by shuffles, the
+// four waves through cbuf (two 4 x 128-float halves, by chunk parity), in a
+// fixed order.
 template <typename T, bool DIAG, int CW>
 __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
-                                        const WaveTiles& wt, f32x16_t acc[4], char* __restrict__ lds) {
+                                        const WaveTiles& wt, f32x16_t acc[4], char* __restrict__ lds,
+                                        float* __restrict__ cs = nullptr, float* bsq = nullptr,
+                                        float* cbuf = nullptr) {
     static_assert(CW == 128 || CW == 256, "chunk width");
     constexpr int EPV = Elem<T>::per16;       // elements per 16 bytes
     constexpr int C16 = CW / 16;              // 16-byte columns per row and chunk
@@ -236,6 +245,55 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
         }
     };
 
+    // Column sums of chunk ch into cbuf, and their completion (after the
+    // next barrier) into cs / bsq.
+    constexpr int RPP = 256 / C16;            // rows apart of one thread's reads
+    auto colsum = [&](int ch) {
+        const char* sR = lds + ((ch % NCH) * SPC) * SLOT;
+        const int j = tid % C16;
+        float c[EPV];
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) c[e] = 0.f;
+#pragma unroll
+        for (int q = 0; q < kSuper / RPP; ++q) {
+            const int row = tid / C16 + RPP * q;
+            const uint4 v = *reinterpret_cast<const uint4*>(sR + row * CW + swz(row, j) * 16);
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    c[2 * e] += __uint_as_float(w[e] << 16);
+                    c[2 * e + 1] += __uint_as_float(w[e] & 0xFFFF0000u);
+                }
+            } else {
+                c[0] += __uint_as_float(v.x);
+                c[1] += __uint_as_float(v.y);
+                c[2] += __uint_as_float(v.z);
+                c[3] += __uint_as_float(v.w);
+            }
+        }
+        // lanes j, j + C16, ... of the wave hold the same columns
+#pragma unroll
+        for (int off = C16; off < 64; off <<= 1)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) c[e] += __shfl_xor(c[e], off, 64);
+        if (lane < C16) {
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) cbuf[(ch & 1) * 512 + wave * 128 + j * EPV + e] = c[e];
+        }
+    };
+    auto colsum_done = [&](int ch) {
+        if (tid < EPC) {
+            const float* cb = cbuf + (ch & 1) * 512 + tid;
+            const float v = ((cb[0] + cb[128]) + cb[256]) + cb[384];
+            const int k = ch * EPC + tid;
+            if (k < K) {
+                cs[k] = v;
+                *bsq += v * v;
+            }
+        }
+    };
+
     // Chunk ch: wait for this wave's loads of it (the NCH - 2 later chunks may
     // stay in flight), barrier (everyone's loads of it have landed, and every
     // wave is done with chunk ch - 1), refill chunk ch - 1's slot with chunk
@@ -245,20 +303,30 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
     for (int ch = 0; ch < nch; ++ch) {
         wait_vmcnt<LPW * (NCH - 2)>();
         lds_barrier();
+        if constexpr (DIAG) {
+            if (cs && ch > 0) colsum_done(ch - 1);
+        }
         issue(ch + NCH - 1);
+        if constexpr (DIAG) {
+            if (cs) colsum(ch);
+        }
         compute(ch);
     }
     // Drain the loads past the end and let every wave finish reading before
     // the ring is reused.
     wait_vmcnt<0>();
     lds_barrier();
+    if constexpr (DIAG) {
+        if (cs && nch > 0) colsum_done(nch - 1);
+    }
 }
 
 template <typename T, bool VEC>
 __device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int K, int rowR, int rowC,
-                                         bool diag, const WaveTiles& wt, f32x16_t acc[4], char* smem) {
+                                         bool diag, const WaveTiles& wt, f32x16_t acc[4], char* smem,
+                                         float* cs = nullptr, float* bsq = nullptr, float* cbuf = nullptr) {
     if constexpr (VEC) {
-        if (diag) gram_dl<T, true, BK_GHOST_DIAG_CW>(X, rows, K, rowR, rowC, wt, acc, smem);
+        if (diag) gram_dl<T, true, BK_GHOST_DIAG_CW>(X, rows, K, rowR, rowC, wt, acc, smem, cs, bsq, cbuf);
         else gram_dl<T, false, 128>(X, rows, K, rowR, rowC, wt, acc, smem);
     } else {
         gram<T, VEC>(X, rows, K, rowR, rowC, diag, wt, acc, reinterpret_cast<uint4*>(smem));
@@ -272,6 +340,7 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     uint4* lds = reinterpret_cast<uint4*>(smem);
     __shared__ int64_t sid[2 * kSuper];
     __shared__ float red[4];
+    __shared__ float cbuf[VEC && !EMBED ? 2 * 4 * 128 : 1];   // column sums of the bias (gram_dl)
 
     const int wg = blockIdx.x;
     const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
@@ -319,7 +388,12 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
         f32x16_t accA[4];
         const size_t off_a = (size_t)sample * (size_t)nT * (size_t)d;
         gram_any<T, VEC>(reinterpret_cast<const T*>(L.x) + off_a, nT, d, rowR, rowC, diag, wt, accA, smem);
-        gram_any<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, smem);
+        // Bias of the layer (host: only with 16-byte rows and T <= 128, one
+        // diagonal block per sample): its per-sample sums s = sum_t g_t go to
+        // Pb and |s|^2 joins this workgroup's partial.
+        float* cs = (VEC && L.Pb) ? L.Pb + (size_t)sample * p : nullptr;
+        gram_any<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, smem,
+                         cs, &part, cbuf);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             if (!wt.w[s]) continue;

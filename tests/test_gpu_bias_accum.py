@@ -176,3 +176,30 @@ def test_empty_batches_with_bias_affine_accumulate(bk, B, T):
         want = 3.0 if acc else 0.0
         for G in bufs.G + [g for g in bufs.Gb if g is not None]:
             assert torch.all(G == want).item()
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("T,d,p", [
+    (1, 64, 200),        # one token; the second 128-column chunk is ragged (bf16)
+    (128, 256, 200),     # a full 128-row block
+    (33, 512, 72),       # fp32 chunks of 64 columns: a ragged second chunk
+    (129, 256, 136),     # two row blocks: the bias sums run in their own pass
+    (100, 1024, 1000),   # many chunks
+])
+def test_bias_sums_formed_in_the_ghost_pass(bk, dtype, T, d, p):
+    """A ghost layer with 16-byte rows and T <= 128 forms its per-sample bias
+    sums while g passes through LDS for the Gram; Pb, the norms (weight plus
+    bias term) and the clipped gradients must match the oracle either way."""
+    layers = [_L("linear", T, d, p, bias=True), _L("linear", T, 256, 256, bias=True)]
+    assert all(bk.bk_use_ghost(L.T, L.d, L.p) for L in layers)
+    B = 6
+    ins = _draw(layers, B, dtype, torch.Generator().manual_seed(T * 7 + p))
+    bufs = _Bufs(bk, layers, B)
+    norms, C = _run(bk, layers, ins, bufs, B, dtype, bk.BK_CLIP_ABADI, 1e-3, 0.0, 0.0, 3, False)
+    ref = oracle.bk_stack(layers, ins, "abadi", 1e-3, 0.0, 0.0, seed=3, with_noise=False)
+    assert _rel(norms, ref["norms"]) <= TOL[dtype]
+    assert _rel(C, ref["C"]) <= TOL[dtype]
+    for l in range(len(layers)):
+        assert _frob(bufs.Pb[l].cpu().numpy(), oracle.bias_sums(ins[l][1])) <= TOL[dtype], l
+        assert _frob(bufs.Gb[l].cpu().numpy(), ref["Gb"][l]) <= TOL[dtype], l
+        assert _frob(bufs.G[l].cpu().numpy(), ref["G"][l]) <= TOL[dtype], l
