@@ -177,9 +177,7 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     return np;
 }
 
-size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t V) {
-    return align_up((size_t)(B * T) * sizeof(uint64_t)) + align_up((size_t)V * sizeof(int32_t));
-}
+size_t embed_grad_ws_bytes(int64_t B, int64_t T) { return bk::embed_grad_ws_bytes(B * T); }
 
 // BK-MixOpt layer that keeps its instantiated per-sample gradients in P.
 bool keeps_grads(const bk_layer& L) {
@@ -533,7 +531,7 @@ std::vector<GradGroup> grad_groups(const bk_layer* layers, int64_t n, bool bf16,
 size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
     size_t tot = 0;
     for (int64_t l = 0; l < n; ++l)
-        if (layers[l].kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T, layers[l].d));
+        if (layers[l].kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T));
     // Grouped launches follow each other on the stream: each one's partial
     // tiles start at the workspace's beginning.
     for (const GradGroup& g : grad_groups(layers, n, dt == BK_BF16, B)) {
@@ -651,12 +649,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     for (int64_t l = 0; l < n; ++l) {
         const bk_layer& L = layers[l];
         if (L.kind != BK_EMBEDDING || L.d * L.p == 0) continue;
-        char* w = static_cast<char*>(ws);
-        uint64_t* keys = reinterpret_cast<uint64_t*>(w);
-        int32_t* first = reinterpret_cast<int32_t*>(w + align_up((size_t)(B * L.T) * sizeof(uint64_t)));
         hipError_t e = bk::launch_embed_grad(static_cast<const int64_t*>(L.x), L.g, C, bf16, B, L.T,
-                                             L.p, L.d, L.G, keys, first,
-                                             (L.flags & BK_LAYER_ACCUMULATE) != 0, s);
+                                             L.p, L.d, L.G, ws, (L.flags & BK_LAYER_ACCUMULATE) != 0, s);
         if (e != hipSuccess) return hip_fail(e, "embedding gradient launch");
     }
     return BK_OK;
@@ -829,7 +823,7 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
             L.kind = BK_LINEAR;
             return weighted_grads_ws(&L, 1, dt, B);
         case BK_OP_EMBED_WEIGHTED_GRAD:
-            return embed_grad_ws_bytes(B, T, d);
+            return embed_grad_ws_bytes(B, T);
         default:
             return 0;
     }

@@ -61,8 +61,10 @@ def test_workspace_sizes():
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 3072, 3072) == 0
     # T not a multiple of 32 (the other 256 x 256 kernel): no tail split
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1000, 768, 768) == 0
-    assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) >= \
-        16 * 256 * 8 + 50257 * 4
+    # sorted keys (8 B per token), run ids (4 B per token), run starts (n + 2 ints), 256-byte aligned
+    n = 16 * 256
+    assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) == \
+        n * 8 + n * 4 + ((n + 2) * 4 + 255) // 256 * 256
     assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, 7, 1, 1, 1, 1) == 0        # bad dtype
     assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_F32, -1, 1, 1, 1) == 0
 

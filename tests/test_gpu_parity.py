@@ -185,6 +185,41 @@ def test_embed_weighted_grad_matches_oracle(bk, B, T, V, p, dtype):
     assert np.all(G[absent] == 0.0)
 
 
+# Runs of equal ids are staged 256 tokens at a time and added 8 at a time:
+# one id repeated over every token (a 1024-token run, four batches), short
+# runs with a ragged column chunk, and a Zipf mix; a zero clip weight; the
+# accumulating form adds exactly the written rows to G's old values.
+@pytest.mark.parametrize("B,T,V,p,dtype,kind", [
+    (4, 256, 300, 1000, torch.bfloat16, "one"),
+    (3, 100, 50, 72, torch.float32, "few"),
+    (2, 300, 2000, 256, torch.bfloat16, "zipf"),
+    (1, 1, 10, 5, torch.float32, "one"),
+])
+def test_embed_weighted_grad_runs(bk, B, T, V, p, dtype, kind):
+    gen = torch.Generator().manual_seed(B * T + p)
+    if kind == "one":
+        ids = torch.full((B, T), V // 3, dtype=torch.int64)
+    elif kind == "few":
+        ids = torch.randint(0, V, (B, T), generator=gen)
+    else:
+        ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.2, 7)).view(B, T)
+    g = torch.randn(B, T, p, generator=gen).to(dtype)
+    C = torch.rand(B, generator=gen) + 0.1
+    C[0] = 0.0
+    ref = oracle.embed_weighted_grad(ids, g, C, V)
+    ids_d, g_d, C_d = ids.to(DEV), g.to(DEV), C.to(DEV)
+    G = bk.bk_embed_weighted_grad(ids_d, g_d, C_d, V)
+    assert _frob(G.cpu().numpy(), ref) <= GRAD_TOL[dtype]
+    absent = np.setdiff1d(np.arange(V), ids.numpy().ravel())
+    assert np.all(G.cpu().numpy()[absent] == 0.0)
+    assert torch.equal(G, bk.bk_embed_weighted_grad(ids_d, g_d, C_d, V))
+    G0 = torch.randn(V, p, generator=gen).to(DEV)
+    Ga = G0.clone()
+    arr = bk.make_layers([{"kind": bk.BK_EMBEDDING, "x": ids_d, "g": g_d, "G": Ga, "V": V, "accumulate": True}])
+    bk.bk_weighted_grads(arr, 1, C_d, bk.BK_BF16 if dtype == torch.bfloat16 else bk.BK_F32, B)
+    assert torch.equal(Ga, G0 + G)
+
+
 @pytest.mark.parametrize("seed,tid,step,q0,nq", [
     (0, 0, 0, 0, 1000), (0xFFFFFFFFFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, 0, 64),
     (0x0123456789ABCDEF, 3, 11, (1 << 32) - 5, 300), (5, 144, 0, 123456789012, 77)])
