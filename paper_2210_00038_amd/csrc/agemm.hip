@@ -739,15 +739,20 @@ constexpr int kSG = 256 * 2 + 64;                // bytes per staged k-row (both
 constexpr int kGOp = kBK * kSG;                  // one operand of one stage
 constexpr int kGStage = 2 * kGOp;
 
-__global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args, int n_wg) {
+__global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args, int n_remap) {
     __shared__ __attribute__((aligned(16))) char lds[2 * kGStage];
 
-    const int wg = xcd_remap(blockIdx.x, n_wg);
+    // As agrad_dl_kernel: the first n_remap workgroups XCD-remapped, the
+    // tail of K slices in launch order.
+    const int wg = (int)blockIdx.x < n_remap ? xcd_remap(blockIdx.x, n_remap) : (int)blockIdx.x;
     const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
-    const int ks = max(L.ksplit, 1), local = wg - L.wg_begin;
-    const int tile = local / ks, slice = local - tile * ks;
+    const int local = wg - L.wg_begin, sf = L.split_from;
+    const int ks = local < sf ? 1 : max(L.ksplit, 1);
+    const int rel = local < sf ? 0 : (local - sf) / ks;              // split tile, from split_from
+    const int tile = local < sf ? local : sf + rel;
+    const int slice = local < sf ? 0 : (local - sf) - rel * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
@@ -920,7 +925,7 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     if (st < nst) stage(std::integral_constant<int, 0>{});
 
     if (ks > 1) {
-        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)tile * ks + slice) * (kGM * kGN),
+        store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)rel * ks + slice) * (kGM * kGN),
                                      acc, 128 * wm, 64 * wn, lane, 1.f);
         return;
     }
@@ -1351,7 +1356,8 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
     const bool vec = v != GemmVariant::Scalar;
     if (v == GemmVariant::Grad) {
         if (inst_norm) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(agrad_bf16_kernel, grid, dim3(512), 0, s, args, n_wg);
+        const int nr = n_remap > 0 && n_remap < n_wg ? n_remap : n_wg;
+        hipLaunchKernelGGL(agrad_bf16_kernel, grid, dim3(512), 0, s, args, nr);
         return hipGetLastError();
     }
     if (v == GemmVariant::GradDL) {

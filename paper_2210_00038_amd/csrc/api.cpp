@@ -436,7 +436,7 @@ struct GradPlan {
     int64_t tm, tn, ksplit, tile_elems;
     bool swap;
     int64_t split_from = 0;
-    bool tail = false;   // the K-split tiles are a GradDL launch's tail (plan_dl_tail)
+    bool tail = false;   // the K-split tiles are a launch's tail (plan_tail)
     int64_t tiles() const { return tm * tn; }
     int64_t split_tiles() const { return ksplit > 1 ? tm * tn - split_from : 0; }
     int64_t wgs() const { return split_from + (tm * tn - split_from) * ksplit; }
@@ -476,13 +476,13 @@ struct GradGroup { bk::GemmVariant v; std::vector<GradEntry> e; };
 constexpr int64_t kTailMinStages = 8;    // stages per slice of a split tail tile, at least
 constexpr int64_t kTailMaxSplit = 16;    // K slices per tail tile, at most
 
-// The GradDL kernel holds one workgroup per CU, so a launch of N tiles of
-// equal work runs in ceil(N / cus) rounds.  When the last round is at most
+// The 256 x 256 clipped-gradient kernels (Grad, GradDL) hold one workgroup
+// per CU, so a launch of N tiles of equal work runs in ceil(N / cus) rounds.  When the last round is at most
 // half full (r = N mod cus tiles), those r tiles are cut into s = cus / r K
 // slices each and moved behind every other tile in launch order: the slices
 // are dispatched last and fill the CUs together once the full rounds are
 // done.  They are taken from the layer with the most tiles, which goes last.
-void plan_dl_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) {
+void plan_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) {
     if (g.e.empty()) return;
     const int64_t T0 = layers[g.e[0].l].T;
     int64_t N = 0;
@@ -494,7 +494,7 @@ void plan_dl_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) 
     }
     const int64_t r = N % cus;
     if (r == 0 || 2 * r > cus || g.e[best].gp.tiles() < r) return;
-    const int64_t nst = cdiv(B * T0, bk::kDLStageRows);
+    const int64_t nst = cdiv(B * T0, g.v == bk::GemmVariant::GradDL ? bk::kDLStageRows : 64);
     const int64_t sp = std::min({cus / r, nst / kTailMinStages, kTailMaxSplit});
     if (sp < 2) return;
     std::rotate(g.e.begin() + (std::ptrdiff_t)best, g.e.begin() + (std::ptrdiff_t)best + 1, g.e.end());
@@ -521,9 +521,9 @@ std::vector<GradGroup> grad_groups(const bk_layer* layers, int64_t n, bool bf16,
     }
     int64_t cus = 0;
     for (GradGroup& g : out)
-        if (g.v == bk::GemmVariant::GradDL) {
+        if (g.v == bk::GemmVariant::GradDL || g.v == bk::GemmVariant::Grad) {
             if (cus == 0) cus = device_cus();
-            plan_dl_tail(g, layers, B, cus);
+            plan_tail(g, layers, B, cus);
         }
     return out;
 }
@@ -572,8 +572,8 @@ bk_status weighted_grads(const char* fn, const bk_layer* layers, int64_t n, cons
     const bool bf16 = dt == BK_BF16;
 
     // Grouped launches by kernel variant.  Layers with few output tiles run
-    // K-split (grad_plan), and so do the tiles of a GradDL launch's last,
-    // partly filled round (plan_dl_tail); the partial tiles sit in the
+    // K-split (grad_plan), and so do the tiles of a 256 x 256 launch's last,
+    // partly filled round (plan_tail); the partial tiles sit in the
     // workspace (launches follow each other on the stream, so each starts
     // from offset 0).
     for (const GradGroup& grp : grad_groups(layers, n, bf16, B)) {

@@ -57,9 +57,9 @@ struct GemmLayer {
     int32_t red_begin;
     int32_t swap;       // narrow kernels: the tile is G^T (rows along p, d < p)
     int32_t accum;      // clipped gradient: add to G instead of writing it
-    // GradDL: tiles below split_from run whole (one workgroup each), the
-    // tiles from it on in ksplit slices (their partial tiles and reduction
-    // workgroups counted from split_from); 0 everywhere else.
+    // Grad / GradDL: tiles below split_from run whole (one workgroup each),
+    // the tiles from it on in ksplit slices (their partial tiles and
+    // reduction workgroups counted from split_from); 0 everywhere else.
     int32_t split_from;
     int64_t ptile_off;  // first float of this layer's partial tiles
 };
@@ -199,7 +199,7 @@ struct PrepArgs {
 // ---- launchers (return the launch status) ----------------------------------
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
-// n_remap (GradDL): the first n_remap workgroups are dealt to the XCDs in
+// n_remap (Grad, GradDL): the first n_remap workgroups are dealt to the XCDs in
 // contiguous runs; the rest (a launch's tail) run in launch order.  0: all.
 hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm, GemmVariant v,
                        hipStream_t s, int n_remap = 0);

@@ -59,8 +59,11 @@ def test_workspace_sizes():
         16 * 16 * 256 * 256 * 4
     # 12 x 12 = 144 tiles, over half of 256: no split
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 3072, 3072) == 0
-    # T not a multiple of 32 (the other 256 x 256 kernel): no tail split
-    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1000, 768, 768) == 0
+    # T not a multiple of 32 (the register-staged 256 x 256 kernel, 64-row stages): split the same way
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1000, 768, 768) == \
+        9 * 16 * 256 * 256 * 4
+    # T < 64 (the wide kernel, two workgroups per CU): no tail split
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 48, 768, 768) == 0
     # sorted keys (8 B per token), run ids (4 B per token), run starts (n + 2 ints), 256-byte aligned
     n = 16 * 256
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) == \

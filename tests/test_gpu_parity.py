@@ -432,13 +432,17 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
 
 
-# A grouped launch of the LDS-DMA kernel (one workgroup per CU) whose last
+# A grouped launch of a 256 x 256 clipped-gradient kernel (one workgroup per
+# CU: the LDS-DMA kernel when 32 | T, else the register-staged one) whose last
 # round of tiles is under half full: those tiles run in K slices, dispatched
 # after every whole tile, and are summed in slice order.
 @pytest.mark.parametrize("shapes,B,T,zero", [
     ([(768, 4096)] * 6, 4, 512, [1]),         # 288 tiles: 32 split from the middle of a layer
     ([(512, 4096)] * 9, 4, 256, []),          # 288 tiles: one whole 32-tile layer split
     ([(768, 768)], 3, 256, [0]),              # 9 tiles, no whole round: all split
+    ([(768, 4096)] * 6, 4, 500, [2]),         # 32 does not divide T: the register-staged kernel
+    ([(768, 768)], 3, 1000, []),              # the same, all split
+    ([(768, 768)], 3, 200, []),               # too few stages per slice: not split
 ])
 def test_weighted_grads_tail_split(bk, shapes, B, T, zero):
     gen = torch.Generator().manual_seed(B * T + len(shapes))
@@ -454,8 +458,12 @@ def test_weighted_grads_tail_split(bk, shapes, B, T, zero):
     tiles = sum((d // 256) * (p // 256) for d, p in shapes)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     ws = bk.bk_weighted_grads_workspace_size(arr, n, bk.BK_BF16, B)
-    if tiles % cus and 2 * (tiles % cus) <= cus:
-        assert ws > 0                      # the tail is split
+    # the host's rule: the last round's r tiles in s = CUs / r slices (at most
+    # 16) of at least 8 stages (32 rows with 32 | T, else 64), when s >= 2
+    r = tiles % cus
+    nst = -(-B * T // (32 if T % 32 == 0 else 64))
+    split = r > 0 and 2 * r <= cus and min(cus // r, nst // 8, 16) >= 2
+    assert (ws > 0) == split
     Cd = C.to(DEV)
     bk.bk_weighted_grads(arr, n, Cd, bk.BK_BF16, B)
     first = [G.clone() for G in Gs]
