@@ -349,12 +349,6 @@ __device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float c) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
-// Logical tile of workgroup `wg` of `n` such that consecutive logical tiles
-// run on the same XCD (workgroups are dealt round-robin to the 8 XCDs).
-__device__ __forceinline__ int xcd_remap(int wg, int n) {
-    const int x = wg & 7, idx = wg >> 3, per = n >> 3, rem = n & 7;
-    return x * per + min(x, rem) + idx;
-}
 
 template <bool INST>
 __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args, int n_wg) {

@@ -118,6 +118,14 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Sum of one float per thread over a 256-thread workgroup; result valid in
 // thread 0.  `red` must hold 4 floats of LDS.
+// Logical index of workgroup `wg` of `n` such that consecutive logical
+// indices run on the same XCD (workgroups are dealt round-robin to the 8
+// XCDs, each with its own L2).
+__device__ __forceinline__ int xcd_remap(int wg, int n) {
+    const int x = wg & 7, idx = wg >> 3, per = n >> 3, rem = n & 7;
+    return x * per + min(x, rem) + idx;
+}
+
 // Descriptor of workgroup `wg` in a grouped launch: the last l < n with
 // begin(l) <= wg, begin(l) being descriptor l's first workgroup
 // (non-decreasing in l, begin(0) = 0).  Binary search: a handful of

@@ -342,7 +342,9 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     __shared__ float red[4];
     __shared__ float cbuf[VEC && !EMBED ? 2 * 4 * 128 : 1];   // column sums of the bias (gram_dl)
 
-    const int wg = blockIdx.x;
+    // Consecutive workgroups (the super-block pairs of one sample, which share
+    // row blocks) on one XCD, so that the repeated block reads hit its L2.
+    const int wg = xcd_remap(blockIdx.x, gridDim.x);
     const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GhostLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, nsb = L.nsb, npairs = L.npairs;
