@@ -277,3 +277,13 @@ def test_grouped_noise_validation():
         assert "NULL" in bk.bk_last_error()
         assert fn(ptrs, nel, tids, 0, 1.0, 0, 0, None) == bk.BK_OK
     assert bk.lib.bk_add_noise_grouped(ptrs, nel, tids, 1, 0.0, 0, 0, None) == bk.BK_OK
+
+
+def test_embedding_token_limit():
+    """An embedding layer's clipped gradient takes at most 8192 tokens per
+    call: one more is refused before any launch."""
+    arr = (bk.bk_layer * 1)()
+    arr[0].kind, arr[0].T, arr[0].d, arr[0].p = bk.BK_EMBEDDING, 8193, 100, 16
+    arr[0].x = arr[0].g = arr[0].G = 0x10000
+    st = bk.lib.bk_weighted_grads(arr, 1, FAKE, bk.BK_BF16, 1, FAKE, 1 << 30, None)
+    assert st != bk.BK_OK and "8192" in bk.bk_last_error()

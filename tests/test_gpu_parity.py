@@ -642,3 +642,29 @@ def test_conv_stack_matches_oracle(bk):
         G = Gs[l].cpu().numpy()
         assert _frob(G, ref["G"][l]) <= GRAD_TOL[dtype], l
         assert not np.any(G[ci * k * k:]), l                 # padded columns of a give zero rows
+
+
+# ------------------------------------------- limits
+def test_embed_weighted_grad_at_the_token_limit(bk):
+    """8192 tokens (the most one call takes): the sort fills its whole LDS
+    table and Zipf ids over a small vocabulary give long runs."""
+    B, T, V, p = 32, 256, 1000, 96
+    ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.1, 17)).view(B, T)
+    g = torch.randn(B, T, p, generator=torch.Generator().manual_seed(18)).to(torch.bfloat16)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(19)) + 0.1
+    ref = oracle.embed_weighted_grad(ids, g, C, V)
+    G = bk.bk_embed_weighted_grad(ids.to(DEV), g.to(DEV), C.to(DEV), V).cpu().numpy()
+    assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("B", [4096, 4097])
+def test_weighted_grad_largest_weight_table(bk, B):
+    """B = 4096 is the largest batch whose clip weights the LDS-DMA kernel
+    keeps in LDS (32 | T); one more sample takes the other kernels."""
+    T, d, p = 32, 256, 256
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(B)) + 0.1
+    C[::7] = 0.0
+    ref = oracle.weighted_grad(a, g, C)
+    G = bk.bk_weighted_grad(a.to(DEV), g.to(DEV), C.to(DEV)).cpu().numpy()
+    assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
