@@ -153,6 +153,9 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
             for (int j = 0; j < 4; ++j)
                 if (j < cnt[u]) patch[dst[u] + j] = v[u][j];
     }
+    // Offset table, element q of 16-byte chunk k at offs[q nch + k]: the
+    // lanes of a wave read consecutive words (no bank conflicts).
+    const int nch = ncols / VE;
     for (int col = tid; col < ncols; col += kUnfoldThreads) {
         const int gc = col0 + col;
         int off = -1;
@@ -161,12 +164,11 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
             const int i = rr / kw, j = rr - i * kw;
             off = ((c - c0) * kh + i) * Wp + j;
         }
-        offs[col] = off;
+        if (col < nch * VE) offs[(col % VE) * nch + col / VE] = off;   // the plan makes VE | ncols
     }
     __syncthreads();
 
     // output rows t = oh Wo + ow, columns col0 .. col0 + ncols, VE at a time
-    const int nch = ncols / VE;
     const int items = Wo * nch;
     int e = tid;
     int ow = e / nch, k = e - ow * nch;
@@ -177,7 +179,7 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
         const int base = ow * stride;
 #pragma unroll
         for (int q = 0; q < VE; ++q) {
-            const int o = offs[k * VE + q];
+            const int o = offs[q * nch + k];
             out.v[q] = patch[o < 0 ? zslot : o + base];
         }
         *reinterpret_cast<Vec16<E>*>(dst0 + (int64_t)ow * ld + k * VE) = out;
