@@ -177,9 +177,9 @@ struct UnfoldJob {
     const void* x;
     void* a;
     int C, H, W, kh, kw, stride, pad, Ho, Wo, ld;
-    int cc, ngroups, Wp, table_off;   // channels per group, groups, patch row length, table offset
+    int cc, ngroups, Wr, table_off;   // channels per group, groups, patch row stride, table offset
     int vw;                           // input elements per load (1, 2 or 4; W % vw == 0)
-    int pad_;
+    int sh;                           // first element of a patch row (sh + pad even, Wr = 2 mod 4)
 };
 struct TokensJob {
     const void* y;

@@ -39,10 +39,16 @@ struct Vec16 {
     E v[N];
 };
 
-// LDS layout: patch [cc][kh][Wp] of E, then one zero element, then (16-byte
-// aligned) the int offset table of the group's columns.
+// LDS layout: patch [cc][kh][Wr] of E, then one zero element, then (16-byte
+// aligned) the int offset table of the group's columns.  A patch row holds
+// the Wp = (Wo - 1) stride + kw input columns an output row reads, starting
+// at element sh of the row, with sh + pad even and the row stride Wr = 2
+// mod 4: image column 0 sits on a 2-element boundary, so the input rows are
+// copied two elements per store, and consecutive rows start an odd number of
+// 4-byte words apart (bf16), which keeps the rows a wave's gather reads on
+// different LDS banks.
 struct UnfoldPlan {
-    int cc = 0, ngroups = 0, Wp = 0;
+    int cc = 0, ngroups = 0, Wr = 0, sh = 0;
     int64_t table_off = 0, lds = 0;
 };
 
@@ -52,8 +58,12 @@ UnfoldPlan unfold_plan(const UnfoldShape& s, int es) {
     if (s.ld % ve != 0 || s.B > 65535 || s.Ho > 65535 || s.ld > INT32_MAX) return p;
     if (s.Wo * (s.ld / ve) > INT32_MAX) return p;          // items of one workgroup fit an int
     const int64_t Wp = (s.Wo - 1) * s.stride + s.kw;
+    // sh + pad even and Wr = 2 mod 4: rows start on 2-element boundaries
+    // and rows lie an odd number of 4-byte words apart (bf16), so that the
+    // rows a wave's gather reads fall on different banks
+    const int64_t sh = s.pad % 2, Wr = (Wp + sh + 1) / 4 * 4 + 2;
     const int64_t khkw = s.kh * s.kw, d = s.C * khkw;
-    const int64_t per_c = s.kh * Wp * es + khkw * 4;
+    const int64_t per_c = s.kh * Wr * es + khkw * 4;
     const int64_t fixed = (s.ld - d) * 4 + es + 16 + 16;
     const int64_t cap = (kUnfoldLds - fixed) / per_c;      // channels whose patch and table fit
     int64_t cc = cap;
@@ -65,11 +75,12 @@ UnfoldPlan unfold_plan(const UnfoldShape& s, int es) {
         if (cc > cap) cc -= ve;
     }
     cc = std::min<int64_t>(cc, s.C);
-    if (cc < 1 || cc * s.kh * Wp >= 65536) return p;
+    if (cc < 1 || cc * s.kh * Wr >= 65536) return p;
     p.cc = (int)cc;
     p.ngroups = (int)((s.C + cc - 1) / cc);
-    p.Wp = (int)Wp;
-    p.table_off = (cc * s.kh * Wp * es + es + 15) / 16 * 16;
+    p.Wr = (int)Wr;
+    p.sh = (int)sh;
+    p.table_off = (cc * s.kh * Wr * es + es + 15) / 16 * 16;
     const int64_t ncols_max = std::max<int64_t>(cc * khkw, s.ld - (s.C - 1) / cc * cc * khkw);
     p.lds = p.table_off + ncols_max * 4;
     if (p.lds > 64 * 1024) p.cc = 0;
@@ -94,6 +105,16 @@ __device__ __forceinline__ void load_vec(const E* src, E (&v)[4]) {
     for (int j = 0; j < N; ++j) v[j] = p.e[j];
 }
 
+// ... and in one store.
+template <typename E, int N>
+__device__ __forceinline__ void store_vec(E* dst, const E (&v)[4]) {
+    struct alignas(N * sizeof(E)) Pack { E e[N]; };
+    Pack p;
+#pragma unroll
+    for (int j = 0; j < N; ++j) p.e[j] = v[j];
+    *reinterpret_cast<Pack*>(dst) = p;
+}
+
 // One unfold workgroup: channel group g of output row oh of sample b.
 template <typename E>
 __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int oh, int g,
@@ -105,19 +126,21 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
     constexpr int VE = Vec16<E>::N;
     const int tid = threadIdx.x;
     const int kh = J.kh, kw = J.kw, khkw = kh * kw, stride = J.stride, pad = J.pad;
-    const int H = J.H, W = J.W, Wo = J.Wo, Wp = J.Wp, C = J.C, cc = J.cc;
+    const int H = J.H, W = J.W, Wo = J.Wo, Wr = J.Wr, sh = J.sh, C = J.C, cc = J.cc;
+    const int Wp = (Wo - 1) * stride + kw;          // input columns of an output row
     const int c0 = g * cc, cg = min(cc, C - c0);
     const int d = C * khkw, ld = J.ld;
     const int col0 = c0 * khkw;
     const int ncols = (c0 + cg == C) ? ld - col0 : cg * khkw;
-    const int zslot = cc * kh * Wp;
+    const int zslot = cc * kh * Wr;
 
-    // input rows (c, i) of this output row: the patch is zeroed, then the
-    // in-image part of each row (columns w < Wv of the input row, at patch
-    // column pad + w) is copied J.vw elements per load, walked flat over
-    // (row, vector) so every lane loads
-    const int nz = cc * kh * Wp + 1;
-    for (int e = tid; e < nz; e += kUnfoldThreads) patch[e] = E{};
+    // input rows (c, i) of this output row: the patch is zeroed (16 bytes per
+    // store, up to the table), then the in-image part of each row (columns
+    // w < Wv of the input row, at patch column pad + w of the row) is copied
+    // J.vw elements per load and per store, walked flat over (row, vector)
+    // so every lane loads
+    const int nz16 = J.table_off / 16;
+    for (int e = tid; e < nz16; e += kUnfoldThreads) reinterpret_cast<uint4*>(smem)[e] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
     const int vw = J.vw;
     const int Wv = min(W, Wp - pad);                  // image columns inside the patch row
@@ -143,15 +166,24 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
                     else if (vw == 2) load_vec<E, 2>(src, v[u]);
                     else v[u][0] = *src;
                     cnt[u] = min(vw, Wv - w0);
-                    dst[u] = r * Wp + pad + w0;
+                    dst[u] = r * Wr + sh + pad + w0;             // even when vw > 1
                 }
             }
         }
 #pragma unroll
-        for (int u = 0; u < kFillUnroll; ++u)
+        for (int u = 0; u < kFillUnroll; ++u) {
+            if (cnt[u] == 4 && vw == 4) {
+                const E lo[4] = {v[u][0], v[u][1]}, hi[4] = {v[u][2], v[u][3]};
+                store_vec<E, 2>(patch + dst[u], lo);
+                store_vec<E, 2>(patch + dst[u] + 2, hi);
+            } else if (cnt[u] == 2 && vw == 2) {
+                store_vec<E, 2>(patch + dst[u], v[u]);
+            } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (j < cnt[u]) patch[dst[u] + j] = v[u][j];
+                for (int j = 0; j < 4; ++j)
+                    if (j < cnt[u]) patch[dst[u] + j] = v[u][j];
+            }
+        }
     }
     // Offset table, element q of 16-byte chunk k at offs[q nch + k]: the
     // lanes of a wave read consecutive words (no bank conflicts).
@@ -162,7 +194,7 @@ __device__ __forceinline__ void unfold_block(const UnfoldJob& J, int64_t b, int 
         if (gc < d) {
             const int c = gc / khkw, rr = gc - c * khkw;
             const int i = rr / kw, j = rr - i * kw;
-            off = ((c - c0) * kh + i) * Wp + j;
+            off = ((c - c0) * kh + i) * Wr + sh + j;
         }
         if (col < nch * VE) offs[(col % VE) * nch + col / VE] = off;   // the plan makes VE | ncols
     }
@@ -337,7 +369,7 @@ hipError_t add_unfold(PrepBuilder& P, const void* x, void* a, const UnfoldShape&
     for (int cand : {4, 2})
         if (s.W % cand == 0 && reinterpret_cast<uintptr_t>(x) % (cand * sizeof(E)) == 0) { vw = cand; break; }
     J = UnfoldJob{x, a, (int)s.C, (int)s.H, (int)s.W, (int)s.kh, (int)s.kw, (int)s.stride, (int)s.pad,
-                  (int)s.Ho, (int)s.Wo, (int)s.ld, p.cc, p.ngroups, p.Wp, (int)p.table_off, vw, 0};
+                  (int)s.Ho, (int)s.Wo, (int)s.ld, p.cc, p.ngroups, p.Wr, (int)p.table_off, vw, p.sh};
     P.blocks += nblk;
     P.A.blk_end[P.A.nu++] = (int)P.blocks;
     P.lds = std::max<int>(P.lds, (int)p.lds);
