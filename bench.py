@@ -60,8 +60,10 @@ def algorithmic_work(w: wl.Workload, mixopt: bool = False):
         L = L0
         if L0.bias or L0.kind == "norm":
             # per-sample sums (App. notes on normalization layers; biases, Section 5):
-            # g (and xhat) read once, B p sums written and read back, p written
-            nin = 2 if L0.kind == "norm" else 1
+            # B p sums written and read back, p written; a normalization layer's
+            # g and xhat read once (a linear layer's g is already counted with
+            # its weight)
+            nin = 2 if L0.kind == "norm" else 0
             nsum = (1 if L0.bias else 0) + (1 if L0.kind == "norm" else 0)
             out["norm_bytes"] += B * L0.T * L0.p * es * nin + 4.0 * B * L0.p * nsum
             out["gemm_bytes"] += (4.0 * B * L0.p + 4.0 * L0.p) * nsum
