@@ -477,11 +477,13 @@ constexpr int64_t kTailMinStages = 8;    // stages per slice of a split tail til
 constexpr int64_t kTailMaxSplit = 16;    // K slices per tail tile, at most
 
 // The 256 x 256 clipped-gradient kernels (Grad, GradDL) hold one workgroup
-// per CU, so a launch of N tiles of equal work runs in ceil(N / cus) rounds.  When the last round is at most
-// half full (r = N mod cus tiles), those r tiles are cut into s = cus / r K
-// slices each and moved behind every other tile in launch order: the slices
-// are dispatched last and fill the CUs together once the full rounds are
-// done.  They are taken from the layer with the most tiles, which goes last.
+// per CU, so a launch of N tiles of equal work runs in ceil(N / cus) rounds.
+// When the last round is at most half full (r = N mod cus tiles), those r
+// tiles are cut into s = cus / r K slices each (at most kTailMaxSplit, of
+// at least kTailMinStages stages) and moved behind every other tile in
+// launch order: the slices are dispatched last and fill the CUs together
+// once the full rounds are done.  They are taken from the layer with the
+// most tiles, which goes last.
 void plan_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) {
     if (g.e.empty()) return;
     const int64_t T0 = layers[g.e[0].l].T;
