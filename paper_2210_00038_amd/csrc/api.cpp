@@ -280,6 +280,22 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
         a.n = (int32_t)v.size();
         a.B = (int32_t)B;
         a.part = part;
+        // One super-block pair per sample (T <= 128): no L2 reuse to keep on
+        // an XCD, and the workgroups' sizes differ by layer (rows of d + p
+        // values), so the layers go largest first and the hardware deals the
+        // grid round-robin over the XCDs: each XCD gets the same mix and the
+        // last round holds the small ones.  (A contiguous share per XCD in
+        // stack order left the XCDs up to ~20% apart in bytes.)
+        a.remap = 0;
+        for (const Item* it : v) a.remap |= it->np.npart > 1 ? 1 : 0;
+        if (!a.remap)
+            std::stable_sort(v.begin(), v.end(), [&](const Item* x, const Item* y) {
+                auto cost = [&](const Item* it) {
+                    const bk_layer& L = layers[it->l];
+                    return (embed ? 0 : L.d) + L.p;
+                };
+                return cost(x) > cost(y);
+            });
         int64_t wg = 0;
         for (size_t k = 0; k < v.size(); ++k) {
             const bk_layer& L = layers[v[k]->l];
@@ -764,6 +780,7 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         bk::GhostArgs a{};
         a.n = 1;
         a.B = (int32_t)B;
+        a.remap = np.npart > 1 ? 1 : 0;
         a.part = part;
         bk::GhostLayer& g = a.L[0];
         g.x = L.x;

@@ -34,6 +34,7 @@ struct GhostLayer {
 constexpr int kMaxGhost = 64;
 struct GhostArgs {
     int32_t n, B;
+    int32_t remap;      // 1: workgroup order remapped per XCD (xcd_remap)
     float* part;        // partial sums, [layer][sample][pair]
     GhostLayer L[kMaxGhost];
 };

@@ -344,7 +344,9 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
 
     // Consecutive workgroups (the super-block pairs of one sample, which share
     // row blocks) on one XCD, so that the repeated block reads hit its L2.
-    const int wg = xcd_remap(blockIdx.x, gridDim.x);
+    // With one pair per sample nothing is shared: the grid runs in launch
+    // order, which the host sets largest workgroups first.
+    const int wg = args.remap ? xcd_remap(blockIdx.x, gridDim.x) : (int)blockIdx.x;
     const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
     const GhostLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, nsb = L.nsb, npairs = L.npairs;
