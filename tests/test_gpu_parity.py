@@ -281,6 +281,26 @@ def _run_stack(bk, layers, ins, B, dtype, mode, R, gamma, std, seed, mixopt=Fals
     return norm_sq.cpu().numpy(), C.cpu().numpy(), tot.cpu().numpy(), [G.cpu().numpy() for G in Gs]
 
 
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_ghost_launch_reordered_by_size(bk, dtype):
+    """Ghost layers at T <= 128 (one super-block pair per sample) share a
+    launch whose layers the host orders by d + p, largest first; here the
+    stack order (160, 224, 360, 152) differs from it.  Every layer's norms
+    and clipped gradient must still be its own."""
+    Lr = wl.Layer
+    layers = [Lr("linear", 48, 64, 96), Lr("linear", 48, 96, 128),
+              Lr("linear", 48, 160, 200), Lr("linear", 48, 80, 72)]
+    B = 5
+    ins = _stack_inputs(layers, B, dtype, seed=31)
+    norms, C, tot, G = _run_stack(bk, layers, ins, B, dtype, 1, 1.0, 0.01, 0.0, seed=3)
+    ref = oracle.bk_stack(layers, ins, "auto", 1.0, 0.01, 0.0, seed=3, with_noise=False)
+    assert ref["paths"] == ["ghost"] * 4
+    for l in range(len(layers)):
+        assert _rel(norms[l], ref["norms"][l]) <= NORM_TOL[dtype], l
+        assert _frob(G[l], ref["G"][l]) <= GRAD_TOL[dtype], l
+    assert _rel(C, ref["C"]) <= NORM_TOL[dtype]
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_private_grad_stack_matches_oracle(bk, dtype):
     """Whole path on a small mixed stack: ghost, instantiated and embedding layers."""
