@@ -18,8 +18,9 @@ workload on the host.
 
     python bench.py [--steps K] [--warmup W] [--workload N] [--mixopt] [--gpus 1]
 
-Defaults: 50 timed steps after untimed warm-up steps that fill 100 ms of GPU
-time (the reported `warmup` is their count).
+Defaults: 50 timed steps.  Before them a ramp of untimed steps fills 100 ms of
+GPU time (reported as `warmup_ramp`), then --warmup more untimed steps run
+(reported as `warmup`, default 0).
 """
 from __future__ import annotations
 
@@ -132,10 +133,16 @@ def _cpu_model() -> str:
 
 
 def _oracle_pass(w: wl.Workload, budget_s: float):
-    """The float64 oracle on the first layers of the stack (all B samples)
-    until ~budget_s of work; returns (seconds, gradient flops done, layers)."""
+    """The float64 oracle on a prefix of the stack (all B samples), in the
+    order of Algorithm 1: the per-sample norms of every layer of the prefix,
+    their sum over those layers and one clip factor per sample, then each
+    layer's clipped gradient and its noise with those factors.  The prefix
+    grows layer by layer while the norm pass stays under a third of budget_s
+    (the gradients cost about twice the norms).  Returns (seconds, flops of
+    both passes done, layers)."""
     import oracle
-    done, t_used, nl = 0.0, 0.0, 0
+    t_norm, nl, done = 0.0, 0, 0.0
+    inputs, norms = [], []
     for l, L in enumerate(w.layers):
         x, g = wl.draw_layer(w, l)
         t0 = time.perf_counter()
@@ -143,8 +150,16 @@ def _oracle_pass(w: wl.Workload, budget_s: float):
         if kind == "conv":
             cin, k, stride, pad, _ = L.conv
             x, g, kind = oracle.unfold(x, k, k, stride, pad, L.d), oracle.tokens_from_nchw(g), "linear"
-        n = oracle.bk_layer_norm(kind, x, g, L.d, L.bias)
-        C = oracle.clip_factors(n, w.clip, w.R, w.gamma)
+        norms.append(oracle.bk_layer_norm(kind, x, g, L.d, L.bias))
+        t_norm += time.perf_counter() - t0
+        inputs.append((kind, x, g))
+        done += layer_flops(w, L)
+        nl += 1
+        if t_norm >= budget_s / 3:
+            break
+    t0 = time.perf_counter()
+    C = oracle.clip_factors(oracle.aggregate(np.stack(norms)), w.clip, w.R, w.gamma)
+    for l, (L, (kind, x, g)) in enumerate(zip(w.layers, inputs)):
         if kind == "embed":
             G = oracle.embed_weighted_grad(x, g, C, L.d)
         elif kind == "norm":
@@ -155,29 +170,38 @@ def _oracle_pass(w: wl.Workload, budget_s: float):
         if L.bias:
             oracle.add_noise(oracle.weighted_sum(oracle.bias_sums(g), C), w.noise_std, w.wid,
                              oracle.BIAS_TENSOR | l, 0)
-        t_used += time.perf_counter() - t0
-        done += 2.0 * w.B * L.T * L.p * true_d(L) if L.kind != "norm" else 0.0
-        nl += 1
-        if t_used >= budget_s:
-            break
-    return t_used, done, nl
+    return t_norm + time.perf_counter() - t0, done, nl
+
+
+def layer_flops(w: wl.Workload, L: wl.Layer) -> float:
+    """The oracle's float64 flops for one layer: its norm by the definition
+    (the d x p per-sample gradients, 2BTdp) plus its clipped gradient (2BTdp);
+    an embedding's row sums (2BTp each) and an affine layer's per-sample sums
+    are counted the same way."""
+    if L.kind == "norm":
+        return 4.0 * w.B * L.T * L.p
+    if L.kind == "embed":
+        return 4.0 * w.B * L.T * L.p
+    return 4.0 * w.B * L.T * L.p * true_d(L)
 
 
 def cpu_baseline(w: wl.Workload, budget_s: float = 12.0, single_budget_s: float = 6.0):
     """The float64 oracle on the host with its BLAS on every thread it is
-    given, then again on one thread; each pass covers the first layers of the
-    stack (all B samples, input generation excluded) for ~its budget of work
-    and is scaled to the whole stack by the fraction of its gradient flops."""
+    given, then again on one thread; each pass runs Algorithm 1 (norms, clip
+    factors, clipped gradients, noise) over a prefix of the stack (all B
+    samples, input generation excluded) for ~its budget of work and is scaled
+    to the whole stack by the fraction of the oracle's flops it covered."""
     from threadpoolctl import threadpool_info, threadpool_limits
     cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    total = algorithmic_work(w)["gemm_flops"] + 1e-9
+    total = sum(layer_flops(w, L) for L in w.layers) + 1e-9
     t_used, done, nl = _oracle_pass(w, budget_s)
     with threadpool_limits(limits=1):
         t1, done1, nl1 = _oracle_pass(w, single_budget_s)
     t_full, t_full1 = t_used * total / done, t1 * total / done1
     return {"value": w.B / t_full, "unit": "samples/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {nl} of {len(w.layers)} layers, all {w.B} samples, full path in float64 "
-                      f"({t_used:.1f} s), scaled by gradient flops to the whole stack",
+            "sample": f"first {nl} of {len(w.layers)} layers, all {w.B} samples, Algorithm 1 in float64 "
+                      f"(norms, clip factors, clipped gradients, noise; {t_used:.1f} s), scaled by the "
+                      f"oracle's flops to the whole stack",
             "s_per_step": round(t_full, 3),
             "single_thread": {"value": w.B / t_full1, "s_per_step": round(t_full1, 3), "cores": 1,
                               "sample": f"first {nl1} layers ({t1:.1f} s), scaled the same way"},
@@ -303,9 +327,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed steps first; default: as many as fill %d ms of GPU time (at least 3)"
-                         % WARMUP_MS)
+    ap.add_argument("--warmup", type=int, default=0,
+                    help="untimed steps after the warm-up ramp (untimed steps filling %d ms of GPU "
+                         "time, at least 3, which always runs)" % WARMUP_MS)
     ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-plain-gemm", action="store_true",
@@ -399,19 +423,22 @@ def main():
                   "bk_add_noise_grouped")
         t()
 
-    if args.warmup >= 0:
-        for _ in range(args.warmup):
-            step()
-    else:
-        # From idle the clipped-gradient GEMM needs some 20-25 ms of this
-        # load before it runs at its steady speed (up to 30% slower before),
-        # whatever the step length: warm up by time.
-        args.warmup, t_w = 0, time.perf_counter()
-        while args.warmup < 3 or time.perf_counter() - t_w < WARMUP_MS * 1e-3:
-            step()
-            args.warmup += 1
-            if args.warmup % 8 == 0 or args.warmup < 3:
-                torch.cuda.synchronize()
+    # From idle the clipped-gradient GEMM needs some 20-25 ms of this load
+    # before it runs at its steady speed (up to 30% slower before), whatever
+    # the step length: a ramp of untimed steps filling WARMUP_MS of GPU time
+    # always runs first, then the requested count of warm-up steps (default:
+    # none beyond the ramp).
+    ramp, t_w = 0, time.perf_counter()
+    while ramp < 3 or time.perf_counter() - t_w < WARMUP_MS * 1e-3:
+        step()
+        ramp += 1
+        if ramp % 8 == 0 or ramp < 3:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    ramp_ms = (time.perf_counter() - t_w) * 1e3
+    args.warmup = max(0, args.warmup)
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
     evs = [[] for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -489,7 +516,8 @@ def main():
             v[k] = round(float(v[k]), 4)
     res = {
         "metric": METRIC, "value": K * B / (ms_step / 1e3), "unit": "samples/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "steps": args.steps, "warmup": args.warmup, "warmup_ramp": {"steps": ramp, "ms": round(ramp_ms, 1)},
+        "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "variant": "BK-MixOpt" if args.mixopt else "BK",
                    "accumulate": K, "logical_batch": K * B,
