@@ -324,6 +324,28 @@ bk_status bk_private_grad(const bk_layer* layers, int64_t n, bk_dtype dt, int64_
                           uint32_t step, float* norm_sq, float* C, float* total_sq, void* ws,
                           size_t ws_bytes, void* stream);
 
+/* Allocation-free form of bk_private_grad, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments and results as
+ * bk_private_grad, without the workspace: a device array of
+ * BK_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * (from the first call on that GPU until the process ends) stands in for it.
+ *  - Returns BK_ERR_NOT_SUPPORTED, doing no work, when
+ *    bk_private_grad_workspace_size of the stack exceeds that size (stacks
+ *    whose instantiated layers split into many K slices, for instance).
+ *  - The stream must belong to the current device (BK_ERR_INVALID_VALUE
+ *    otherwise).
+ *  - The call allocates and frees nothing and issues no memset.
+ *  - Every call on one GPU uses that GPU's one array, which keeps the last
+ *    call's contents (each call writes every word it reads first): calls
+ *    that overlap on one GPU (other streams, other threads) race, so the
+ *    caller must order them, e.g. on one stream. */
+#define BK_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+bk_status bk_private_grad_noalloc(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
+                                  bk_clip mode, float R, float gamma, float noise_std, uint64_t seed,
+                                  uint32_t step, float* norm_sq, float* C, float* total_sq,
+                                  void* stream);
+
 /* Diagnostics. */
 const char* bk_status_string(bk_status s);
 const char* bk_last_error(void);

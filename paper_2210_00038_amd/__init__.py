@@ -29,7 +29,8 @@ __all__ = [
     "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv",
     "bk_conv_prep", "make_convs",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
-    "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad", "make_layers",
+    "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad",
+    "bk_private_grad_noalloc", "BK_NOALLOC_SCRATCH_BYTES", "make_layers",
     "conv_out_size",
     "bk_layer_norms_workspace_size", "bk_weighted_grads_workspace_size",
     "bk_private_grad_workspace_size", "bk_status_string", "bk_last_error", "bk_version",
@@ -41,6 +42,7 @@ BK_CLIP_ABADI, BK_CLIP_AUTO = 0, 1
 BK_LINEAR, BK_EMBEDDING, BK_NORM_AFFINE = 0, 1, 2
 BK_LAYER_MIXOPT, BK_LAYER_BIAS, BK_LAYER_ACCUMULATE = 1, 2, 4
 BK_BIAS_TENSOR = 0x80000000
+BK_NOALLOC_SCRATCH_BYTES = 64 << 20
 (BK_OP_GHOST_NORM, BK_OP_INST_NORM, BK_OP_EMBED_GHOST_NORM, BK_OP_WEIGHTED_GRAD,
  BK_OP_EMBED_WEIGHTED_GRAD) = range(5)
 
@@ -52,7 +54,8 @@ EXPORTS = (
     "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv_prep",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
     "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
-    "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_status_string",
+    "bk_weighted_grads", "bk_private_grad_workspace_size", "bk_private_grad", "bk_private_grad_noalloc",
+    "bk_status_string",
     "bk_last_error", "bk_version",
 )
 
@@ -113,6 +116,8 @@ _SIG = {
     "bk_private_grad_workspace_size": (_sz, [_P, _i64, ctypes.c_int, _i64]),
     "bk_private_grad": (_st, [_P, _i64, ctypes.c_int, _i64, ctypes.c_int, _f32, _f32, _f32, _u64, _u32,
                               _vp, _vp, _vp, _vp, _sz, _vp]),
+    "bk_private_grad_noalloc": (_st, [_P, _i64, ctypes.c_int, _i64, ctypes.c_int, _f32, _f32, _f32, _u64,
+                                      _u32, _vp, _vp, _vp, _vp]),
     "bk_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "bk_last_error": (ctypes.c_char_p, []),
     "bk_version": (ctypes.c_char_p, []),
@@ -470,6 +475,15 @@ def bk_weighted_grads(layers, n: int, C, dtype: int, B: int, ws=None, device="cu
     ws, nws = _workspace(bk_weighted_grads_workspace_size(layers, n, dtype, B), device, ws)
     _check(lib.bk_weighted_grads(layers, n, _ptr(C), dtype, B, _ptr(ws), nws, _stream(stream)),
            "bk_weighted_grads")
+
+
+def bk_private_grad_noalloc(layers, n: int, dtype: int, B: int, mode: int, R: float, gamma: float,
+                            noise_std: float, seed: int, step: int, norm_sq, C, total_sq=None, stream=None):
+    """bk_private_grad with the library's own per-GPU scratch array instead of
+    a workspace (nothing is allocated; calls on one GPU must not overlap)."""
+    _check(lib.bk_private_grad_noalloc(layers, n, dtype, B, mode, R, gamma, noise_std, seed, step,
+                                       _ptr(norm_sq), _ptr(C), _ptr(total_sq), _stream(stream)),
+           "bk_private_grad_noalloc")
 
 
 def bk_private_grad(layers, n: int, dtype: int, B: int, mode: int, R: float, gamma: float,

@@ -34,6 +34,23 @@ bk_status hip_fail(hipError_t e, const char* what) {
     return BK_ERR_LAUNCH;
 }
 
+}  // namespace
+
+namespace bk {
+bk_status host_fail(bk_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+bk_status host_hip_fail(hipError_t e, const char* what) { return hip_fail(e, what); }
+}  // namespace bk
+
+namespace {
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 

@@ -9,6 +9,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "bk.h"
+
 #include <algorithm>
 
 namespace bk {
@@ -253,5 +255,11 @@ struct AffineArgs {
     AffineLayer L[kMaxAffine];
 };
 hipError_t launch_affine(const AffineArgs& args, int n_wg, bool bf16, hipStream_t s);
+
+// Host-side error reporting of the C ABI: record the detail that
+// bk_last_error() returns on this thread and return the status
+// (host_hip_fail: BK_ERR_LAUNCH with the HIP error text).
+bk_status host_fail(bk_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+bk_status host_hip_fail(hipError_t e, const char* what);
 
 }  // namespace bk

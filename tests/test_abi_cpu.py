@@ -287,3 +287,20 @@ def test_embedding_token_limit():
     arr[0].x = arr[0].g = arr[0].G = 0x10000
     st = bk.lib.bk_weighted_grads(arr, 1, FAKE, bk.BK_BF16, 1, FAKE, 1 << 30, None)
     assert st != bk.BK_OK and "8192" in bk.bk_last_error()
+
+
+def test_noalloc_rejects_stacks_beyond_its_scratch():
+    """The allocation-free call refuses, before any HIP call, a stack whose
+    workspace exceeds its fixed scratch (here the ResNet-18 convolutions,
+    whose instantiated early layers split into many K slices)."""
+    import workloads as wl
+    w = wl.get(6)
+    arr = (bk.bk_layer * len(w.layers))()
+    for c, L in zip(arr, w.layers):
+        c.kind, c.T, c.d, c.p = bk.BK_LINEAR, L.T, L.d, L.p
+        c.x = c.g = c.G = 0x10000
+    n = len(w.layers)
+    assert bk.bk_private_grad_workspace_size(arr, n, bk.BK_BF16, w.B) > bk.BK_NOALLOC_SCRATCH_BYTES
+    st = bk.lib.bk_private_grad_noalloc(arr, n, bk.BK_BF16, w.B, bk.BK_CLIP_AUTO, 1.0, 0.01, 1.0, 0, 0,
+                                        FAKE, FAKE, None, None)
+    assert st == bk.BK_ERR_NOT_SUPPORTED and "scratch" in bk.bk_last_error()
