@@ -953,26 +953,6 @@ __device__ __forceinline__ uint2 frag_dl_half(const char* lds, int kb, int cb, i
     return lds_tr16(lds + row * kDRow + dswz(row, col >> 3) * 16 + (col & 7) * 2);
 }
 
-// LDS DMA of 16 bytes per lane (as buffer_load16_lds), issued from inline
-// assembly.  The compiler treats the LDS transpose reads as possibly reading
-// any LDS DMA destination and would wait for every DMA in flight before each
-// of them, which serialises the prefetch; hidden in assembly, the DMA is not
-// tracked, and the kernel waits for it itself (vmcnt) before the barrier that
-// publishes a stage.  rs: buffer descriptor words (base, base high, bytes,
-// flags); m0 takes the wave-uniform LDS destination.
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    return (u32x4_t){(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, bytes, 0x00020000u};
-}
-
-__device__ __forceinline__ void dma16_asm(const u32x4_t& rs, uint32_t off, char* lds_dst) {
-    const uint32_t m0v = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_dst;
-    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :: "v"(off), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(m0v)) : "memory", "m0");
-}
-
 // Position of a stage in the batch: its sample and its stage within the
 // sample (spt stages per sample), advanced one stage at a time.
 struct StagePos {

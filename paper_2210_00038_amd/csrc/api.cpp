@@ -92,7 +92,8 @@ struct NormPlan {
     Path path;
     int64_t nwg;        // workgroups of the norm kernel
     int64_t npart;      // partials per sample
-    int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads;
+    int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads,
+                        // 2 = whole-sample kernel (bf16, 128 < T <= 256);
                         // instantiation: bk::GemmVariant
     int64_t tiles = 0;  // instantiation: output tiles per sample
     int64_t ksplit = 1; // instantiation: K slices per tile (wide and narrow kernels)
@@ -152,6 +153,13 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
         const int64_t K = np.path == Path::Embed ? L.p : std::max(L.d, L.p);
         const bool fits = (L.T + bk::kSuper) * K * (int64_t)es < ((int64_t)1 << 31);
         np.var = (xv && fits && aligned16(L.g) && (L.p * es) % 16 == 0) ? 1 : 0;
+        // 128 < T <= 256 on bf16 16-byte rows: the whole-sample kernel, which
+        // streams every row once (one partial per sample)
+        if (np.var == 1 && np.path == Path::Ghost && dt == BK_BF16 && L.T > bk::kSuper &&
+            L.T <= 2 * bk::kSuper) {
+            np.var = 2;
+            np.npart = 1;
+        }
     }
 }
 
@@ -179,6 +187,13 @@ size_t norm_tile_floats(const NormPlan& np, int64_t B) {
 size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
     return align_up(norm_part_floats(np, B) * sizeof(float)) + norm_tile_floats(np, B) * sizeof(float);
 }
+
+// Launch of a ghost-norm variant (NormPlan::var) and the super-block count
+// its descriptors carry.
+hipError_t launch_ghost_var(const bk::GhostArgs& a, int n_wg, bool bf16, bool embed, int var, hipStream_t s) {
+    return var == 2 ? bk::launch_ghost_full(a, n_wg, s) : bk::launch_ghost(a, n_wg, bf16, embed, var == 1, s);
+}
+int32_t ghost_nsb(int64_t T, int var) { return (int32_t)cdiv(T, var == 2 ? bk::kFullSub : bk::kSuper); }
 
 NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
@@ -291,7 +306,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     }
     float* tiles = part + off;
 
-    auto flush_ghost = [&](std::vector<const Item*>& v, bool embed, bool vec) -> bk_status {
+    auto flush_ghost = [&](std::vector<const Item*>& v, bool embed, int var) -> bk_status {
         if (v.empty()) return BK_OK;
         bk::GhostArgs a{};
         a.n = (int32_t)v.size();
@@ -322,7 +337,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             g.T = (int32_t)L.T;
             g.d = (int32_t)L.d;
             g.p = (int32_t)L.p;
-            g.nsb = (int32_t)cdiv(L.T, bk::kSuper);
+            g.nsb = ghost_nsb(L.T, var);
             g.npairs = (int32_t)v[k]->np.npart;
             g.wg_begin = (int32_t)wg;
             g.part_off = (int32_t)v[k]->part_off;
@@ -330,7 +345,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
             wg += v[k]->np.nwg;
         }
         if (wg > INT32_MAX) return fail(BK_ERR_NOT_SUPPORTED, "%s: grid too large", fn);
-        hipError_t e = bk::launch_ghost(a, (int)wg, bf16, embed, vec, s);
+        hipError_t e = launch_ghost_var(a, (int)wg, bf16, embed, var, s);
         v.clear();
         return e == hipSuccess ? BK_OK : hip_fail(e, "ghost norm launch");
     };
@@ -373,22 +388,23 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
         return e == hipSuccess ? BK_OK : hip_fail(e, "instantiated norm launch");
     };
 
-    // Group by (path, kernel variant), preserving layer order inside a group.
+    // Group by (path, kernel variant), preserving layer order inside a group;
+    // a group larger than one launch's descriptor table is cut into launches
+    // of near-equal layer counts (no small last launch).
     for (int kind = 0; kind < 3; ++kind)
-        for (int var = 0; var < (kind == 2 ? bk::kGemmVariants : 2); ++var) {
-            std::vector<const Item*> batch;
-            for (const Item& it : items) {
-                const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
-                if (it.np.path != want || it.np.var != var || it.np.nwg == 0) continue;
-                batch.push_back(&it);
-                const size_t cap = kind == 2 ? bk::kMaxGemm : bk::kMaxGhost;
-                if (batch.size() == cap) {
-                    st = kind == 2 ? flush_inst(batch, var) : flush_ghost(batch, kind == 1, var == 1);
-                    if (st != BK_OK) return st;
-                }
+        for (int var = 0; var < (kind == 2 ? bk::kGemmVariants : 3); ++var) {
+            const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
+            std::vector<const Item*> all;
+            for (const Item& it : items)
+                if (it.np.path == want && it.np.var == var && it.np.nwg > 0) all.push_back(&it);
+            const size_t cap = kind == 2 ? bk::kMaxGemm : bk::kMaxGhost;
+            const size_t nb = (all.size() + cap - 1) / cap;
+            for (size_t b = 0; b < nb; ++b) {
+                std::vector<const Item*> batch(all.begin() + (std::ptrdiff_t)(all.size() * b / nb),
+                                               all.begin() + (std::ptrdiff_t)(all.size() * (b + 1) / nb));
+                st = kind == 2 ? flush_inst(batch, var) : flush_ghost(batch, kind == 1, var);
+                if (st != BK_OK) return st;
             }
-            st = kind == 2 ? flush_inst(batch, var) : flush_ghost(batch, kind == 1, var == 1);
-            if (st != BK_OK) return st;
         }
 
     // Per-sample bias / affine sums of the layers that have them (their
@@ -805,9 +821,9 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
         g.T = (int32_t)L.T;
         g.d = (int32_t)L.d;
         g.p = (int32_t)L.p;
-        g.nsb = (int32_t)cdiv(L.T, bk::kSuper);
+        g.nsb = ghost_nsb(L.T, np.var);
         g.npairs = (int32_t)np.npart;
-        e = bk::launch_ghost(a, (int)np.nwg, dt == BK_BF16, want == Path::Embed, np.var == 1, s);
+        e = launch_ghost_var(a, (int)np.nwg, dt == BK_BF16, want == Path::Embed, np.var, s);
     }
     if (e != hipSuccess) return hip_fail(e, "norm launch");
     bk::ReduceArgs r{};

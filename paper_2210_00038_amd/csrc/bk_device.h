@@ -107,6 +107,26 @@ __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, uint
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_dst, 16, off, 0, 0, 0);
 }
 
+// LDS DMA of 16 bytes per lane (as buffer_load16_lds), issued from inline
+// assembly.  The compiler treats LDS reads as possibly reading any LDS DMA
+// destination and would wait for every DMA in flight before each of them,
+// which serialises a prefetch ring; hidden in assembly, the DMA is not
+// tracked, and the kernel waits for it itself (wait_vmcnt) before the barrier
+// that publishes a stage.  rs: buffer descriptor words (base, base high, bytes,
+// flags); m0 takes the wave-uniform LDS destination.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return (u32x4_t){(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, bytes, 0x00020000u};
+}
+
+__device__ __forceinline__ void dma16_asm(const u32x4_t& rs, uint32_t off, char* lds_dst) {
+    const uint32_t m0v = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_dst;
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :: "v"(off), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(m0v)) : "memory", "m0");
+}
+
 // ---------------------------------------------------------------------------
 // Reductions in a fixed order (deterministic).
 // ---------------------------------------------------------------------------

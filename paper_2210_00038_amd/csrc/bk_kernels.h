@@ -200,6 +200,11 @@ struct PrepArgs {
 };
 
 // ---- launchers (return the launch status) ----------------------------------
+// Whole-sample ghost norm (bf16, 16-byte rows, kSuper < T <= 2 kSuper): one
+// 512-thread workgroup per (layer, sample), GhostLayer::nsb = ceil(T / 32)
+// (5 .. 8), one partial per sample.
+constexpr int kFullSub = 32;
+hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, hipStream_t s);
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
 // n_remap (Grad, GradDL): the first n_remap workgroups are dealt to the XCDs in

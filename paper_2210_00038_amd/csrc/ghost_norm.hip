@@ -333,6 +333,223 @@ __device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Whole-sample ghost norm for 128 < T <= 256 (bf16, 16-byte rows).  With
+// 128-row super-block pairs every row block of such a sample is streamed
+// twice (pairs (0,0), (0,1), (1,1)), and the second read mostly comes from
+// HBM again.  Here one 512-thread workgroup owns one (layer, sample): the
+// rows of a_i and then of g_i pass through a 128 KB LDS ring once, in chunks
+// of 256 rows x 128 bytes (rows >= T load zeros), three chunks in flight,
+// one continuous stream over a's chunks and then g's.  The T x T Grams are
+// cut into NSUB = ceil(T / 32) blocks of 32 rows; the NSUB (NSUB + 1) / 2
+// upper-triangle 32 x 32 sub-tiles (row-major order) are dealt to the 8 waves
+// in contiguous runs, the first NT mod 8 waves taking one more, which puts
+// the same number of sub-tiles on each SIMD for NSUB = 7, 8 (waves w and
+// w + 4 share a SIMD).  Each wave keeps both Grams of its sub-tiles in
+// registers and reads each 32-row fragment its sub-tiles need once per k
+// step.  Off-diagonal sub-tiles count twice.  One partial per sample.
+// ---------------------------------------------------------------------------
+constexpr int kFullThreads = 512;
+constexpr int kFullRows = 256;                   // rows per chunk (T padded to 256)
+constexpr int kFullCW = 128;                     // bytes of each row per chunk
+constexpr int kFullSlot = kFullRows * kFullCW;   // 32 KB per chunk
+constexpr int kFullSlots = 4;                    // the ring: 128 KB
+constexpr int kFullLPW = kFullSlot / 1024 / 8;   // 1 KB LDS-DMA loads per wave per chunk
+
+template <int NSUB>
+struct FullTiles {
+    static constexpr int NT = NSUB * (NSUB + 1) / 2;
+    static constexpr int BASE = NT / 8, REM = NT % 8;
+    static constexpr int count(int w) { return BASE + (w < REM ? 1 : 0); }
+    static constexpr int start(int w) { return w * BASE + (w < REM ? w : REM); }
+    // row / column block of sub-tile q in row-major upper-triangle order
+    static constexpr int row(int q) {
+        int i = 0;
+        while (q >= NSUB - i) { q -= NSUB - i; ++i; }
+        return i;
+    }
+    static constexpr int col(int q) {
+        int i = 0;
+        while (q >= NSUB - i) { q -= NSUB - i; ++i; }
+        return i + q;
+    }
+    // bit b set: the wave's sub-tiles use 32-row block b
+    static constexpr unsigned used(int w) {
+        unsigned m = 0;
+        for (int q = start(w); q < start(w) + count(w); ++q) m |= (1u << row(q)) | (1u << col(q));
+        return m;
+    }
+};
+
+// 16-byte column c of row r of a chunk sits at column c ^ (r / 2 mod 8): the
+// 16 rows read by 16 lanes then meet 16 different 16-byte bank groups.
+__device__ __forceinline__ int full_swz(int row, int c) { return c ^ ((row >> 1) & 7); }
+
+// Rows of a_i / g_i of one sample and the LDS-DMA addressing of this wave.
+struct FullStream {
+    u32x4_t ra, rg;                  // resources over the sample's T rows (zeros beyond)
+    uint32_t ba[kFullLPW], bg[kFullLPW];   // byte offset of each load's lane within a chunk column
+    int lcol[kFullLPW];              // 16-byte chunk column each load's lane fetches
+    int Ka, Kg, nca, ncg;            // row lengths (elements) and chunks of a and g
+};
+
+// Queue chunk v of the stream (a's chunks first, then g's) into its ring
+// slot.  Chunks past the end load zeros, so every call issues the same
+// number of loads.
+__device__ __forceinline__ void full_issue(const FullStream& fs, int v, char* ring, int wave) {
+    char* slot = ring + (v % kFullSlots) * kFullSlot;
+    const bool isa = v < fs.nca;
+    const int ch = isa ? v : v - fs.nca;
+    const int K = isa ? fs.Ka : fs.Kg;
+    const bool live = v < fs.nca + fs.ncg;
+    const u32x4_t rs = isa ? fs.ra : fs.rg;
+#pragma unroll
+    for (int i = 0; i < kFullLPW; ++i) {
+        const bool ok = live && ch * (kFullCW / 2) + fs.lcol[i] * 8 < K;
+        const uint32_t off = (uint32_t)ch * kFullCW + (isa ? fs.ba[i] : fs.bg[i]);
+        dma16_asm(rs, ok ? off : kGhostOut, slot + (8 * i + wave) * 1024);
+    }
+}
+
+// Sub-tiles Q .. Q + N - 1 with their blocks as constants (so that fragment
+// and accumulator indices stay compile-time): one MFMA step each, and the
+// weighted sum of Gram(a) o Gram(g) (off-diagonal sub-tiles twice).
+template <int NSUB, int Q, int N>
+struct FullStep {
+    static constexpr int I = FullTiles<NSUB>::row(Q), J = FullTiles<NSUB>::col(Q);
+    static __device__ __forceinline__ void mfma(f32x16_t* acc, const uint4* fr) {
+        Mfma<bf16_t>::step(acc[0], fr[I], fr[J]);
+        FullStep<NSUB, Q + 1, N - 1>::mfma(acc + 1, fr);
+    }
+    static __device__ __forceinline__ float dot(const f32x16_t* a, const f32x16_t* g) {
+        float v = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v += a[0][i] * g[0][i];
+        return (I == J ? 1.f : 2.f) * v + FullStep<NSUB, Q + 1, N - 1>::dot(a + 1, g + 1);
+    }
+};
+template <int NSUB, int Q>
+struct FullStep<NSUB, Q, 0> {
+    static __device__ __forceinline__ void mfma(f32x16_t*, const uint4*) {}
+    static __device__ __forceinline__ float dot(const f32x16_t*, const f32x16_t*) { return 0.f; }
+};
+
+// acc[t] += sub-tile t of X X^T over one chunk (4 k steps of 16 bf16).
+template <int NSUB, int W>
+__device__ __forceinline__ void full_compute(const char* __restrict__ slot, f32x16_t* acc) {
+    using FT = FullTiles<NSUB>;
+    constexpr int N = FT::count(W), Q0 = FT::start(W);
+    constexpr unsigned USED = FT::used(W);
+    const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int j = 0; j < kFullCW / 32; ++j) {
+        const int col = 2 * j + h;
+        uint4 fr[NSUB];
+#pragma unroll
+        for (int b = 0; b < NSUB; ++b)
+            if (USED & (1u << b)) {
+                const int row = 32 * b + r;
+                fr[b] = *reinterpret_cast<const uint4*>(slot + row * kFullCW + full_swz(row, col) * 16);
+            }
+        FullStep<NSUB, Q0, N>::mfma(acc, fr);
+    }
+}
+
+// This wave's weighted sum of Gram(a) o Gram(g) over its sub-tiles.
+template <int NSUB, int W>
+__device__ __forceinline__ float full_wave(const FullStream& fs, char* ring, int wave) {
+    using FT = FullTiles<NSUB>;
+    constexpr int N = FT::count(W), Q0 = FT::start(W);
+    f32x16_t accA[N > 0 ? N : 1], accG[N > 0 ? N : 1];
+#pragma unroll
+    for (int t = 0; t < N; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) accA[t][i] = accG[t][i] = 0.f;
+    // Chunk v: wait for this wave's loads of it (the later chunks may stay
+    // in flight), barrier (every wave's loads of it have landed and every
+    // wave is done with chunk v - 1), refill chunk v - 1's slot, multiply.
+    const int nv = fs.nca + fs.ncg;
+#pragma unroll
+    for (int c = 0; c < kFullSlots - 1; ++c) full_issue(fs, c, ring, wave);
+    for (int v = 0; v < fs.nca; ++v) {
+        wait_vmcnt<kFullLPW * (kFullSlots - 2)>();
+        lds_barrier();
+        full_issue(fs, v + kFullSlots - 1, ring, wave);
+        full_compute<NSUB, W>(ring + (v % kFullSlots) * kFullSlot, accA);
+    }
+    for (int v = fs.nca; v < nv; ++v) {
+        wait_vmcnt<kFullLPW * (kFullSlots - 2)>();
+        lds_barrier();
+        full_issue(fs, v + kFullSlots - 1, ring, wave);
+        full_compute<NSUB, W>(ring + (v % kFullSlots) * kFullSlot, accG);
+    }
+    wait_vmcnt<0>();
+    return FullStep<NSUB, Q0, N>::dot(accA, accG);
+}
+
+template <int NSUB>
+__device__ __forceinline__ float full_sample(const FullStream& fs, char* ring, int wave) {
+    switch (wave) {
+        case 0: return full_wave<NSUB, 0>(fs, ring, wave);
+        case 1: return full_wave<NSUB, 1>(fs, ring, wave);
+        case 2: return full_wave<NSUB, 2>(fs, ring, wave);
+        case 3: return full_wave<NSUB, 3>(fs, ring, wave);
+        case 4: return full_wave<NSUB, 4>(fs, ring, wave);
+        case 5: return full_wave<NSUB, 5>(fs, ring, wave);
+        case 6: return full_wave<NSUB, 6>(fs, ring, wave);
+        default: return full_wave<NSUB, 7>(fs, ring, wave);
+    }
+}
+
+__global__ __launch_bounds__(kFullThreads) void ghost_full_kernel(const GhostArgs args) {
+    __shared__ __attribute__((aligned(16))) char ring[kFullSlots * kFullSlot];
+    __shared__ float red[kFullThreads / 64];
+    // One workgroup per (layer, sample); nothing is shared between them, so
+    // the hardware's round-robin deal over the XCDs stays (the host orders the
+    // layers largest first).
+    const int wg = blockIdx.x;
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
+    const GhostLayer& L = args.L[l];
+    const int sample = wg - L.wg_begin;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+
+    FullStream fs;
+    fs.Ka = L.d;
+    fs.Kg = L.p;
+    fs.nca = (L.d + kFullCW / 2 - 1) / (kFullCW / 2);
+    fs.ncg = (L.p + kFullCW / 2 - 1) / (kFullCW / 2);
+    const uint32_t rba = (uint32_t)L.d * 2u, rbg = (uint32_t)L.p * 2u;
+    // The host guarantees (T + 128) * row bytes < 2^31 for this path.
+    fs.ra = raw_rsrc(reinterpret_cast<const bf16_t*>(L.x) + (size_t)sample * L.T * L.d, (uint32_t)L.T * rba);
+    fs.rg = raw_rsrc(reinterpret_cast<const bf16_t*>(L.g) + (size_t)sample * L.T * L.p, (uint32_t)L.T * rbg);
+    // Load i of this wave fills rows 8 (8 i + wave) .. + 7 of a slot; lane l
+    // writes 16-byte column l % 8 of row l / 8, which holds chunk column
+    // full_swz(row, l % 8).
+#pragma unroll
+    for (int i = 0; i < kFullLPW; ++i) {
+        const int row = 8 * (8 * i + wave) + lane / 8;
+        fs.lcol[i] = full_swz(row, lane % 8);
+        fs.ba[i] = (uint32_t)row * rba + (uint32_t)fs.lcol[i] * 16u;
+        fs.bg[i] = (uint32_t)row * rbg + (uint32_t)fs.lcol[i] * 16u;
+    }
+    float part;
+    switch (L.nsb) {            // 32-row blocks, 5 .. 8 (the host's range for this kernel)
+        case 5: part = full_sample<5>(fs, ring, wave); break;
+        case 6: part = full_sample<6>(fs, ring, wave); break;
+        case 7: part = full_sample<7>(fs, ring, wave); break;
+        default: part = full_sample<8>(fs, ring, wave); break;
+    }
+    part = wave_sum(part);
+    if (lane == 0) red[wave] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kFullThreads / 64; ++w) s += red[w];
+        args.part[(size_t)L.part_off + (size_t)sample] = s;
+    }
+}
+
 template <typename T, bool EMBED, bool VEC>
 __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     // VEC: the ring of gram_dl; otherwise two padded blocks for gram.
@@ -413,6 +630,12 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
 }
 
 }  // namespace
+
+hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, hipStream_t s) {
+    if (n_wg <= 0) return hipSuccess;
+    hipLaunchKernelGGL(ghost_full_kernel, dim3(n_wg), dim3(kFullThreads), 0, s, args);
+    return hipGetLastError();
+}
 
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s) {

@@ -72,6 +72,37 @@ def test_ghost_and_inst_norm_match_oracle(bk, B, T, d, p, dtype):
     assert _rel(inst, ref) <= NORM_TOL[dtype]
 
 
+@pytest.mark.parametrize("B,T,d,p", [
+    (3, 129, 72, 40), (2, 160, 8, 200), (2, 192, 136, 64), (4, 197, 768, 96), (2, 224, 64, 8),
+    (3, 255, 200, 128), (2, 256, 1280, 3840), (2, 197, 768, 2304), (2, 160, 512, 256), (3, 136, 256, 256)])
+def test_whole_sample_ghost_norm(bk, B, T, d, p):
+    """128 < T <= 256, bf16, 16-byte rows: the whole-sample ghost kernel (every
+    row streamed once, the full upper triangle of 32 x 32 Gram sub-tiles in one
+    workgroup), single-layer and grouped with layers of other T in one launch,
+    against the definition; a zero sample gives exactly 0."""
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B * 7 + T, g_scale=1e-2)
+    a[B - 1].zero_()
+    ref = oracle.linear_norm_sq(a, g)
+    da, dg = a.to(DEV), g.to(DEV)
+    out = bk.bk_ghost_norm(da, dg).cpu().numpy()
+    assert out[B - 1] == 0.0
+    assert _rel(out[:B - 1], ref[:B - 1]) <= 1e-4
+    # grouped: this layer between two ghost layers of other T (T = 200 shares the
+    # launch of the 128 < T <= 256 layers, T = 100 takes the super-block kernel)
+    a2, g2 = _pair(B, 200, 768, 256, torch.bfloat16, seed=T + 1)
+    a3, g3 = _pair(B, 100, 256, 128, torch.bfloat16, seed=T + 2)
+    ins = [(a2.to(DEV), g2.to(DEV)), (da, dg), (a3.to(DEV), g3.to(DEV))]
+    arr = bk.make_layers([{"kind": bk.BK_LINEAR, "x": x, "g": y} for x, y in ins])
+    norm_sq = torch.empty(3, B, device=DEV)
+    bk.bk_layer_norms(arr, 3, bk.BK_BF16, B, norm_sq)
+    got = norm_sq.cpu().numpy()
+    if oracle.use_ghost(T, d, p):
+        assert np.array_equal(got[1], out)                  # grouped == single-layer, bit for bit
+    assert got[1][B - 1] == 0.0 and _rel(got[1][:B - 1], ref[:B - 1]) <= 1e-4
+    assert _rel(got[0], oracle.linear_norm_sq(a2, g2)) <= 1e-4
+    assert _rel(got[2], oracle.linear_norm_sq(a3, g3)) <= 1e-4
+
+
 def test_ghost_norm_ties_and_zero(bk):
     a, g = _pair(3, 40, 32, 16, torch.float32, seed=5)
     a[1].zero_()
