@@ -93,7 +93,8 @@ struct NormPlan {
     int64_t nwg;        // workgroups of the norm kernel
     int64_t npart;      // partials per sample
     int var;            // kernel variant: ghost 0 = scalar, 1 = 16-byte loads,
-                        // 2 = whole-sample kernel (bf16, 128 < T <= 256);
+                        // 2 = whole-sample kernel (bf16, 128 < T <= 256),
+                        // 3 = 256-row super blocks (bf16, T > 256);
                         // instantiation: bk::GemmVariant
     int64_t tiles = 0;  // instantiation: output tiles per sample
     int64_t ksplit = 1; // instantiation: K slices per tile (wide and narrow kernels)
@@ -153,12 +154,15 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
         const int64_t K = np.path == Path::Embed ? L.p : std::max(L.d, L.p);
         const bool fits = (L.T + bk::kSuper) * K * (int64_t)es < ((int64_t)1 << 31);
         np.var = (xv && fits && aligned16(L.g) && (L.p * es) % 16 == 0) ? 1 : 0;
-        // 128 < T <= 256 on bf16 16-byte rows: the whole-sample kernel, which
-        // streams every row once (one partial per sample)
-        if (np.var == 1 && np.path == Path::Ghost && dt == BK_BF16 && L.T > bk::kSuper &&
-            L.T <= 2 * bk::kSuper) {
-            np.var = 2;
-            np.npart = 1;
+        // bf16 16-byte rows with T > 128: the kernels over 256-row super
+        // blocks (their 32-bit offsets reach 256 rows past T): 128 < T <= 256
+        // streams every row once (one partial per sample); longer T has nsb
+        // diagonal items and two half items per pair of super blocks.
+        const bool fits256 = (L.T + 2 * bk::kSuper) * K * (int64_t)es < ((int64_t)1 << 31);
+        if (np.var == 1 && np.path == Path::Ghost && dt == BK_BF16 && L.T > bk::kSuper && fits256) {
+            const int64_t nsb = cdiv(L.T, bk::kLongSuper);
+            np.var = L.T <= 2 * bk::kSuper ? 2 : 3;
+            np.npart = np.var == 2 ? 1 : nsb * nsb;
         }
     }
 }
@@ -191,9 +195,11 @@ size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
 // Launch of a ghost-norm variant (NormPlan::var) and the super-block count
 // its descriptors carry.
 hipError_t launch_ghost_var(const bk::GhostArgs& a, int n_wg, bool bf16, bool embed, int var, hipStream_t s) {
-    return var == 2 ? bk::launch_ghost_full(a, n_wg, s) : bk::launch_ghost(a, n_wg, bf16, embed, var == 1, s);
+    return var >= 2 ? bk::launch_ghost_full(a, n_wg, var == 3, s) : bk::launch_ghost(a, n_wg, bf16, embed, var == 1, s);
 }
-int32_t ghost_nsb(int64_t T, int var) { return (int32_t)cdiv(T, var == 2 ? bk::kFullSub : bk::kSuper); }
+int32_t ghost_nsb(int64_t T, int var) {
+    return (int32_t)cdiv(T, var == 2 ? bk::kFullSub : var == 3 ? bk::kLongSuper : bk::kSuper);
+}
 
 NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
@@ -392,7 +398,7 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     // a group larger than one launch's descriptor table is cut into launches
     // of near-equal layer counts (no small last launch).
     for (int kind = 0; kind < 3; ++kind)
-        for (int var = 0; var < (kind == 2 ? bk::kGemmVariants : 3); ++var) {
+        for (int var = 0; var < (kind == 2 ? bk::kGemmVariants : 4); ++var) {
             const Path want = kind == 0 ? Path::Ghost : kind == 1 ? Path::Embed : Path::Inst;
             std::vector<const Item*> all;
             for (const Item& it : items)

@@ -200,11 +200,14 @@ struct PrepArgs {
 };
 
 // ---- launchers (return the launch status) ----------------------------------
-// Whole-sample ghost norm (bf16, 16-byte rows, kSuper < T <= 2 kSuper): one
-// 512-thread workgroup per (layer, sample), GhostLayer::nsb = ceil(T / 32)
-// (5 .. 8), one partial per sample.
+// Ghost norms over 256-row super blocks (bf16, 16-byte rows), 512-thread
+// workgroups.  kSuper < T <= 2 kSuper (long_t false): one workgroup and one
+// partial per (layer, sample), GhostLayer::nsb = ceil(T / 32) (5 .. 8).
+// T > 2 kSuper (long_t true): GhostLayer::nsb = ceil(T / 256) super blocks,
+// npairs = nsb^2 items (workgroups, partials) per sample.
 constexpr int kFullSub = 32;
-hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, hipStream_t s);
+constexpr int kLongSuper = 256;
+hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, bool long_t, hipStream_t s);
 hipError_t launch_ghost(const GhostArgs& args, int n_wg, bool bf16, bool embed, bool vec,
                         hipStream_t s);
 // n_remap (Grad, GradDL): the first n_remap workgroups are dealt to the XCDs in

@@ -150,14 +150,18 @@ __device__ __forceinline__ void gram(const T* __restrict__ X, int rows, int K, i
 // ---------------------------------------------------------------------------
 constexpr int kRingBytes = 64 * 1024;        // LDS ring of gram_dl
 #ifndef BK_GHOST_DIAG_CW
-#define BK_GHOST_DIAG_CW 256
+#define BK_GHOST_DIAG_CW 128
+#endif
+#ifndef BK_GHOST_OFF_CW
+#define BK_GHOST_OFF_CW 128
 #endif
 
-// CW: bytes of each row per chunk (128 or 256).  A slot holds one 128-row
-// block of a chunk; the ring holds kRingBytes / (128 CW) slots.  Column c of
-// row r sits at column c ^ (r / 2 mod 8) (CW = 128: a 256-byte bank line
-// holds two rows) or c ^ (r mod 16) (CW = 256), so that the 16 rows read by
-// 16 lanes land on distinct 16-byte bank groups.
+// CW: bytes of each row per chunk (64, 128 or 256).  A slot holds one
+// 128-row block of a chunk; the ring holds kRingBytes / (128 CW) slots.
+// Column c of row r sits at column c ^ (r / 4 mod 4) (CW = 64: a 256-byte
+// bank line holds four rows), c ^ (r / 2 mod 8) (CW = 128) or c ^ (r mod 16)
+// (CW = 256), so that the 16 rows read by 16 lanes land on distinct 16-byte
+// bank groups.
 // Column sums (DIAG with a single 128-row block, i.e. T <= 128): with cs set,
 // each chunk's columns are also summed over the block's rows from LDS, cs[k] =
 // sum_t X[t, k] is written and bsq accumulates cs[k]^2 (threads that finish
@@ -170,7 +174,7 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
                                         const WaveTiles& wt, f32x16_t acc[4], char* __restrict__ lds,
                                         float* __restrict__ cs = nullptr, float* bsq = nullptr,
                                         float* cbuf = nullptr) {
-    static_assert(CW == 128 || CW == 256, "chunk width");
+    static_assert(CW == 64 || CW == 128 || CW == 256, "chunk width");
     constexpr int EPV = Elem<T>::per16;       // elements per 16 bytes
     constexpr int C16 = CW / 16;              // 16-byte columns per row and chunk
     constexpr int EPC = C16 * EPV;            // elements per row and chunk
@@ -182,7 +186,9 @@ __device__ __forceinline__ void gram_dl(const T* __restrict__ X, int rows, int K
     constexpr int RPL = 64 / C16;             // rows filled by one 1 KB load
     constexpr int LPB = kSuper / RPL / 4;     // loads per wave per block
     constexpr int LPW = LPB * SPC;            // loads per wave per chunk
-    auto swz = [](int row, int c) { return C16 == 8 ? c ^ ((row >> 1) & 7) : c ^ (row & 15); };
+    auto swz = [](int row, int c) {
+        return C16 == 4 ? c ^ ((row >> 2) & 3) : C16 == 8 ? c ^ ((row >> 1) & 7) : c ^ (row & 15);
+    };
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -327,34 +333,44 @@ __device__ __forceinline__ void gram_any(const T* __restrict__ X, int rows, int 
                                          float* cs = nullptr, float* bsq = nullptr, float* cbuf = nullptr) {
     if constexpr (VEC) {
         if (diag) gram_dl<T, true, BK_GHOST_DIAG_CW>(X, rows, K, rowR, rowC, wt, acc, smem, cs, bsq, cbuf);
-        else gram_dl<T, false, 128>(X, rows, K, rowR, rowC, wt, acc, smem);
+        else gram_dl<T, false, BK_GHOST_OFF_CW>(X, rows, K, rowR, rowC, wt, acc, smem);
     } else {
         gram<T, VEC>(X, rows, K, rowR, rowC, diag, wt, acc, reinterpret_cast<uint4*>(smem));
     }
 }
 
 // ---------------------------------------------------------------------------
-// Whole-sample ghost norm for 128 < T <= 256 (bf16, 16-byte rows).  With
-// 128-row super-block pairs every row block of such a sample is streamed
-// twice (pairs (0,0), (0,1), (1,1)), and the second read mostly comes from
-// HBM again.  Here one 512-thread workgroup owns one (layer, sample): the
-// rows of a_i and then of g_i pass through a 128 KB LDS ring once, in chunks
-// of 256 rows x 128 bytes (rows >= T load zeros), three chunks in flight,
-// one continuous stream over a's chunks and then g's.  The T x T Grams are
-// cut into NSUB = ceil(T / 32) blocks of 32 rows; the NSUB (NSUB + 1) / 2
-// upper-triangle 32 x 32 sub-tiles (row-major order) are dealt to the 8 waves
-// in contiguous runs, the first NT mod 8 waves taking one more, which puts
-// the same number of sub-tiles on each SIMD for NSUB = 7, 8 (waves w and
-// w + 4 share a SIMD).  Each wave keeps both Grams of its sub-tiles in
-// registers and reads each 32-row fragment its sub-tiles need once per k
-// step.  Off-diagonal sub-tiles count twice.  One partial per sample.
+// Ghost norms that stream 256-row super blocks (bf16, 16-byte rows).
+//
+// 128 < T <= 256 (ghost_full_kernel).  With 128-row super-block pairs every
+// row block of such a sample is streamed twice (pairs (0,0), (0,1), (1,1)),
+// and the second read mostly comes from HBM again.  Here one 512-thread
+// workgroup owns one (layer, sample): the rows of a_i and then of g_i pass
+// through a 128 KB LDS ring once, in chunks of 256 rows x 128 bytes (rows >= T
+// load zeros), three chunks in flight, one continuous stream over a's chunks
+// and then g's.  The T x T Grams are cut into NSUB = ceil(T / 32) blocks of 32
+// rows; the NSUB (NSUB + 1) / 2 upper-triangle 32 x 32 sub-tiles (row-major
+// order) are dealt to the 8 waves in contiguous runs, the first NT mod 8
+// waves taking one more, which puts the same number of sub-tiles on each SIMD
+// for NSUB = 7, 8 (waves w and w + 4 share a SIMD).  Each wave keeps both
+// Grams of its sub-tiles in registers and reads each 32-row fragment its
+// sub-tiles need once per k step.  Off-diagonal sub-tiles count twice.  One
+// partial per sample.
+//
+// T > 256 (ghost_long_kernel).  The Grams are cut into 256-row super blocks
+// (nsb = ceil(T / 256)); a sample has nsb diagonal items (one super block
+// against itself: the sub-tiles of the T <= 256 kernel with NSUB = 8) and,
+// for each pair R < C of super blocks, two half items (super block R against
+// one 128-row half of C: 8 x 4 sub-tiles, all counted twice, four per wave in
+// 2 x 2 arrangements).  nsb^2 items per sample, each one workgroup and one
+// partial; chunks of up to 384 rows (256 of R, 128 of the half of C) in a
+// three-slot 144 KB ring, two in flight.  Every item executes only useful
+// sub-tiles (528 per 1024-row sample against 544 with 128-row pairs) and
+// streams each row 5.5 times instead of 8 at T = 1024.  Items of one sample
+// run on one XCD (they share super blocks through its L2).
 // ---------------------------------------------------------------------------
 constexpr int kFullThreads = 512;
-constexpr int kFullRows = 256;                   // rows per chunk (T padded to 256)
 constexpr int kFullCW = 128;                     // bytes of each row per chunk
-constexpr int kFullSlot = kFullRows * kFullCW;   // 32 KB per chunk
-constexpr int kFullSlots = 4;                    // the ring: 128 KB
-constexpr int kFullLPW = kFullSlot / 1024 / 8;   // 1 KB LDS-DMA loads per wave per chunk
 
 template <int NSUB>
 struct FullTiles {
@@ -385,31 +401,57 @@ struct FullTiles {
 // 16 rows read by 16 lanes then meet 16 different 16-byte bank groups.
 __device__ __forceinline__ int full_swz(int row, int c) { return c ^ ((row >> 1) & 7); }
 
-// Rows of a_i / g_i of one sample and the LDS-DMA addressing of this wave.
+// Rows of a_i / g_i of one work item and this wave's LDS-DMA addressing:
+// chunk rows 0 .. 255 are rows rowA .. rowA + 255 of the sample, chunk rows
+// 256 .. 8 64 LPW - 1 rows rowB onwards.  Load i of the wave fills chunk rows
+// 8 (8 i + wave) .. + 7; lane l writes 16-byte column l % 8 of row l / 8,
+// which holds chunk column full_swz(row, l % 8).
+template <int LPW>
 struct FullStream {
     u32x4_t ra, rg;                  // resources over the sample's T rows (zeros beyond)
-    uint32_t ba[kFullLPW], bg[kFullLPW];   // byte offset of each load's lane within a chunk column
-    int lcol[kFullLPW];              // 16-byte chunk column each load's lane fetches
+    uint32_t ba[LPW], bg[LPW];       // byte offset of each load's lane within a chunk column
+    int lcol[LPW];                   // 16-byte chunk column each load's lane fetches
     int Ka, Kg, nca, ncg;            // row lengths (elements) and chunks of a and g
-};
 
-// Queue chunk v of the stream (a's chunks first, then g's) into its ring
-// slot.  Chunks past the end load zeros, so every call issues the same
-// number of loads.
-__device__ __forceinline__ void full_issue(const FullStream& fs, int v, char* ring, int wave) {
-    char* slot = ring + (v % kFullSlots) * kFullSlot;
-    const bool isa = v < fs.nca;
-    const int ch = isa ? v : v - fs.nca;
-    const int K = isa ? fs.Ka : fs.Kg;
-    const bool live = v < fs.nca + fs.ncg;
-    const u32x4_t rs = isa ? fs.ra : fs.rg;
+    __device__ __forceinline__ void init(const GhostLayer& L, int sample, int rowA, int rowB, int wave,
+                                         int lane) {
+        Ka = L.d;
+        Kg = L.p;
+        nca = (L.d + kFullCW / 2 - 1) / (kFullCW / 2);
+        ncg = (L.p + kFullCW / 2 - 1) / (kFullCW / 2);
+        const uint32_t rba = (uint32_t)L.d * 2u, rbg = (uint32_t)L.p * 2u;
+        // The host guarantees (T + 256) * row bytes < 2^31 for these kernels.
+        ra = raw_rsrc(reinterpret_cast<const bf16_t*>(L.x) + (size_t)sample * L.T * L.d, (uint32_t)L.T * rba);
+        rg = raw_rsrc(reinterpret_cast<const bf16_t*>(L.g) + (size_t)sample * L.T * L.p, (uint32_t)L.T * rbg);
 #pragma unroll
-    for (int i = 0; i < kFullLPW; ++i) {
-        const bool ok = live && ch * (kFullCW / 2) + fs.lcol[i] * 8 < K;
-        const uint32_t off = (uint32_t)ch * kFullCW + (isa ? fs.ba[i] : fs.bg[i]);
-        dma16_asm(rs, ok ? off : kGhostOut, slot + (8 * i + wave) * 1024);
+        for (int i = 0; i < LPW; ++i) {
+            const int lr = 8 * (8 * i + wave) + lane / 8;
+            const int row = lr < 256 ? rowA + lr : rowB + (lr - 256);
+            lcol[i] = full_swz(lr, lane % 8);
+            ba[i] = (uint32_t)row * rba + (uint32_t)lcol[i] * 16u;
+            bg[i] = (uint32_t)row * rbg + (uint32_t)lcol[i] * 16u;
+        }
     }
-}
+
+    // Queue chunk v (a's chunks first, then g's) into its slot of an
+    // NSLOT-slot ring.  Chunks past the end load zeros, so every call issues
+    // the same number of loads.
+    template <int NSLOT, int SLOTB>
+    __device__ __forceinline__ void issue(int v, char* ring, int wave) const {
+        char* slot = ring + (v % NSLOT) * SLOTB;
+        const bool isa = v < nca;
+        const int ch = isa ? v : v - nca;
+        const int K = isa ? Ka : Kg;
+        const bool live = v < nca + ncg;
+        const u32x4_t rs = isa ? ra : rg;
+#pragma unroll
+        for (int i = 0; i < LPW; ++i) {
+            const bool ok = live && ch * (kFullCW / 2) + lcol[i] * 8 < K;
+            const uint32_t off = (uint32_t)ch * kFullCW + (isa ? ba[i] : bg[i]);
+            dma16_asm(rs, ok ? off : kGhostOut, slot + (8 * i + wave) * 1024);
+        }
+    }
+};
 
 // Sub-tiles Q .. Q + N - 1 with their blocks as constants (so that fragment
 // and accumulator indices stay compile-time): one MFMA step each, and the
@@ -434,72 +476,143 @@ struct FullStep<NSUB, Q, 0> {
     static __device__ __forceinline__ float dot(const f32x16_t*, const f32x16_t*) { return 0.f; }
 };
 
-// acc[t] += sub-tile t of X X^T over one chunk (4 k steps of 16 bf16).
-template <int NSUB, int W>
-__device__ __forceinline__ void full_compute(const char* __restrict__ slot, f32x16_t* acc) {
-    using FT = FullTiles<NSUB>;
-    constexpr int N = FT::count(W), Q0 = FT::start(W);
-    constexpr unsigned USED = FT::used(W);
-    const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
-#pragma unroll
-    for (int j = 0; j < kFullCW / 32; ++j) {
-        const int col = 2 * j + h;
-        uint4 fr[NSUB];
-#pragma unroll
-        for (int b = 0; b < NSUB; ++b)
-            if (USED & (1u << b)) {
-                const int row = 32 * b + r;
-                fr[b] = *reinterpret_cast<const uint4*>(slot + row * kFullCW + full_swz(row, col) * 16);
-            }
-        FullStep<NSUB, Q0, N>::mfma(acc, fr);
-    }
+__device__ __forceinline__ uint4 full_frag(const char* slot, int row, int col) {
+    return *reinterpret_cast<const uint4*>(slot + row * kFullCW + full_swz(row, col) * 16);
 }
 
-// This wave's weighted sum of Gram(a) o Gram(g) over its sub-tiles.
+// Diagonal item: acc[t] += sub-tile t of X X^T over one chunk (4 k steps of
+// 16 bf16).
 template <int NSUB, int W>
-__device__ __forceinline__ float full_wave(const FullStream& fs, char* ring, int wave) {
+struct DiagTiles {
     using FT = FullTiles<NSUB>;
-    constexpr int N = FT::count(W), Q0 = FT::start(W);
+    static constexpr int N = FT::count(W), Q0 = FT::start(W);
+    static __device__ __forceinline__ void compute(const char* __restrict__ slot, f32x16_t* acc) {
+        constexpr unsigned USED = FT::used(W);
+        const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
+#pragma unroll
+        for (int j = 0; j < kFullCW / 32; ++j) {
+            uint4 fr[NSUB];
+#pragma unroll
+            for (int b = 0; b < NSUB; ++b)
+                if (USED & (1u << b)) fr[b] = full_frag(slot, 32 * b + r, 2 * j + h);
+            FullStep<NSUB, Q0, N>::mfma(acc, fr);
+        }
+    }
+    static __device__ __forceinline__ float dot(const f32x16_t* a, const f32x16_t* g) {
+        return FullStep<NSUB, Q0, N>::dot(a, g);
+    }
+};
+
+// Off-diagonal half item: wave w takes 32-row blocks I = 2 (w / 2) + {0, 1}
+// of super block R (chunk rows 0 .. 255) against blocks J = 2 (w mod 2) +
+// {0, 1} of the half of C (chunk rows 256 .. 383); every sub-tile counts twice.
+template <int W>
+struct HalfTiles {
+    static constexpr int N = 4;
+    static __device__ __forceinline__ void compute(const char* __restrict__ slot, f32x16_t* acc) {
+        const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
+        constexpr int I0 = 2 * (W >> 1), J0 = 2 * (W & 1);
+#pragma unroll
+        for (int j = 0; j < kFullCW / 32; ++j) {
+            const int col = 2 * j + h;
+            const uint4 x0 = full_frag(slot, 32 * I0 + r, col), x1 = full_frag(slot, 32 * (I0 + 1) + r, col);
+            const uint4 y0 = full_frag(slot, 256 + 32 * J0 + r, col);
+            const uint4 y1 = full_frag(slot, 256 + 32 * (J0 + 1) + r, col);
+            Mfma<bf16_t>::step(acc[0], x0, y0);
+            Mfma<bf16_t>::step(acc[1], x0, y1);
+            Mfma<bf16_t>::step(acc[2], x1, y0);
+            Mfma<bf16_t>::step(acc[3], x1, y1);
+        }
+    }
+    static __device__ __forceinline__ float dot(const f32x16_t* a, const f32x16_t* g) {
+        float v = 0.f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) v += a[t][i] * g[t][i];
+        return 2.f * v;
+    }
+};
+
+// One wave's share of a work item: stream a's then g's chunks through the
+// ring, accumulating this wave's sub-tiles (Tiles) of both Grams, and return
+// its weighted sum of Gram(a) o Gram(g).  Chunk v: wait for this wave's loads
+// of it (the later chunks may stay in flight), barrier (every wave's loads of
+// it have landed and every wave is done with chunk v - 1), refill chunk
+// v - 1's slot, multiply.
+template <typename Tiles, int LPW, int NSLOT, int SLOTB>
+__device__ __forceinline__ float stream_wave(const FullStream<LPW>& fs, char* ring, int wave) {
+    constexpr int N = Tiles::N;
     f32x16_t accA[N > 0 ? N : 1], accG[N > 0 ? N : 1];
 #pragma unroll
     for (int t = 0; t < N; ++t)
 #pragma unroll
         for (int i = 0; i < 16; ++i) accA[t][i] = accG[t][i] = 0.f;
-    // Chunk v: wait for this wave's loads of it (the later chunks may stay
-    // in flight), barrier (every wave's loads of it have landed and every
-    // wave is done with chunk v - 1), refill chunk v - 1's slot, multiply.
     const int nv = fs.nca + fs.ncg;
 #pragma unroll
-    for (int c = 0; c < kFullSlots - 1; ++c) full_issue(fs, c, ring, wave);
+    for (int c = 0; c < NSLOT - 1; ++c) fs.template issue<NSLOT, SLOTB>(c, ring, wave);
     for (int v = 0; v < fs.nca; ++v) {
-        wait_vmcnt<kFullLPW * (kFullSlots - 2)>();
+        wait_vmcnt<LPW * (NSLOT - 2)>();
         lds_barrier();
-        full_issue(fs, v + kFullSlots - 1, ring, wave);
-        full_compute<NSUB, W>(ring + (v % kFullSlots) * kFullSlot, accA);
+        fs.template issue<NSLOT, SLOTB>(v + NSLOT - 1, ring, wave);
+        Tiles::compute(ring + (v % NSLOT) * SLOTB, accA);
     }
     for (int v = fs.nca; v < nv; ++v) {
-        wait_vmcnt<kFullLPW * (kFullSlots - 2)>();
+        wait_vmcnt<LPW * (NSLOT - 2)>();
         lds_barrier();
-        full_issue(fs, v + kFullSlots - 1, ring, wave);
-        full_compute<NSUB, W>(ring + (v % kFullSlots) * kFullSlot, accG);
+        fs.template issue<NSLOT, SLOTB>(v + NSLOT - 1, ring, wave);
+        Tiles::compute(ring + (v % NSLOT) * SLOTB, accG);
     }
     wait_vmcnt<0>();
-    return FullStep<NSUB, Q0, N>::dot(accA, accG);
+    return Tiles::dot(accA, accG);
 }
 
-template <int NSUB>
-__device__ __forceinline__ float full_sample(const FullStream& fs, char* ring, int wave) {
+template <int NSUB, int LPW, int NSLOT, int SLOTB>
+__device__ __forceinline__ float diag_item(const FullStream<LPW>& fs, char* ring, int wave) {
     switch (wave) {
-        case 0: return full_wave<NSUB, 0>(fs, ring, wave);
-        case 1: return full_wave<NSUB, 1>(fs, ring, wave);
-        case 2: return full_wave<NSUB, 2>(fs, ring, wave);
-        case 3: return full_wave<NSUB, 3>(fs, ring, wave);
-        case 4: return full_wave<NSUB, 4>(fs, ring, wave);
-        case 5: return full_wave<NSUB, 5>(fs, ring, wave);
-        case 6: return full_wave<NSUB, 6>(fs, ring, wave);
-        default: return full_wave<NSUB, 7>(fs, ring, wave);
+        case 0: return stream_wave<DiagTiles<NSUB, 0>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 1: return stream_wave<DiagTiles<NSUB, 1>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 2: return stream_wave<DiagTiles<NSUB, 2>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 3: return stream_wave<DiagTiles<NSUB, 3>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 4: return stream_wave<DiagTiles<NSUB, 4>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 5: return stream_wave<DiagTiles<NSUB, 5>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 6: return stream_wave<DiagTiles<NSUB, 6>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        default: return stream_wave<DiagTiles<NSUB, 7>, LPW, NSLOT, SLOTB>(fs, ring, wave);
     }
 }
+
+template <int LPW, int NSLOT, int SLOTB>
+__device__ __forceinline__ float half_item(const FullStream<LPW>& fs, char* ring, int wave) {
+    switch (wave) {
+        case 0: return stream_wave<HalfTiles<0>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 1: return stream_wave<HalfTiles<1>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 2: return stream_wave<HalfTiles<2>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 3: return stream_wave<HalfTiles<3>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 4: return stream_wave<HalfTiles<4>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 5: return stream_wave<HalfTiles<5>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 6: return stream_wave<HalfTiles<6>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        default: return stream_wave<HalfTiles<7>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+    }
+}
+
+// Sum of one float per wave of a 512-thread workgroup, in wave order, into
+// the partial `out` (thread 0).
+__device__ __forceinline__ void write_part_512(float part, float* red, float* out) {
+    part = wave_sum(part);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kFullThreads / 64; ++w) s += red[w];
+        *out = s;
+    }
+}
+
+constexpr int kFullSlot = 256 * kFullCW;         // 32 KB: 256 rows
+constexpr int kFullSlots = 4;                    // 128 KB ring, three chunks in flight
+constexpr int kLongSlot = 384 * kFullCW;         // 48 KB: 256 + 128 rows
+constexpr int kLongSlots = 3;                    // 144 KB ring, two chunks in flight
 
 __global__ __launch_bounds__(kFullThreads) void ghost_full_kernel(const GhostArgs args) {
     __shared__ __attribute__((aligned(16))) char ring[kFullSlots * kFullSlot];
@@ -512,42 +625,45 @@ __global__ __launch_bounds__(kFullThreads) void ghost_full_kernel(const GhostArg
     const GhostLayer& L = args.L[l];
     const int sample = wg - L.wg_begin;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-
-    FullStream fs;
-    fs.Ka = L.d;
-    fs.Kg = L.p;
-    fs.nca = (L.d + kFullCW / 2 - 1) / (kFullCW / 2);
-    fs.ncg = (L.p + kFullCW / 2 - 1) / (kFullCW / 2);
-    const uint32_t rba = (uint32_t)L.d * 2u, rbg = (uint32_t)L.p * 2u;
-    // The host guarantees (T + 128) * row bytes < 2^31 for this path.
-    fs.ra = raw_rsrc(reinterpret_cast<const bf16_t*>(L.x) + (size_t)sample * L.T * L.d, (uint32_t)L.T * rba);
-    fs.rg = raw_rsrc(reinterpret_cast<const bf16_t*>(L.g) + (size_t)sample * L.T * L.p, (uint32_t)L.T * rbg);
-    // Load i of this wave fills rows 8 (8 i + wave) .. + 7 of a slot; lane l
-    // writes 16-byte column l % 8 of row l / 8, which holds chunk column
-    // full_swz(row, l % 8).
-#pragma unroll
-    for (int i = 0; i < kFullLPW; ++i) {
-        const int row = 8 * (8 * i + wave) + lane / 8;
-        fs.lcol[i] = full_swz(row, lane % 8);
-        fs.ba[i] = (uint32_t)row * rba + (uint32_t)fs.lcol[i] * 16u;
-        fs.bg[i] = (uint32_t)row * rbg + (uint32_t)fs.lcol[i] * 16u;
-    }
+    FullStream<4> fs;
+    fs.init(L, sample, 0, 256, wave, lane);
     float part;
     switch (L.nsb) {            // 32-row blocks, 5 .. 8 (the host's range for this kernel)
-        case 5: part = full_sample<5>(fs, ring, wave); break;
-        case 6: part = full_sample<6>(fs, ring, wave); break;
-        case 7: part = full_sample<7>(fs, ring, wave); break;
-        default: part = full_sample<8>(fs, ring, wave); break;
+        case 5: part = diag_item<5, 4, kFullSlots, kFullSlot>(fs, ring, wave); break;
+        case 6: part = diag_item<6, 4, kFullSlots, kFullSlot>(fs, ring, wave); break;
+        case 7: part = diag_item<7, 4, kFullSlots, kFullSlot>(fs, ring, wave); break;
+        default: part = diag_item<8, 4, kFullSlots, kFullSlot>(fs, ring, wave); break;
     }
-    part = wave_sum(part);
-    if (lane == 0) red[wave] = part;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float s = 0.f;
-#pragma unroll
-        for (int w = 0; w < kFullThreads / 64; ++w) s += red[w];
-        args.part[(size_t)L.part_off + (size_t)sample] = s;
+    write_part_512(part, red, args.part + (size_t)L.part_off + (size_t)sample);
+}
+
+__global__ __launch_bounds__(kFullThreads) void ghost_long_kernel(const GhostArgs args) {
+    __shared__ __attribute__((aligned(16))) char ring[kLongSlots * kLongSlot];
+    __shared__ float red[kFullThreads / 64];
+    // Consecutive workgroups (the items of one sample, which share super
+    // blocks) on one XCD.
+    const int wg = xcd_remap(blockIdx.x, gridDim.x);
+    const int l = find_desc(args.n, (int64_t)wg, [&](int k) { return args.L[k].wg_begin; });
+    const GhostLayer& L = args.L[l];
+    const int local = wg - L.wg_begin, nsb = L.nsb, items = L.npairs;   // items = nsb^2
+    const int sample = local / items, q = local - sample * items;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    float part;
+    if (q < nsb) {                                   // diagonal: super block q against itself
+        FullStream<4> fs;
+        fs.init(L, sample, 256 * q, 0, wave, lane);
+        part = diag_item<8, 4, kLongSlots, kLongSlot>(fs, ring, wave);
+    } else {                                         // pair R < C, half h of C
+        int m = (q - nsb) >> 1;
+        const int h = (q - nsb) & 1;
+        int R = 0;
+        while (m >= nsb - 1 - R) { m -= nsb - 1 - R; ++R; }
+        const int C = R + 1 + m;
+        FullStream<6> fs;
+        fs.init(L, sample, 256 * R, 256 * C + 128 * h, wave, lane);
+        part = half_item<6, kLongSlots, kLongSlot>(fs, ring, wave);
     }
+    write_part_512(part, red, args.part + (size_t)L.part_off + (size_t)sample * items + q);
 }
 
 template <typename T, bool EMBED, bool VEC>
@@ -631,9 +747,10 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
 
 }  // namespace
 
-hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, hipStream_t s) {
+hipError_t launch_ghost_full(const GhostArgs& args, int n_wg, bool long_t, hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
-    hipLaunchKernelGGL(ghost_full_kernel, dim3(n_wg), dim3(kFullThreads), 0, s, args);
+    if (long_t) hipLaunchKernelGGL(ghost_long_kernel, dim3(n_wg), dim3(kFullThreads), 0, s, args);
+    else hipLaunchKernelGGL(ghost_full_kernel, dim3(n_wg), dim3(kFullThreads), 0, s, args);
     return hipGetLastError();
 }
 

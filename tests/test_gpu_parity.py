@@ -103,6 +103,32 @@ def test_whole_sample_ghost_norm(bk, B, T, d, p):
     assert _rel(got[2], oracle.linear_norm_sq(a3, g3)) <= 1e-4
 
 
+@pytest.mark.parametrize("B,T,d,p", [
+    (2, 257, 72, 40), (2, 300, 256, 136), (3, 513, 64, 1280), (2, 1000, 768, 3072), (2, 1024, 3072, 768),
+    (2, 1024, 8, 8)])
+def test_long_ghost_norm(bk, B, T, d, p):
+    """T > 256, bf16, 16-byte rows: 256-row super blocks (diagonal items and
+    half-pair items, several per sample), against the definition; a zero
+    sample gives exactly 0; grouped with a T <= 256 layer, bit-identical to
+    the single-layer call when the layer takes the ghost path."""
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B * 11 + T, g_scale=1e-2)
+    a[B - 1].zero_()
+    ref = oracle.linear_norm_sq(a, g)
+    da, dg = a.to(DEV), g.to(DEV)
+    out = bk.bk_ghost_norm(da, dg).cpu().numpy()
+    assert out[B - 1] == 0.0
+    assert _rel(out[:B - 1], ref[:B - 1]) <= 1e-4
+    a2, g2 = _pair(B, 200, 768, 256, torch.bfloat16, seed=T + 5)
+    arr = bk.make_layers([{"kind": bk.BK_LINEAR, "x": x, "g": y} for x, y in ((da, dg), (a2.to(DEV), g2.to(DEV)))])
+    norm_sq = torch.empty(2, B, device=DEV)
+    bk.bk_layer_norms(arr, 2, bk.BK_BF16, B, norm_sq)
+    got = norm_sq.cpu().numpy()
+    if oracle.use_ghost(T, d, p):
+        assert np.array_equal(got[0], out)
+    assert got[0][B - 1] == 0.0 and _rel(got[0][:B - 1], ref[:B - 1]) <= 1e-4
+    assert _rel(got[1], oracle.linear_norm_sq(a2, g2)) <= 1e-4
+
+
 def test_ghost_norm_ties_and_zero(bk):
     a, g = _pair(3, 40, 32, 16, torch.float32, seed=5)
     a[1].zero_()
