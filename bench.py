@@ -331,6 +331,8 @@ def main():
                     help="untimed steps after the warm-up ramp (untimed steps filling %d ms of GPU "
                          "time, at least 3, which always runs)" % WARMUP_MS)
     ap.add_argument("--workload", type=int, default=2, help="synthetic stack id (1-8)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="run the workload's stack at this batch size instead of its own (0: its own)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-plain-gemm", action="store_true",
                     help="skip the hipBLASLt plain-GEMM denominator (keeps a kernel trace to the library)")
@@ -355,6 +357,9 @@ def main():
     import paper_2210_00038_amd as bk
 
     w = wl.get(args.workload)
+    if args.batch > 0:
+        import dataclasses
+        w = dataclasses.replace(w, B=args.batch, name=f"{w.name}@B{args.batch}")
     dev = torch.device("cuda:0")
     dt = bk.BK_BF16 if w.dtype == "bf16" else bk.BK_F32
     mode = bk.BK_CLIP_ABADI if w.clip == "abadi" else bk.BK_CLIP_AUTO

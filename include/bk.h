@@ -231,7 +231,9 @@ bk_status bk_conv_prep(const bk_conv* convs, int64_t n, bk_dtype dt, int64_t B, 
  * a_i is the one-hot encoding of the ids x_i, so a_i a_i^T is the token-id
  * equality matrix and
  *   norm_sq[i] = sum_{t,t'} [x_it == x_it'] <g_it, g_it'>.
- *   ids [B,T] int64 in [0, V), g [B,T,p] (dtype dt), norm_sq [B] out. */
+ *   ids [B,T] int64, g [B,T,p] (dtype dt), norm_sq [B] out.
+ * An id outside [0, V) has an all-zero one-hot row: its token adds nothing
+ * (here and in bk_embed_weighted_grad). */
 bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B,
                               int64_t T, int64_t p, int64_t V, float* norm_sq, void* ws,
                               size_t ws_bytes, void* stream);
@@ -256,9 +258,12 @@ bk_status bk_weighted_grad(const void* a, const void* g, const float* C, bk_dtyp
 
 /* The same for an embedding layer (a = one_hot(ids)):
  *   G[v,:] = sum_i C_i sum_{t : x_it = v} g_it   for every v in [0, V),
- * rows of ids that do not occur are zero.  Each row sums its tokens in
- * ascending (i, t) order.  G [V,p] float32 out.  B*T <= 8192 in this build
- * (BK_ERR_NOT_SUPPORTED above that). */
+ * rows of ids that do not occur are zero; tokens whose id lies outside
+ * [0, V) add nothing.  Each row sums its tokens in ascending (i, t) order
+ * (deterministic: a stable radix sort of the ids, then fixed-size chunks of
+ * the sorted tokens).  G [V,p] float32 out.  B*T <= 2^24 tokens per call
+ * (BK_ERR_NOT_SUPPORTED above); the workspace is about 16 B T + B T p / 8
+ * bytes (bk_workspace_size). */
 bk_status bk_embed_weighted_grad(const int64_t* ids, const void* g, const float* C,
                                  bk_dtype dt, int64_t B, int64_t T, int64_t p, int64_t V,
                                  float* G, void* ws, size_t ws_bytes, void* stream);

@@ -215,7 +215,7 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     return np;
 }
 
-size_t embed_grad_ws_bytes(int64_t B, int64_t T) { return bk::embed_grad_ws_bytes(B * T); }
+size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t p) { return bk::embed_grad_ws_bytes(B * T, p); }
 
 // BK-MixOpt layer that keeps its instantiated per-sample gradients in P.
 bool keeps_grads(const bk_layer& L) {
@@ -261,10 +261,10 @@ bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, b
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: NULL input pointer", fn, (long long)l);
     if (need_G && !L.G && L.d * L.p > 0)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: NULL gradient output", fn, (long long)l);
-    if (L.kind == BK_EMBEDDING && need_G && B * L.T > 8192)
+    if (L.kind == BK_EMBEDDING && need_G && B * L.T > bk::kEmbedMaxTokens)
         return fail(BK_ERR_NOT_SUPPORTED,
-                    "%s: layer %lld: embedding gradient supports at most 8192 tokens per call (B*T=%lld)",
-                    fn, (long long)l, (long long)(B * L.T));
+                    "%s: layer %lld: embedding gradient supports at most %lld tokens per call (B*T=%lld)",
+                    fn, (long long)l, (long long)bk::kEmbedMaxTokens, (long long)(B * L.T));
     return BK_OK;
 }
 
@@ -588,7 +588,7 @@ std::vector<GradGroup> grad_groups(const bk_layer* layers, int64_t n, bool bf16,
 size_t weighted_grads_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
     size_t tot = 0;
     for (int64_t l = 0; l < n; ++l)
-        if (layers[l].kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T));
+        if (layers[l].kind == BK_EMBEDDING) tot = std::max(tot, embed_grad_ws_bytes(B, layers[l].T, layers[l].p));
     // Grouped launches follow each other on the stream: each one's partial
     // tiles start at the workspace's beginning.
     for (const GradGroup& g : grad_groups(layers, n, dt == BK_BF16, B)) {
@@ -881,7 +881,7 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
             L.kind = BK_LINEAR;
             return weighted_grads_ws(&L, 1, dt, B);
         case BK_OP_EMBED_WEIGHTED_GRAD:
-            return embed_grad_ws_bytes(B, T);
+            return embed_grad_ws_bytes(B, T, p);
         default:
             return 0;
     }

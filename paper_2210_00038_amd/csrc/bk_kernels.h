@@ -230,9 +230,12 @@ hipError_t launch_conv_prep(const ConvPrepLayer* L, int n, int64_t B, bool bf16,
 hipError_t launch_tokens(const void* y, void* out, int64_t B, int64_t C, int64_t HW, bool bf16, hipStream_t st);
 hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_t q0, int64_t nq,
                              uint32_t* out, hipStream_t s);
-// Embedding gradient; ws holds embed_grad_ws_bytes(B*T) bytes (sorted keys
-// and the runs of equal ids).
-size_t embed_grad_ws_bytes(int64_t n);
+// Embedding gradient of n = B*T tokens (n <= kEmbedMaxTokens) into rows of p
+// columns; ws holds embed_grad_ws_bytes(n, p) bytes (the radix-sort key
+// buffers and digit histograms, and the chunks' partial rows, about n p / 8
+// bytes).
+constexpr int64_t kEmbedMaxTokens = (int64_t)1 << 24;
+size_t embed_grad_ws_bytes(int64_t n, int64_t p);
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
                              int64_t B, int64_t T, int64_t p, int64_t V, float* G, void* ws,
                              bool accum, hipStream_t s);

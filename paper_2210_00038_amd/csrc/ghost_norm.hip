@@ -704,10 +704,13 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
     f32x16_t accG[4];
     float part = 0.f;
     if constexpr (EMBED) {
+        // Ids outside [0, V) (V = L.d) are zero one-hot rows, like the padding
+        // rows: -1, which matches nothing.
         const int64_t* ids = reinterpret_cast<const int64_t*>(L.x) + (size_t)sample * nT;
         const int t = threadIdx.x;
         const int row = (t < kSuper) ? rowR + t : rowC + (t - kSuper);
-        sid[t] = (row < nT) ? ids[row] : (int64_t)-1;
+        const int64_t id = (row < nT) ? ids[row] : (int64_t)-1;
+        sid[t] = (id >= 0 && id < (int64_t)d) ? id : (int64_t)-1;
         gram_any<T, VEC>(reinterpret_cast<const T*>(L.g) + off_g, nT, p, rowR, rowC, diag, wt, accG, smem);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
@@ -717,10 +720,9 @@ __global__ __launch_bounds__(256) void ghost_norm_kernel(const GhostArgs args) {
             const int64_t* idr = sid + (wt.r0 + (s >> 1)) * 32;
             float v = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) v += (idr[acc_row(i, lane)] == idc) ? accG[s][i] : 0.f;
+            for (int i = 0; i < 16; ++i) v += (idr[acc_row(i, lane)] == idc && idc >= 0) ? accG[s][i] : 0.f;
             part += (float)wt.w[s] * v;
         }
-        (void)d;
     } else {
         f32x16_t accA[4];
         const size_t off_a = (size_t)sample * (size_t)nT * (size_t)d;

@@ -64,10 +64,12 @@ def test_workspace_sizes():
         9 * 16 * 256 * 256 * 4
     # T < 64 (the wide kernel, two workgroups per CU): no tail split
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 48, 768, 768) == 0
-    # sorted keys (8 B per token), run ids (4 B per token), run starts (n + 2 ints), 256-byte aligned
-    n = 16 * 256
-    assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, 1280) == \
-        n * 8 + n * 4 + ((n + 2) * 4 + 255) // 256 * 256
+    # two radix key buffers (8 B per token), 256-bin digit histograms per 1024-key tile, two
+    # partial rows per 64-token chunk and one flag per chunk, each 256-byte aligned
+    n, p = 16 * 256, 1280
+    al = lambda x: (x + 255) // 256 * 256
+    assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, p) == \
+        2 * al(n * 8) + al(256 * (n // 1024) * 4) + al(2 * (n // 64) * p * 4) + al((n // 64) * 4)
     assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, 7, 1, 1, 1, 1) == 0        # bad dtype
     assert bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_F32, -1, 1, 1, 1) == 0
 
@@ -118,8 +120,8 @@ def test_validation_before_any_device_call():
     assert L.bk_add_noise(None, 10, 1.0, 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
     assert L.bk_add_noise(FAKE, -1, 1.0, 0, 0, 0, None) == bk.BK_ERR_INVALID_VALUE
     assert L.bk_philox_raw(0, 0, 0, 0, 4, None, None) == bk.BK_ERR_INVALID_VALUE
-    # embedding gradient token limit of this build
-    assert L.bk_embed_weighted_grad(FAKE, FAKE, FAKE, bk.BK_BF16, 64, 256, 16, 100, FAKE, FAKE, 1 << 30,
+    # embedding gradient token limit of this build (2^24 tokens per call)
+    assert L.bk_embed_weighted_grad(FAKE, FAKE, FAKE, bk.BK_BF16, 4097, 4096, 16, 100, FAKE, FAKE, 1 << 40,
                                     None) == bk.BK_ERR_NOT_SUPPORTED
 
 
@@ -280,13 +282,13 @@ def test_grouped_noise_validation():
 
 
 def test_embedding_token_limit():
-    """An embedding layer's clipped gradient takes at most 8192 tokens per
+    """An embedding layer's clipped gradient takes at most 2^24 tokens per
     call: one more is refused before any launch."""
     arr = (bk.bk_layer * 1)()
-    arr[0].kind, arr[0].T, arr[0].d, arr[0].p = bk.BK_EMBEDDING, 8193, 100, 16
+    arr[0].kind, arr[0].T, arr[0].d, arr[0].p = bk.BK_EMBEDDING, (1 << 24) + 1, 100, 16
     arr[0].x = arr[0].g = arr[0].G = 0x10000
-    st = bk.lib.bk_weighted_grads(arr, 1, FAKE, bk.BK_BF16, 1, FAKE, 1 << 30, None)
-    assert st != bk.BK_OK and "8192" in bk.bk_last_error()
+    st = bk.lib.bk_weighted_grads(arr, 1, FAKE, bk.BK_BF16, 1, FAKE, 1 << 40, None)
+    assert st == bk.BK_ERR_NOT_SUPPORTED and str(1 << 24) in bk.bk_last_error()
 
 
 def test_noalloc_rejects_stacks_beyond_its_scratch():

@@ -722,16 +722,69 @@ def test_conv_stack_matches_oracle(bk):
 
 
 # ------------------------------------------- limits
-def test_embed_weighted_grad_at_the_token_limit(bk):
-    """8192 tokens (the most one call takes): the sort fills its whole LDS
-    table and Zipf ids over a small vocabulary give long runs."""
-    B, T, V, p = 32, 256, 1000, 96
-    ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.1, 17)).view(B, T)
-    g = torch.randn(B, T, p, generator=torch.Generator().manual_seed(18)).to(torch.bfloat16)
+@pytest.mark.parametrize("B,T,V,p,kind", [
+    (1, 8193, 1000, 96, "zipf"),          # one past the former single-workgroup limit
+    (64, 512, 50257, 1280, "zipf"),       # the GPT-2-large embedding at B = 64 (32768 tokens)
+    (16, 4096, 300, 64, "one"),           # one run over every token: 1024 chunks, one fix-up walk
+    (8, 1024, 130, 72, "blocks64"),       # runs of 64 tokens aligned to the chunks
+    (8, 1024, 126, 40, "blocks65"),       # runs of 65 tokens: every boundary crossed
+    (3, 20000, 70000, 24, "zipf"),        # 3 radix passes (V > 2^16)
+])
+def test_embed_weighted_grad_many_tokens(bk, B, T, V, p, kind):
+    """Beyond one workgroup's sort: a stable radix sort of the ids over
+    several tiles, then chunked segmented sums with a fix-up of the runs that
+    cross chunk boundaries; bit-identical on a second call; absent rows stay
+    zero; accumulation adds exactly the written rows."""
+    n = B * T
+    if kind == "zipf":
+        ids = torch.from_numpy(wl.zipf_ids(n, V, 1.1, 17)).view(B, T)
+    elif kind == "one":
+        ids = torch.full((B, T), V - 1, dtype=torch.int64)
+    else:
+        r = 64 if kind == "blocks64" else 65
+        ids = (torch.arange(n, dtype=torch.int64) // r % V).view(B, T)
+    g = (torch.randn(B, T, p, generator=torch.Generator().manual_seed(18)) * 1e-2).to(torch.bfloat16)
     C = torch.rand(B, generator=torch.Generator().manual_seed(19)) + 0.1
     ref = oracle.embed_weighted_grad(ids, g, C, V)
-    G = bk.bk_embed_weighted_grad(ids.to(DEV), g.to(DEV), C.to(DEV), V).cpu().numpy()
-    assert _frob(G, ref) <= GRAD_TOL[torch.bfloat16]
+    ids_d, g_d, C_d = ids.to(DEV), g.to(DEV), C.to(DEV)
+    G = bk.bk_embed_weighted_grad(ids_d, g_d, C_d, V)
+    Gh = G.cpu().numpy()
+    absent = np.setdiff1d(np.arange(V), ids.numpy().ravel())
+    assert np.all(Gh[absent] == 0.0)
+    e = _frob(Gh, ref)
+    print(f"n={n} V={V} {kind}: frob {e:.2e}")
+    assert e <= GRAD_TOL[torch.bfloat16] and e <= 1e-5
+    assert torch.equal(G, bk.bk_embed_weighted_grad(ids_d, g_d, C_d, V))
+    G0 = torch.randn(V, p, generator=torch.Generator().manual_seed(20)).to(DEV)
+    Ga = G0.clone()
+    arr = bk.make_layers([{"kind": bk.BK_EMBEDDING, "x": ids_d, "g": g_d, "G": Ga, "V": V, "accumulate": True}])
+    bk.bk_weighted_grads(arr, 1, C_d, bk.BK_BF16, B)
+    assert torch.equal(Ga, G0 + G)
+
+
+def test_embed_out_of_range_ids_are_zero_rows(bk):
+    """Ids outside [0, V) (negative, V, V + k, beyond 2^32) are all-zero
+    one-hot rows: norm and gradient equal the oracle's on the same batch with
+    those tokens' gradient rows zeroed (and any valid id in their place)."""
+    B, T, V, p = 4, 300, 500, 64
+    gen = torch.Generator().manual_seed(23)
+    ids = torch.randint(0, V, (B, T), generator=gen)
+    bad = torch.rand(B, T, generator=gen) < 0.1
+    vals = torch.tensor([-5, V, V + 7, (1 << 32) + 3, -(1 << 40)], dtype=torch.int64)
+    ids[bad] = vals[torch.randint(0, len(vals), (int(bad.sum()),), generator=gen)]
+    ids[0, :2] = torch.tensor([(1 << 32) + 3, 3])        # aliases id 3 modulo 2^32
+    g = torch.randn(B, T, p, generator=gen).to(torch.bfloat16)
+    C = torch.rand(B, generator=gen) + 0.1
+    g_ref = g.clone()
+    g_ref[bad | (ids < 0) | (ids >= V)] = 0
+    ids_ref = torch.where((ids >= 0) & (ids < V), ids, torch.zeros_like(ids))
+    ref_n = oracle.embed_norm_sq(ids_ref, g_ref, V)
+    ref_G = oracle.embed_weighted_grad(ids_ref, g_ref, C, V)
+    ids_d, g_d = ids.to(DEV), g.to(DEV)
+    n = bk.bk_embed_ghost_norm(ids_d, g_d, V).cpu().numpy()
+    assert _rel(n, ref_n) <= 1e-4
+    G = bk.bk_embed_weighted_grad(ids_d, g_d, C.to(DEV), V).cpu().numpy()
+    assert _frob(G, ref_G) <= 1e-5
 
 
 @pytest.mark.parametrize("B", [4096, 4097])
