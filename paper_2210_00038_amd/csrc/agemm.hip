@@ -368,13 +368,13 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kBM, n0 = nt * kBN;
 
-    // Contraction rows: one sample's T rows (instantiation) or all B*T rows.
-    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    // Contraction rows: one sample's T rows (instantiation) or all B*T rows,
+    // addressed stage by stage (rows_rsrc).
     const int64_t row0 = INST ? (int64_t)sample * nT : 0;
     const uint32_t nrows = INST ? (uint32_t)nT : (uint32_t)args.B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
-    const __amdgpu_buffer_rsrc_t rA = make_rsrc(reinterpret_cast<const bf16_t*>(L.a) + row0 * d, nrows * rowA);
-    const __amdgpu_buffer_rsrc_t rB = make_rsrc(reinterpret_cast<const bf16_t*>(L.g) + row0 * p, nrows * rowB);
+    const bf16_t* baseA = reinterpret_cast<const bf16_t*>(L.a) + row0 * d;
+    const bf16_t* baseB = reinterpret_cast<const bf16_t*>(L.g) + row0 * p;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -398,12 +398,14 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
     uint4 va[8], vb[4];
     float cw[4];
     auto fetch = [&](uint32_t k0) {
+        const __amdgpu_buffer_rsrc_t rA = rows_rsrc(baseA, rowA, k0, nrows, kBK);
+        const __amdgpu_buffer_rsrc_t rB = rows_rsrc(baseB, rowB, k0, nrows, kBK);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            va[j] = buffer_load16(rA, offA == kOut ? kOut : offA + (k0 + 8u * j) * rowA);
+            va[j] = buffer_load16(rA, offA == kOut ? kOut : offA + 8u * j * rowA);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            vb[j] = buffer_load16(rB, offB == kOut ? kOut : offB + (k0 + 16u * j) * rowB);
+            vb[j] = buffer_load16(rB, offB == kOut ? kOut : offB + 16u * j * rowB);
         if constexpr (!INST) {
             // Clip weight of each staged g row: C[k / T].  When T >= 64 the 64
             // rows of a stage span at most two samples (scalar split point).
@@ -557,14 +559,12 @@ __global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, in
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kNM, n0 = nt * BN;
 
-    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    // Contraction rows addressed stage by stage (rows_rsrc).
     const int64_t row0 = INST ? (int64_t)sample * nT : 0;
     const uint32_t nrows = INST ? (uint32_t)nT : (uint32_t)args.B * (uint32_t)nT;
     const uint32_t rowX = (uint32_t)Md * 2u, rowY = (uint32_t)Nd * 2u;
-    const bf16_t* X = reinterpret_cast<const bf16_t*>(sw ? L.g : L.a);
-    const bf16_t* Y = reinterpret_cast<const bf16_t*>(sw ? L.a : L.g);
-    const __amdgpu_buffer_rsrc_t rA = make_rsrc(X + row0 * Md, nrows * rowX);
-    const __amdgpu_buffer_rsrc_t rB = make_rsrc(Y + row0 * Nd, nrows * rowY);
+    const bf16_t* X = reinterpret_cast<const bf16_t*>(sw ? L.g : L.a) + row0 * Md;
+    const bf16_t* Y = reinterpret_cast<const bf16_t*>(sw ? L.a : L.g) + row0 * Nd;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -601,12 +601,14 @@ __global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, in
     auto fetch = [&](uint4 (&va)[8], uint4 (&vb)[NP], float (&cw)[NP], uint32_t st) {
         const uint32_t k0 = st * kBK;
         const bool live = st < nst;
+        const __amdgpu_buffer_rsrc_t rA = rows_rsrc(X, rowX, k0, nrows, kBK);
+        const __amdgpu_buffer_rsrc_t rB = rows_rsrc(Y, rowY, k0, nrows, kBK);
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            va[j] = buffer_load16(rA, (offA == kOut || !live) ? kOut : offA + (k0 + 8u * j) * rowX);
+            va[j] = buffer_load16(rA, (offA == kOut || !live) ? kOut : offA + 8u * j * rowX);
 #pragma unroll
         for (int j = 0; j < NP; ++j)
-            vb[j] = buffer_load16(rB, (offB == kOut || !live) ? kOut : offB + (k0 + (uint32_t)RPP * j) * rowY);
+            vb[j] = buffer_load16(rB, (offB == kOut || !live) ? kOut : offB + (uint32_t)RPP * j * rowY);
         if constexpr (!INST) {
             // Clip weight of each staged row: C[k / T].  The host sends only
             // T >= 64 here, so the 64 rows of a stage span at most two
@@ -750,7 +752,8 @@ __global__ __launch_bounds__(512, 1) void agrad_bf16_kernel(const GemmArgs args,
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
-    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel.
+    // The host guarantees (nrows + 3 kBK) * row bytes < 2^31 for this kernel
+    // (its registers leave no room to rebase the rows stage by stage).
     const uint32_t nrows = (uint32_t)args.B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(L.a, nrows * rowA);
@@ -939,9 +942,6 @@ constexpr int kDKS = kDLStageRows;               // k rows per stage
 constexpr int kDNB = kDLBuffers;                 // LDS stage buffers
 static_assert(kDKS == 32 || kDKS == 64, "stage rows");
 static_assert(kDNB >= 2 && kDNB * 2 * kDKS * kDRow <= 128 * 1024, "LDS ring");
-// Loads run up to NB + 1 stages past the last row; the Wide/Grad condition
-// (rows + 3 kBK) * row bytes < 2^31 covers that.
-static_assert((kDNB + 1) * kDKS <= 3 * kBK, "overrun bound");
 
 __device__ __forceinline__ int dswz(int row, int c16) { return c16 ^ (4 * (row & 3)); }
 
@@ -1013,13 +1013,11 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
-    // The host guarantees KS | T, B <= kDMaxB and
-    // (nrows + (NB + 1) KS) * row bytes < 2^31 for this kernel.
+    // The host guarantees KS | T and B <= kDMaxB for this kernel.  Rows are
+    // addressed stage by stage (rows_raw_rsrc).
     const int B = args.B;
     const uint32_t nrows = (uint32_t)B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
-    const u32x4_t rA = raw_rsrc(L.a, nrows * rowA);
-    const u32x4_t rB = raw_rsrc(L.g, nrows * rowB);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1044,12 +1042,12 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // the buffer at `buf`; `zero` (the stage's sample has weight 0) loads zeros.
     auto dma = [&](char* buf, uint32_t k0, bool zero, int i) {
         if (i < NI) {
-            const uint32_t o = (offA[i] == kOut || zero) ? kOut : offA[i] + k0 * rowA;
-            dma16_asm(rA, o, buf + (8 * i + wave) * 1024);
+            const uint32_t o = (offA[i] == kOut || zero) ? kOut : offA[i];
+            dma16_asm(rows_raw_rsrc(L.a, rowA, k0, nrows, kDKS), o, buf + (8 * i + wave) * 1024);
         } else {
             const int j = i - NI;
-            const uint32_t o = (offB[j] == kOut || zero) ? kOut : offB[j] + k0 * rowB;
-            dma16_asm(rB, o, buf + kDOp + (8 * j + wave) * 1024);
+            const uint32_t o = (offB[j] == kOut || zero) ? kOut : offB[j];
+            dma16_asm(rows_raw_rsrc(L.g, rowB, k0, nrows, kDKS), o, buf + kDOp + (8 * j + wave) * 1024);
         }
     };
 
@@ -1294,9 +1292,10 @@ GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool ali
     const int64_t es = bf16 ? 2 : 4;
     const bool vec = aligned && (d * es) % 16 == 0 && (p * es) % 16 == 0;
     if (!vec) return GemmVariant::Scalar;
-    // The wide and narrow kernels address a layer's rows (plus three stages
-    // of overrun) with 32-bit buffer offsets.
-    if (bf16 && (rows + 3 * kBK) * std::max(d, p) * es < ((int64_t)1 << 31)) {
+    // The wide and narrow kernels address one K stage of rows at a time with
+    // 32-bit buffer offsets (rows_rsrc): a stage must fit in 2^31 bytes.
+    (void)rows;
+    if (bf16 && 4 * kBK * std::max(d, p) * es < ((int64_t)1 << 31)) {
         const int64_t lo = std::min(d, p), hi = std::max(d, p);
         if (lo <= 64 && hi >= 128) return lo <= 32 ? GemmVariant::Narrow32 : GemmVariant::Narrow64;
         return GemmVariant::Wide;

@@ -482,7 +482,12 @@ bk::GemmVariant grad_variant(const bk_layer& L, bool bf16, int64_t B) {
     const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
     if (is_narrow(v)) return L.T < 64 ? bk::GemmVariant::Wide : v;   // narrow kernel: T >= 64
     if (v != bk::GemmVariant::Wide || L.T < 64) return v;
-    return (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) ? bk::GemmVariant::GradDL : bk::GemmVariant::Grad;
+    if (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) return bk::GemmVariant::GradDL;
+    // The register-staged 256 x 256 kernel addresses all B T rows (and three
+    // stages of 64 past them) with 32-bit offsets; longer layers take the
+    // wide kernel, which addresses one stage at a time.
+    const bool fits = (B * L.T + 3 * 64) * std::max(L.d, L.p) * (bf16 ? 2 : 4) < ((int64_t)1 << 31);
+    return fits ? bk::GemmVariant::Grad : bk::GemmVariant::Wide;
 }
 
 // Tiles and K slices of a linear layer's clipped gradient on variant v

@@ -81,6 +81,16 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+// A buffer resource over rows k0 .. k0 + rows_max - 1 of a row-major matrix
+// (fewer past its last row nrows; none at or past it): the GEMM kernels take
+// one per K stage, so the 32-bit offsets of their loads stay within one stage
+// and a matrix longer than 2^31 bytes needs no 64-bit offsets.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, uint32_t row_bytes, uint32_t k0,
+                                                            uint32_t nrows, uint32_t rows_max) {
+    const uint32_t left = k0 < nrows ? min(nrows - k0, rows_max) : 0u;
+    return make_rsrc(static_cast<const char*>(base) + (size_t)k0 * row_bytes, left * row_bytes);
+}
+
 // ---------------------------------------------------------------------------
 // Workgroup barrier for LDS producer/consumer hand-offs.  It waits for this
 // wave's LDS (and scalar) operations only, not for its global loads still in
@@ -119,6 +129,13 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ u32x4_t raw_rsrc(const void* base, uint32_t bytes) {
     const uint64_t a = reinterpret_cast<uint64_t>(base);
     return (u32x4_t){(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, bytes, 0x00020000u};
+}
+
+// rows_rsrc as raw descriptor words (for dma16_asm).
+__device__ __forceinline__ u32x4_t rows_raw_rsrc(const void* base, uint32_t row_bytes, uint32_t k0,
+                                                 uint32_t nrows, uint32_t rows_max) {
+    const uint32_t left = k0 < nrows ? min(nrows - k0, rows_max) : 0u;
+    return raw_rsrc(static_cast<const char*>(base) + (size_t)k0 * row_bytes, left * row_bytes);
 }
 
 __device__ __forceinline__ void dma16_asm(const u32x4_t& rs, uint32_t off, char* lds_dst) {

@@ -787,6 +787,37 @@ def test_embed_out_of_range_ids_are_zero_rows(bk):
     assert _frob(G, ref_G) <= 1e-5
 
 
+@pytest.mark.parametrize("B,T,d,p", [
+    (137, 1024, 8192, 256),     # LDS-DMA kernel (32 | T): a is 2.3 GB
+    (141, 1000, 8192, 256),     # 32 does not divide T: the wide kernel
+    (137, 1024, 8192, 32),      # narrow kernel
+])
+def test_weighted_grad_beyond_2_31_bytes(bk, B, T, d, p):
+    """Layers whose a (B T rows of d bf16) passes 2^31 bytes: the kernels
+    address one K stage at a time, so the offsets never wrap.  A 32 x 32 block
+    (and the last row and column) of G against the oracle; samples with
+    weight 0 included."""
+    assert B * T * d * 2 >= (1 << 31)
+    gen = torch.Generator(device=DEV).manual_seed(T + p)
+    a = torch.randn(B, T, d, generator=gen, device=DEV).to(torch.bfloat16)
+    g = (torch.randn(B, T, p, generator=gen, device=DEV) * 1e-2).to(torch.bfloat16)
+    C = torch.rand(B, generator=torch.Generator().manual_seed(B)) + 0.1
+    C[::5] = 0.0
+    G = bk.bk_weighted_grad(a, g, C.to(DEV))
+    rng = np.random.default_rng(d + p)
+    rows = np.sort(np.append(rng.choice(d - 1, 31, replace=False), d - 1))
+    cols = np.sort(np.append(rng.choice(p - 1, min(31, p - 1), replace=False), p - 1))
+    ri, ci = torch.as_tensor(rows, device=DEV), torch.as_tensor(cols, device=DEV)
+    ref = oracle.weighted_grad(a[:, :, ri].cpu(), g[:, :, ci].cpu(), C)
+    got = G[ri][:, ci].cpu().numpy()
+    e = _frob(got, ref)
+    print(f"B T = {B * T}, d = {d}, p = {p}: frob {e:.2e}")
+    from tolerances import grad_guard
+    assert e <= GRAD_TOL[torch.bfloat16] and e <= grad_guard(T, d, p, B)
+    del a, g, G
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("B", [4096, 4097])
 def test_weighted_grad_largest_weight_table(bk, B):
     """B = 4096 is the largest batch whose clip weights the LDS-DMA kernel
