@@ -214,8 +214,11 @@ KERNEL_SOURCES = {"agrad_dl_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "agemm_bf16_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "anarrow_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "ghost_norm_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
+                  "ghost_full_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
+                  "ghost_long_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
                   "split_reduce_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
-                  "conv_prep_kernel": "paper_2210_00038_amd/csrc/conv_prep.hip"}
+                  "conv_prep_kernel": "paper_2210_00038_amd/csrc/conv_prep.hip",
+                  "noise_kernel": "paper_2210_00038_amd/csrc/clip_noise.hip"}
 
 
 def _narrow(L) -> bool:
@@ -227,7 +230,9 @@ def norm_kernel(L, dtype: str = "bf16") -> str:
     if L.kind == "embed":
         return "ghost_norm_kernel"
     if 2 * L.T * L.T < L.p * L.d:
-        return "ghost_norm_kernel"
+        if dtype != "bf16" or L.T <= 128:
+            return "ghost_norm_kernel"
+        return "ghost_full_kernel" if L.T <= 256 else "ghost_long_kernel"
     if dtype != "bf16":
         return "agemm_kernel"
     return "anarrow_kernel" if _narrow(L) else "agemm_bf16_kernel"
@@ -252,7 +257,7 @@ def dominant_kernel(w: wl.Workload, phase: str) -> str:
     for L in w.layers:
         if phase == "norms":
             k = norm_kernel(L, w.dtype)
-            f = 2.0 * L.T * L.T * (L.p + L.d) if k == "ghost_norm_kernel" else 2.0 * L.T * L.p * L.d
+            f = 2.0 * L.T * L.T * (L.p + L.d) if k.startswith("ghost_") else 2.0 * L.T * L.p * L.d
         else:
             k, f = grad_kernel(L, w.dtype), 2.0 * L.T * L.p * L.d
         share[k] = share.get(k, 0.0) + f

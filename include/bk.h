@@ -293,7 +293,11 @@ bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64
 /* ---------------------------------------------------------------------------
  * Grouped forms: the same computations for n layers in as few launches as
  * possible.  Results are bit-identical to calling the per-layer form on each
- * layer.  The bk_layer array is read on the host during the call only.
+ * layer, with one exception: bf16 ghost-norm layers with 128 < T <= 256 (and
+ * 16-byte rows) take a whole-sample kernel when the launch gives it at least
+ * 512 workgroups (one per layer and sample), and a kernel over pairs of
+ * 128-row blocks otherwise; the two agree to fp32 rounding.  Every result is
+ * deterministic.  The bk_layer array is read on the host during the call only.
  * ------------------------------------------------------------------------- */
 
 /* Norms of every layer: ghost or instantiated per bk_use_ghost for linear

@@ -215,6 +215,35 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     return np;
 }
 
+// The whole-sample ghost kernel (variant 2) runs one workgroup per CU and
+// gives one per (layer, sample); a launch with fewer than kFullMinWG of them
+// (few samples and few such layers) keeps those layers on the super-block
+// pair kernel, which spreads three workgroups per sample over more CUs.
+constexpr int64_t kFullMinWG = 512;
+void demote_small_full(std::vector<NormPlan>& plans, const bk_layer* layers, int64_t B) {
+    int64_t wg = 0;
+    for (const NormPlan& np : plans) wg += np.path == Path::Ghost && np.var == 2 ? np.nwg : 0;
+    if (wg == 0 || wg >= kFullMinWG) return;
+    for (size_t l = 0; l < plans.size(); ++l) {
+        NormPlan& np = plans[l];
+        if (np.path != Path::Ghost || np.var != 2) continue;
+        const int64_t nsb = cdiv(layers[l].T, bk::kSuper);
+        np.var = 1;
+        np.npart = nsb * (nsb + 1) / 2;
+        finish_norm_plan(np, layers[l], B);
+    }
+}
+
+// The norm plans of a launch's layers (norm_plan each, then the launch-wide
+// choice of demote_small_full).
+std::vector<NormPlan> norm_plans(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
+    std::vector<NormPlan> v;
+    v.reserve((size_t)n);
+    for (int64_t l = 0; l < n; ++l) v.push_back(norm_plan(layers[l], dt, B));
+    demote_small_full(v, layers, B);
+    return v;
+}
+
 size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t p) { return bk::embed_grad_ws_bytes(B * T, p); }
 
 // BK-MixOpt layer that keeps its instantiated per-sample gradients in P.
@@ -273,7 +302,7 @@ bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, b
 // ---------------------------------------------------------------------------
 size_t layer_norms_ws(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B) {
     size_t tot = 0;
-    for (int64_t l = 0; l < n; ++l) tot += norm_ws_bytes(norm_plan(layers[l], dt, B), B);
+    for (const NormPlan& np : norm_plans(layers, n, dt, B)) tot += norm_ws_bytes(np, B);
     return tot;
 }
 
@@ -304,8 +333,9 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     std::vector<Item> items;
     items.reserve((size_t)n);
     int64_t off = 0, toff = 0;
+    const std::vector<NormPlan> plans = norm_plans(layers, n, dt, B);
     for (int64_t l = 0; l < n; ++l) {
-        const NormPlan np = norm_plan(layers[l], dt, B);
+        const NormPlan& np = plans[(size_t)l];
         items.push_back({l, np, off, toff});
         off += (int64_t)(align_up(norm_part_floats(np, B) * sizeof(float)) / sizeof(float));
         toff += (int64_t)norm_tile_floats(np, B);
@@ -786,10 +816,12 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
     if (st != BK_OK) return st;
     if ((st = check_layer(fn, L, 0, B, false)) != BK_OK) return st;
     if (B > 0 && !norm_sq) return fail(BK_ERR_INVALID_VALUE, "%s: NULL norm output", fn);
-    NormPlan np{};
-    np.path = want;
-    set_norm_variant(np, L, dt);
-    finish_norm_plan(np, L, B);
+    std::vector<NormPlan> one(1);
+    one[0].path = want;
+    set_norm_variant(one[0], L, dt);
+    finish_norm_plan(one[0], L, B);
+    demote_small_full(one, &L, B);
+    const NormPlan np = one[0];
     const size_t need = norm_ws_bytes(np, B);
     if (ws_bytes < need || (need > 0 && !ws))
         return fail(BK_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
