@@ -977,16 +977,24 @@ struct StagePos {
 // zeros.  (Products are exact in fp32 and each sample boundary rounds once,
 // instead of C_j g being rounded to bf16.)
 //
-// LDS: a ring of NB stage buffers (an a stage and a g stage each), 512-byte
-// rows without padding (one DMA instruction fills 1 KB contiguously); the
-// 16-byte column c of row r sits at c ^ 4 (r mod 4), which puts the four rows
-// that each half of a transpose read touches on distinct bank groups.  One
-// barrier per stage, before its last 16-row step: by then every wave has read
-// all of the stage's fragments (so its buffer is refilled right after, with
-// stage s + NB) and has waited for its own DMA of stage s + 1 (so the last
-// step reads the first fragments of stage s + 1).  A stage's loads thus have
-// NB - 1 stages to land.  The clip weights of the batch sit in LDS after the
-// ring (B <= kDMaxB).
+// LDS: a ring of NB = 4 stage buffers (an a stage and a g stage each),
+// 512-byte rows without padding (one DMA instruction fills 1 KB
+// contiguously); the 16-byte column c of row r sits at c ^ 4 (r mod 4), which
+// puts the four rows that each half of a transpose read touches on distinct
+// bank groups.  The clip weights of the batch sit in LDS after the ring
+// (B <= kDMaxB).
+//
+// Schedule (ping-pong): waves w and w + 4 share a SIMD.  Each stage is a
+// memory phase (all 24 transpose reads of the wave's fragments, the rescale
+// on entering a sample, the wait for the wave's own DMA of the next stage)
+// followed by an MFMA phase (the stage's 16 MFMAs, with the wave's four DMA
+// instructions of the stage three ahead among the first eight), and every
+// phase ends at a workgroup barrier.  Waves 4-7 run one phase behind waves
+// 0-3, so that on every SIMD one wave issues MFMAs while the other reads.
+// The buffer refilled during the MFMA phase of stage s, (s + 3) mod 4, was
+// last read in the memory phases of stage s - 1, which both halves have
+// passed; a stage's buffer is complete once every wave has waited for its
+// DMA of it before the barrier that precedes the first reads of it.
 // ---------------------------------------------------------------------------
 constexpr int kDOp = kDKS * kDRow;               // one operand of one stage
 constexpr int kDStage = 2 * kDOp;
@@ -1067,126 +1075,94 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // Weight of the stage at `pos` (0 past the batch).
     auto cw_of = [&](const StagePos& pos) { return ctab[min(pos.smp, (uint32_t)B)]; };
 
-    uint2 fa[4][2], fb[2][2][2];
-    auto read_a = [&](const char* A, int kk, int x, int h) {
-        fa[x][h] = frag_dl_half(A, 16 * (kk % kDKK), 128 * wm + 32 * x, lane, h);
-    };
-    auto read_b = [&](const char* Bt, int kk, int y, int h) {
-        fb[kk & 1][y][h] = frag_dl_half(Bt, 16 * (kk % kDKK), 64 * wn + 32 * y, lane, h);
-    };
-
     float c_last = 0.f;   // weight of the last sample with a nonzero weight
-    // Positions of stages st + 1 (its weight: the rescale on entering it) and
-    // st + NB (its weight: the zero test of its DMA).
-    StagePos pos1{0u, 0u}, posN{0u, 0u};
-    // Stage st out of buffer BUF.  Slot i of step kk issues MFMA (i / 2,
-    // i % 2) of step kk and its share of the next step's transpose reads (an
-    // even slot one half of a g fragment, double-buffered; an odd slot both
-    // halves of a fragment, whose two MFMAs of this step have then been
-    // issued).  After the barrier, the first slots of the last step refill
-    // this buffer with stage st + NB, one DMA instruction each.
-    auto stage = [&](auto buf_c, uint32_t st) {
+    static_assert(kDNB == 4 && kDKK == 2 && kDPW == 4, "ping-pong ring");
+    const bool late = wave >= 4;
+    uint2 fa[kDKK][4][2], fb[kDKK][2][2];
+    StagePos pos0{st_begin / spt, st_begin % spt};        // stage st
+    StagePos posD = pos0;                                  // stage st + 3
+    __syncthreads();      // clip weights in LDS
+    // Prologue: stages st_begin .. st_begin + 2 into buffers 0 .. 2.
+#pragma unroll
+    for (int b = 0; b < kDNB - 1; ++b) {
+        const bool z = cw_of(posD) == 0.f;
+#pragma unroll
+        for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (st_begin + (uint32_t)b) * kDKS, z, i);
+        posD.next(spt);
+    }
+    wait_vmcnt<(kDNB - 2) * kDPW>();
+    lds_barrier();
+    if (late) {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    auto run = [&](auto buf_c, uint32_t st) {
         constexpr int BUF = decltype(buf_c)::value;
-        char* A = lds + BUF * kDStage;
-        char* Bt = A + kDOp;
-        const char* An = lds + ((BUF + 1) % kDNB) * kDStage;
-        const char* Bn = An + kDOp;
-        float c_next = 0.f, c_dma = 0.f;
+        const char* A = lds + BUF * kDStage;
+        const char* Bt = A + kDOp;
+        char* D = lds + ((BUF + kDNB - 1) % kDNB) * kDStage;
+        // Memory phase: the stage's fragments, then (entering a sample, or at
+        // the slice's first stage) the accumulators times c_last / c (c != 0).
 #pragma unroll
         for (int kk = 0; kk < kDKK; ++kk) {
-            const int cur = kk & 1;
-            const char* RA = kk + 1 < kDKK ? A : An;
-            const char* RB = kk + 1 < kDKK ? Bt : Bn;
-            if (kk == kDKK - 1) {
-                wait_vmcnt<(kDNB - 2) * kDPW>();
-                lds_barrier();
-            }
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int x = i >> 1, y = i & 1;
-                const uint2 al = fa[x][0], ah = fa[x][1], bl = fb[cur][y][0], bh = fb[cur][y][1];
-                Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
-                if (i & 1) {
-                    read_a(RA, kk + 1, x, 0);
-                    read_a(RA, kk + 1, x, 1);
-                } else {
-                    read_b(RB, kk + 1, i >> 2, (i >> 1) & 1);
-                }
-                if (kk == 0 && i == 0) {
-                    c_next = cw_of(pos1);
-                    c_dma = cw_of(posN);
-                }
-                if (kk == kDKK - 1 && i < kDPW) dma(A, (st + kDNB) * kDKS, c_dma == 0.f, i);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        pos1.next(spt);
-        posN.next(spt);
-        return c_next;
-    };
-    // Entering a stage with weight c; `first`: it starts a sample.  (The test
-    // on `first` is uniform: a scalar branch; the one on c is a select.)
-    auto enter = [&](bool first, float c) {
-        if (!first) return;
-        const bool nz = c != 0.f;
-        const float r = nz ? c_last / c : 1.f;
+            for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int x = 0; x < 4; ++x)
+                for (int h = 0; h < 2; ++h) fa[kk][x][h] = frag_dl_half(A, 16 * kk, 128 * wm + 32 * x, lane, h);
 #pragma unroll
             for (int y = 0; y < 2; ++y)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) acc[x][y][i] *= r;
-        c_last = nz ? c : c_last;
-    };
-
-    __syncthreads();      // clip weights in LDS
-    float c_cur = 0.f;
-    StagePos pos0{st_begin / spt, st_begin % spt};        // stage st
-    pos1 = pos0;
-    pos1.next(spt);
-    // Prologue: stages st_begin .. st_begin + NB - 1 into the NB buffers.
-    {
-        StagePos q = pos0;
-#pragma unroll
-        for (int b = 0; b < kDNB; ++b) {
-            const bool z = cw_of(q) == 0.f;
-#pragma unroll
-            for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (st_begin + (uint32_t)b) * kDKS, z, i);
-            q.next(spt);
+                for (int h = 0; h < 2; ++h) fb[kk][y][h] = frag_dl_half(Bt, 16 * kk, 64 * wn + 32 * y, lane, h);
         }
-        posN = q;
-    }
-    c_cur = cw_of(pos0);
-    wait_vmcnt<(kDNB - 1) * kDPW>();
-    lds_barrier();
+        if (pos0.in == 0u || st == st_begin) {
+            const float c = cw_of(pos0);
+            const bool nz = c != 0.f;
+            const float r = nz ? c_last / c : 1.f;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-        read_a(lds, 0, x, 0);
-        read_a(lds, 0, x, 1);
-    }
+            for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 2; ++y) {
-        read_b(lds + kDOp, 0, y, 0);
-        read_b(lds + kDOp, 0, y, 1);
-    }
-    // The first stage of the slice sets the weight even inside a sample.
-    auto run = [&](auto buf_c, uint32_t st) {
-        enter(pos0.in == 0u || st == st_begin, c_cur);
-        c_cur = stage(buf_c, st);
+                for (int y = 0; y < 2; ++y)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[x][y][e] *= r;
+            c_last = nz ? c : c_last;
+        }
+        const bool zd = cw_of(posD) == 0.f;
+        wait_vmcnt<kDPW>();
+        __builtin_amdgcn_sched_barrier(0);
+        lds_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // MFMA phase.
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int kk = 0; kk < kDKK; ++kk) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int x = i >> 1, y = i & 1;
+                const uint2 al = fa[kk][x][0], ah = fa[kk][x][1], bl = fb[kk][y][0], bh = fb[kk][y][1];
+                Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
+                if (kk == 0 && (i & 1)) dma(D, (st + kDNB - 1) * kDKS, zd, i >> 1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
         pos0.next(spt);
+        posD.next(spt);
     };
     const uint32_t nst = st_end;
     uint32_t st = st_begin;
     for (; st + kDNB <= nst; st += kDNB) {
         run(std::integral_constant<int, 0>{}, st);
         run(std::integral_constant<int, 1>{}, st + 1);
-        if constexpr (kDNB > 2) run(std::integral_constant<int, 2 % kDNB>{}, st + 2);
-        if constexpr (kDNB > 3) run(std::integral_constant<int, 3 % kDNB>{}, st + 3);
+        run(std::integral_constant<int, 2>{}, st + 2);
+        run(std::integral_constant<int, 3>{}, st + 3);
     }
-    static_assert(kDNB <= 4, "ring unroll");
     if (st < nst) run(std::integral_constant<int, 0>{}, st++);
-    if (kDNB > 2 && st < nst) run(std::integral_constant<int, 1>{}, st++);
-    if (kDNB > 3 && st < nst) run(std::integral_constant<int, 2 % kDNB>{}, st++);
+    if (st < nst) run(std::integral_constant<int, 1>{}, st++);
+    if (st < nst) run(std::integral_constant<int, 2>{}, st++);
+    if (!late) __builtin_amdgcn_s_barrier();
     // Drain the DMA past the end before the workgroup exits.
     wait_vmcnt<0>();
 
