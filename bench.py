@@ -248,7 +248,8 @@ def grad_kernel(L, dtype: str = "bf16") -> str:
         return "agemm_bf16_kernel"
     if _narrow(L):
         return "anarrow_kernel"
-    return "agrad_dl_kernel" if L.T % 32 == 0 else "agrad_bf16_kernel"
+    # the DMA kernel pads each sample to 16-row steps; it takes T when that adds at most 1/8
+    return "agrad_dl_kernel" if 8 * (-(-L.T // 16) * 16) <= 9 * L.T else "agrad_bf16_kernel"
 
 
 def dominant_kernel(w: wl.Workload, phase: str) -> str:

@@ -248,10 +248,12 @@ bk_status bk_clip_factors(const float* norm_sq, int64_t L, int64_t B, bk_clip mo
 
 /* Algorithm 1, sum of clipped gradients (App. B.3 with the clip weights):
  *   G = a^T diag(C) g = sum_i C_i a_i^T g_i,   G [d,p] float32 out,
- * one GEMM over the flattened B*T rows.  For bf16 layers with 16-byte rows
- * and 32 | T the weights multiply the float32 accumulators (each GEMM stage
- * lies inside one sample); otherwise C_i multiplies the rows of g as they are
- * loaded (for bf16 the product C_i g is rounded to bf16 before the MFMA). */
+ * one GEMM over the flattened B*T rows.  For bf16 layers with 16-byte rows,
+ * min(d, p) > 64 or max(d, p) < 128, T >= 64, B <= 4096 and T at most 1/8
+ * short of a multiple of 16, the weights multiply the float32 accumulators
+ * (every sample starts a GEMM stage of 32 rows, its last stage padded with
+ * zero rows); otherwise C_i multiplies the rows of g as they are loaded (for
+ * bf16 the product C_i g is rounded to bf16 before the MFMA). */
 bk_status bk_weighted_grad(const void* a, const void* g, const float* C, bk_dtype dt,
                            int64_t B, int64_t T, int64_t d, int64_t p, float* G, void* ws,
                            size_t ws_bytes, void* stream);

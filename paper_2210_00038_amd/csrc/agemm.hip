@@ -1021,10 +1021,11 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
-    // The host guarantees KS | T and B <= kDMaxB for this kernel.  Rows are
-    // addressed stage by stage (rows_raw_rsrc).
+    // The host guarantees B <= kDMaxB for this kernel.  Each sample takes
+    // spt = ceil(T / KS) stages, its last one padded with zero rows (a
+    // stage's descriptor ends at its sample's last row: rows_raw_rsrc), and
+    // rows are addressed stage by stage.
     const int B = args.B;
-    const uint32_t nrows = (uint32_t)B * (uint32_t)nT;
     const uint32_t rowA = (uint32_t)d * 2u, rowB = (uint32_t)p * 2u;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -1046,16 +1047,19 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         offA[i] = (m0 + 8 * lc < d) ? (uint32_t)row * rowA + (uint32_t)(m0 + 8 * lc) * 2u : kOut;
         offB[i] = (n0 + 8 * lc < p) ? (uint32_t)row * rowB + (uint32_t)(n0 + 8 * lc) * 2u : kOut;
     }
-    // DMA piece i (i < NI: a, else g) of the stage starting at row k0 into
-    // the buffer at `buf`; `zero` (the stage's sample has weight 0) loads zeros.
-    auto dma = [&](char* buf, uint32_t k0, bool zero, int i) {
+    // DMA piece i (i < NI: a, else g) of stage `pos` into the buffer at
+    // `buf`; `zero` (the stage's sample has weight 0, or lies past the batch)
+    // loads zeros.
+    auto dma = [&](char* buf, const StagePos& pos, bool zero, int i) {
+        const uint32_t s0 = pos.smp * (uint32_t)nT;
+        const uint32_t k0 = s0 + pos.in * kDKS, kend = s0 + (uint32_t)nT;
         if (i < NI) {
             const uint32_t o = (offA[i] == kOut || zero) ? kOut : offA[i];
-            dma16_asm(rows_raw_rsrc(L.a, rowA, k0, nrows, kDKS), o, buf + (8 * i + wave) * 1024);
+            dma16_asm(rows_raw_rsrc(L.a, rowA, k0, kend, kDKS), o, buf + (8 * i + wave) * 1024);
         } else {
             const int j = i - NI;
             const uint32_t o = (offB[j] == kOut || zero) ? kOut : offB[j];
-            dma16_asm(rows_raw_rsrc(L.g, rowB, k0, nrows, kDKS), o, buf + kDOp + (8 * j + wave) * 1024);
+            dma16_asm(rows_raw_rsrc(L.g, rowB, k0, kend, kDKS), o, buf + kDOp + (8 * j + wave) * 1024);
         }
     };
 
@@ -1067,8 +1071,11 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[x][y][i] = 0.f;
 
-    const uint32_t nst_all = (nrows + kDKS - 1) / kDKS;
-    const uint32_t spt = (uint32_t)nT / kDKS;            // stages per sample
+    const uint32_t spt = ((uint32_t)nT + kDKS - 1) / kDKS;   // stages per sample
+    const uint32_t nst_all = (uint32_t)B * spt;
+    // The last stage of a sample holds at most 16 rows (16-row MFMA steps,
+    // the second one all zeros): its second step is skipped.
+    const bool short_last = (uint32_t)nT - (spt - 1) * kDKS <= 16u;
     // This workgroup's stages (K slice `slice` of `ks`).
     const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
     const uint32_t st_end = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
@@ -1087,7 +1094,7 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     for (int b = 0; b < kDNB - 1; ++b) {
         const bool z = cw_of(posD) == 0.f;
 #pragma unroll
-        for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, (st_begin + (uint32_t)b) * kDKS, z, i);
+        for (int i = 0; i < kDPW; ++i) dma(lds + b * kDStage, posD, z, i);
         posD.next(spt);
     }
     wait_vmcnt<(kDNB - 2) * kDPW>();
@@ -1104,8 +1111,10 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         char* D = lds + ((BUF + kDNB - 1) % kDNB) * kDStage;
         // Memory phase: the stage's fragments, then (entering a sample, or at
         // the slice's first stage) the accumulators times c_last / c (c != 0).
+        const bool two = !(short_last && pos0.in + 1u == spt);   // second step
 #pragma unroll
         for (int kk = 0; kk < kDKK; ++kk) {
+            if (kk > 0 && !two) break;
 #pragma unroll
             for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -1136,12 +1145,13 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int kk = 0; kk < kDKK; ++kk) {
+            if (kk > 0 && !two) break;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int x = i >> 1, y = i & 1;
                 const uint2 al = fa[kk][x][0], ah = fa[kk][x][1], bl = fb[kk][y][0], bh = fb[kk][y][1];
                 Mfma<bf16_t>::step(acc[x][y], make_uint4(al.x, al.y, ah.x, ah.y), make_uint4(bl.x, bl.y, bh.x, bh.y));
-                if (kk == 0 && (i & 1)) dma(D, (st + kDNB - 1) * kDKS, zd, i >> 1);
+                if (kk == 0 && (i & 1)) dma(D, posD, zd, i >> 1);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }

@@ -503,16 +503,22 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     return BK_OK;
 }
 
+// Stages per sample of the GradDL kernel: every sample starts a stage, its
+// last stage padded with zero rows.  The MFMAs run over T rounded up to
+// 16-row steps (a last stage of at most 16 rows skips its second step).
+int64_t dl_stages_per_sample(int64_t T) { return cdiv(T, bk::kDLStageRows); }
+bool dl_padding_ok(int64_t T) { return 8 * (cdiv(T, 16) * 16) <= 9 * T; }   // at most 1/8 padding
+
 // Kernel variant of a linear layer's clipped gradient: narrow layers with
 // T >= 64 run on the narrow kernel (shorter T on the wide one), the other
-// Wide layers with T >= 64 on the 256 x 256 kernels, with the weights on the accumulators
-// when the stage height divides T (and B fits the kernel's LDS table), else
-// on g.
+// Wide layers with T >= 64 on the 256 x 256 kernels, with the weights on the
+// accumulators when B fits the kernel's LDS table and padding each sample to
+// 16-row steps adds at most 1/8 to its rows, else on g.
 bk::GemmVariant grad_variant(const bk_layer& L, bool bf16, int64_t B) {
     const auto v = bk::gemm_variant(bf16, L.d, L.p, B * L.T, aligned16(L.x) && aligned16(L.g));
     if (is_narrow(v)) return L.T < 64 ? bk::GemmVariant::Wide : v;   // narrow kernel: T >= 64
     if (v != bk::GemmVariant::Wide || L.T < 64) return v;
-    if (L.T % bk::kDLStageRows == 0 && B <= bk::kDMaxB) return bk::GemmVariant::GradDL;
+    if (dl_padding_ok(L.T) && B <= bk::kDMaxB) return bk::GemmVariant::GradDL;
     // The register-staged 256 x 256 kernel addresses all B T rows (and three
     // stages of 64 past them) with 32-bit offsets; longer layers take the
     // wide kernel, which addresses one stage at a time.
@@ -535,8 +541,8 @@ GradPlan grad_plan(const bk_layer& L, bk::GemmVariant v, int64_t B) {
     const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
     GradPlan g{geo.tm, geo.tn, 1, geo.tile_elems, geo.swap};
     if (v == bk::GemmVariant::Grad || v == bk::GemmVariant::GradDL) {
-        const int64_t rows = v == bk::GemmVariant::Grad ? 64 : bk::kDLStageRows;
-        g.ksplit = grad_ksplit(g.tm * g.tn, cdiv(B * L.T, rows));
+        const int64_t nst = v == bk::GemmVariant::Grad ? cdiv(B * L.T, 64) : B * dl_stages_per_sample(L.T);
+        g.ksplit = grad_ksplit(g.tm * g.tn, nst);
     } else if (is_narrow(v)) {
         g.ksplit = narrow_grad_ksplit(g.tm * g.tn, cdiv(B * L.T, 64));
     }
@@ -586,7 +592,7 @@ void plan_tail(GradGroup& g, const bk_layer* layers, int64_t B, int64_t cus) {
     }
     const int64_t r = N % cus;
     if (r == 0 || 2 * r > cus || g.e[best].gp.tiles() < r) return;
-    const int64_t nst = cdiv(B * T0, g.v == bk::GemmVariant::GradDL ? bk::kDLStageRows : 64);
+    const int64_t nst = g.v == bk::GemmVariant::GradDL ? B * dl_stages_per_sample(T0) : cdiv(B * T0, 64);
     const int64_t sp = std::min({cus / r, nst / kTailMinStages, kTailMaxSplit});
     if (sp < 2) return;
     std::rotate(g.e.begin() + (std::ptrdiff_t)best, g.e.begin() + (std::ptrdiff_t)best + 1, g.e.end());

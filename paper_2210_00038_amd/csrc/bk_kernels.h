@@ -115,7 +115,8 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // most counter blocks handled by o
 //  Wide  : bf16, LDS transpose reads, larger tiles;
 //  Grad  : bf16 clipped gradient only, 256 x 256 tiles, 512 threads (T >= 64);
 //  GradDL: as Grad with LDS DMA and the weights on the accumulators
-//          (kDLStageRows divides T, B <= kDMaxB).
+//          (B <= kDMaxB; each sample padded to whole stages of
+//          kDLStageRows rows).
 //  Narrow32 / Narrow64: bf16, one side of d x p at most 32 / 64, tiles of
 //          256 along the long side (operands swapped when d < p).
 enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4, Narrow32 = 5, Narrow64 = 6 };

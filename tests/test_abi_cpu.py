@@ -59,9 +59,13 @@ def test_workspace_sizes():
         16 * 16 * 256 * 256 * 4
     # 12 x 12 = 144 tiles, over half of 256: no split
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1024, 3072, 3072) == 0
-    # T not a multiple of 32 (the register-staged 256 x 256 kernel, 64-row stages): split the same way
+    # T = 1000: each sample padded to 32 stages of 32 rows, split the same way
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 1000, 768, 768) == \
         9 * 16 * 256 * 256 * 4
+    # T = 70 (padding to 80 rows is over 1/8: the register-staged kernel, 64-row
+    # stages over all B T rows): 18 stages, slices of at least 8 stages
+    assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 70, 768, 768) == \
+        9 * 2 * 256 * 256 * 4
     # T < 64 (the wide kernel, two workgroups per CU): no tail split
     assert bk.bk_workspace_size(bk.BK_OP_WEIGHTED_GRAD, bk.BK_BF16, 16, 48, 768, 768) == 0
     # two radix key buffers (8 B per token), 256-bin digit histograms per 1024-key tile, two

@@ -30,16 +30,23 @@ DL_STAGE_ROWS = 32
 DL_MAX_B = 4096
 
 
+def dl_padding_ok(T: int) -> bool:
+    """That kernel pads every sample with zero rows to whole stages and runs
+    its MFMAs over T rounded up to 16 rows; it takes layers where that adds at
+    most 1/8 to T."""
+    return 8 * (-(-T // 16) * 16) <= 9 * T
+
+
 def weights_on_accumulators(T: int, d: int, p: int, B: int, dtype: str = "bf16") -> bool:
     """Whether a bf16 linear layer's clipped gradient runs on the kernel that
     applies C_i to its fp32 accumulators (exact weights) rather than to the
     rows of g (weights rounded with g to bf16): 16-byte rows, both sides wider
-    than 64 or neither narrow, T >= 64 and a multiple of the stage height."""
+    than 64 or neither narrow, T >= 64 with little padding (dl_padding_ok)."""
     if dtype != "bf16":
         return True
     lo, hi = min(d, p), max(d, p)
     narrow = lo <= 64 and hi >= 128
-    return (not narrow and T >= 64 and T % DL_STAGE_ROWS == 0 and B <= DL_MAX_B and
+    return (not narrow and T >= 64 and dl_padding_ok(T) and B <= DL_MAX_B and
             d % 8 == 0 and p % 8 == 0)
 
 
