@@ -501,6 +501,21 @@ struct DiagTiles {
     static __device__ __forceinline__ float dot(const f32x16_t* a, const f32x16_t* g) {
         return FullStep<NSUB, Q0, N>::dot(a, g);
     }
+    // The fragments of k step j (of 4) that the wave's sub-tiles use, and
+    // their MFMAs (the ping-pong stream reads and multiplies apart).
+    struct Frag {
+        uint4 fr[NSUB];
+    };
+    static __device__ __forceinline__ void read(const char* __restrict__ slot, int j, Frag& f) {
+        constexpr unsigned USED = FT::used(W);
+        const int lane = threadIdx.x & 63, r = lane & 31, h = lane >> 5;
+#pragma unroll
+        for (int b = 0; b < NSUB; ++b)
+            if (USED & (1u << b)) f.fr[b] = full_frag(slot, 32 * b + r, 2 * j + h);
+    }
+    static __device__ __forceinline__ void mma(f32x16_t* acc, const Frag& f) {
+        FullStep<NSUB, Q0, N>::mfma(acc, f.fr);
+    }
 };
 
 // Off-diagonal half item: wave w takes 32-row blocks I = 2 (w / 2) + {0, 1}
@@ -531,6 +546,23 @@ struct HalfTiles {
 #pragma unroll
             for (int i = 0; i < 16; ++i) v += a[t][i] * g[t][i];
         return 2.f * v;
+    }
+    struct Frag {
+        uint4 x0, x1, y0, y1;
+    };
+    static __device__ __forceinline__ void read(const char* __restrict__ slot, int j, Frag& f) {
+        const int lane = threadIdx.x & 63, r = lane & 31, col = 2 * j + (lane >> 5);
+        constexpr int I0 = 2 * (W >> 1), J0 = 2 * (W & 1);
+        f.x0 = full_frag(slot, 32 * I0 + r, col);
+        f.x1 = full_frag(slot, 32 * (I0 + 1) + r, col);
+        f.y0 = full_frag(slot, 256 + 32 * J0 + r, col);
+        f.y1 = full_frag(slot, 256 + 32 * (J0 + 1) + r, col);
+    }
+    static __device__ __forceinline__ void mma(f32x16_t* acc, const Frag& f) {
+        Mfma<bf16_t>::step(acc[0], f.x0, f.y0);
+        Mfma<bf16_t>::step(acc[1], f.x0, f.y1);
+        Mfma<bf16_t>::step(acc[2], f.x1, f.y0);
+        Mfma<bf16_t>::step(acc[3], f.x1, f.y1);
     }
 };
 
@@ -567,31 +599,97 @@ __device__ __forceinline__ float stream_wave(const FullStream<LPW>& fs, char* ri
     return Tiles::dot(accA, accG);
 }
 
-template <int NSUB, int LPW, int NSLOT, int SLOTB>
+// Ping-pong form of stream_wave.  Waves w and w + 4 share a SIMD; each half
+// chunk (two k steps) is a memory phase (the wave's fragments of both steps,
+// and in the second half the wait for its own loads of the next chunk) and
+// an MFMA phase (the MFMAs of both steps; in the first half, the refill of
+// chunk v - 1's slot with chunk v + NSLOT - 1 between them), each ended by a
+// workgroup barrier.  Waves 4-7 run one phase behind waves 0-3, so on every
+// SIMD one wave multiplies while the other reads.  Chunk v - 1's slot is
+// refilled only after the memory phases of both halves of the workgroup for
+// chunk v - 1 have passed a barrier, and chunk v + 1 is read only after a
+// barrier that every wave reaches after waiting for its loads of it.
+template <typename Tiles, int LPW, int NSLOT, int SLOTB>
+__device__ __forceinline__ float stream_wave_pp(const FullStream<LPW>& fs, char* ring, int wave) {
+    constexpr int N = Tiles::N;
+    static_assert(N > 0 && NSLOT >= 3, "ping-pong stream");
+    f32x16_t accA[N], accG[N];
+#pragma unroll
+    for (int t = 0; t < N; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) accA[t][i] = accG[t][i] = 0.f;
+    const bool late = wave >= 4;
+    const int nv = fs.nca + fs.ncg;
+#pragma unroll
+    for (int c = 0; c < NSLOT - 1; ++c) fs.template issue<NSLOT, SLOTB>(c, ring, wave);
+    wait_vmcnt<LPW * (NSLOT - 2)>();
+    lds_barrier();
+    if (late) {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    auto chunk = [&](int v, f32x16_t* acc) {
+        const char* slot = ring + (v % NSLOT) * SLOTB;
+#pragma unroll
+        for (int hs = 0; hs < 2; ++hs) {
+            typename Tiles::Frag f0, f1;
+            Tiles::read(slot, 2 * hs, f0);
+            Tiles::read(slot, 2 * hs + 1, f1);
+            if (hs == 1) wait_vmcnt<LPW * (NSLOT - 2)>();
+            __builtin_amdgcn_sched_barrier(0);
+            lds_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(1);
+            Tiles::mma(acc, f0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (hs == 0) fs.template issue<NSLOT, SLOTB>(v + NSLOT - 1, ring, wave);
+            __builtin_amdgcn_sched_barrier(0);
+            Tiles::mma(acc, f1);
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    for (int v = 0; v < fs.nca; ++v) chunk(v, accA);
+    for (int v = fs.nca; v < nv; ++v) chunk(v, accG);
+    if (!late) __builtin_amdgcn_s_barrier();
+    wait_vmcnt<0>();
+    return Tiles::dot(accA, accG);
+}
+
+template <typename Tiles, int LPW, int NSLOT, int SLOTB, bool PP>
+__device__ __forceinline__ float stream_any(const FullStream<LPW>& fs, char* ring, int wave) {
+    if constexpr (PP) return stream_wave_pp<Tiles, LPW, NSLOT, SLOTB>(fs, ring, wave);
+    else return stream_wave<Tiles, LPW, NSLOT, SLOTB>(fs, ring, wave);
+}
+
+template <int NSUB, int LPW, int NSLOT, int SLOTB, bool PP = false>
 __device__ __forceinline__ float diag_item(const FullStream<LPW>& fs, char* ring, int wave) {
     switch (wave) {
-        case 0: return stream_wave<DiagTiles<NSUB, 0>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 1: return stream_wave<DiagTiles<NSUB, 1>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 2: return stream_wave<DiagTiles<NSUB, 2>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 3: return stream_wave<DiagTiles<NSUB, 3>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 4: return stream_wave<DiagTiles<NSUB, 4>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 5: return stream_wave<DiagTiles<NSUB, 5>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 6: return stream_wave<DiagTiles<NSUB, 6>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        default: return stream_wave<DiagTiles<NSUB, 7>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 0: return stream_any<DiagTiles<NSUB, 0>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 1: return stream_any<DiagTiles<NSUB, 1>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 2: return stream_any<DiagTiles<NSUB, 2>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 3: return stream_any<DiagTiles<NSUB, 3>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 4: return stream_any<DiagTiles<NSUB, 4>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 5: return stream_any<DiagTiles<NSUB, 5>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 6: return stream_any<DiagTiles<NSUB, 6>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        default: return stream_any<DiagTiles<NSUB, 7>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
     }
 }
 
-template <int LPW, int NSLOT, int SLOTB>
+template <int LPW, int NSLOT, int SLOTB, bool PP = false>
 __device__ __forceinline__ float half_item(const FullStream<LPW>& fs, char* ring, int wave) {
     switch (wave) {
-        case 0: return stream_wave<HalfTiles<0>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 1: return stream_wave<HalfTiles<1>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 2: return stream_wave<HalfTiles<2>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 3: return stream_wave<HalfTiles<3>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 4: return stream_wave<HalfTiles<4>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 5: return stream_wave<HalfTiles<5>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        case 6: return stream_wave<HalfTiles<6>, LPW, NSLOT, SLOTB>(fs, ring, wave);
-        default: return stream_wave<HalfTiles<7>, LPW, NSLOT, SLOTB>(fs, ring, wave);
+        case 0: return stream_any<HalfTiles<0>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 1: return stream_any<HalfTiles<1>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 2: return stream_any<HalfTiles<2>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 3: return stream_any<HalfTiles<3>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 4: return stream_any<HalfTiles<4>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 5: return stream_any<HalfTiles<5>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        case 6: return stream_any<HalfTiles<6>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
+        default: return stream_any<HalfTiles<7>, LPW, NSLOT, SLOTB, PP>(fs, ring, wave);
     }
 }
 
@@ -613,6 +711,10 @@ constexpr int kFullSlot = 256 * kFullCW;         // 32 KB: 256 rows
 constexpr int kFullSlots = 4;                    // 128 KB ring, three chunks in flight
 constexpr int kLongSlot = 384 * kFullCW;         // 48 KB: 256 + 128 rows
 constexpr int kLongSlots = 3;                    // 144 KB ring, two chunks in flight
+#ifndef BK_GHOST_LONG_PP
+#define BK_GHOST_LONG_PP 1
+#endif
+constexpr bool kLongPP = BK_GHOST_LONG_PP != 0;  // ping-pong stream (stream_wave_pp)
 
 __global__ __launch_bounds__(kFullThreads) void ghost_full_kernel(const GhostArgs args) {
     __shared__ __attribute__((aligned(16))) char ring[kFullSlots * kFullSlot];
@@ -652,7 +754,7 @@ __global__ __launch_bounds__(kFullThreads) void ghost_long_kernel(const GhostArg
     if (q < nsb) {                                   // diagonal: super block q against itself
         FullStream<4> fs;
         fs.init(L, sample, 256 * q, 0, wave, lane);
-        part = diag_item<8, 4, kLongSlots, kLongSlot>(fs, ring, wave);
+        part = diag_item<8, 4, kLongSlots, kLongSlot, kLongPP>(fs, ring, wave);
     } else {                                         // pair R < C, half h of C
         int m = (q - nsb) >> 1;
         const int h = (q - nsb) & 1;
@@ -661,7 +763,7 @@ __global__ __launch_bounds__(kFullThreads) void ghost_long_kernel(const GhostArg
         const int C = R + 1 + m;
         FullStream<6> fs;
         fs.init(L, sample, 256 * R, 256 * C + 128 * h, wave, lane);
-        part = half_item<6, kLongSlots, kLongSlot>(fs, ring, wave);
+        part = half_item<6, kLongSlots, kLongSlot, kLongPP>(fs, ring, wave);
     }
     write_part_512(part, red, args.part + (size_t)L.part_off + (size_t)sample * items + q);
 }
