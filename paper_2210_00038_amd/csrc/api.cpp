@@ -164,6 +164,15 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
             np.var = L.T <= 2 * bk::kSuper ? 2 : 3;
             np.npart = np.var == 2 ? 1 : nsb * nsb;
         }
+        // An embedding with T > 128 (more than one super block): the id join
+        // (every row of g read once) instead of the masked Gram, one partial
+        // per chunk of 8 ct columns of g (variant 2: ct = 8, 3: ct = 32).
+        if (np.path == Path::Embed && L.T > bk::kSuper && L.T <= bk::kEmbedJoinMaxT && aligned16(L.g) &&
+            L.p % 8 == 0) {
+            const int ct = bk::embed_join_ct(L.p);
+            np.var = ct == 8 ? 2 : 3;
+            np.npart = cdiv(L.p, 8 * ct);
+        }
     }
 }
 
@@ -195,6 +204,7 @@ size_t norm_ws_bytes(const NormPlan& np, int64_t B) {
 // Launch of a ghost-norm variant (NormPlan::var) and the super-block count
 // its descriptors carry.
 hipError_t launch_ghost_var(const bk::GhostArgs& a, int n_wg, bool bf16, bool embed, int var, hipStream_t s) {
+    if (embed && var >= 2) return bk::launch_embed_join(a, n_wg, bf16, var == 2 ? 8 : 32, s);
     return var >= 2 ? bk::launch_ghost_full(a, n_wg, var == 3, s) : bk::launch_ghost(a, n_wg, bf16, embed, var == 1, s);
 }
 int32_t ghost_nsb(int64_t T, int var) {
@@ -908,8 +918,20 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
     switch (op) {
         case BK_OP_GHOST_NORM:
         case BK_OP_EMBED_GHOST_NORM: {
+            // super-block pairs (an upper bound over the ghost kernels), or
+            // the id join's column chunks when it applies (NULL pointers
+            // count as aligned): the larger of the two, since the alignment
+            // of the caller's g is not known here
             const int64_t nsb = cdiv(T, bk::kSuper);
-            return align_up((size_t)(B * (nsb * (nsb + 1) / 2)) * sizeof(float));
+            int64_t npart = nsb * (nsb + 1) / 2;
+            if (op == BK_OP_EMBED_GHOST_NORM) {
+                L.kind = BK_EMBEDDING;
+                NormPlan np{};
+                np.path = Path::Embed;
+                set_norm_variant(np, L, dt);
+                npart = std::max(npart, np.npart);
+            }
+            return align_up((size_t)(B * npart) * sizeof(float));
         }
         case BK_OP_INST_NORM: {  // upper bound over the kernels (alignment is not known here)
             const size_t small = align_up((size_t)(B * cdiv(d, bk::kTile) * cdiv(p, bk::kTile)) * sizeof(float));

@@ -153,8 +153,6 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-// Sum of one float per thread over a 256-thread workgroup; result valid in
-// thread 0.  `red` must hold 4 floats of LDS.
 // Logical index of workgroup `wg` of `n` such that consecutive logical
 // indices run on the same XCD (workgroups are dealt round-robin to the 8
 // XCDs, each with its own L2).
@@ -179,6 +177,8 @@ __device__ __forceinline__ int find_desc(int n, int64_t wg, Begin begin) {
     return lo;
 }
 
+// Sum of one float per thread over a 256-thread workgroup; result valid in
+// thread 0.  `red` must hold 4 floats of LDS.
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
     v = wave_sum(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -236,6 +236,17 @@ hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_
 // buffers and digit histograms, and the chunks' partial rows, about n p / 8
 // bytes).
 constexpr int64_t kEmbedMaxTokens = (int64_t)1 << 24;
+
+// Embedding ghost norm as an id join (embed_join.hip): one 1024-thread
+// workgroup per (layer, sample, chunk of 8 ct columns of g), ct =
+// embed_join_ct(p) (8 or 32, the same for every layer of a launch), the
+// sample's T <= kEmbedJoinMaxT keys sorted in LDS (embed_join_lds_bytes(T)
+// of dynamic LDS); p % 8 == 0 and 16-byte aligned rows of g.  One partial
+// per chunk.
+constexpr int64_t kEmbedJoinMaxT = 16384;
+int embed_join_ct(int64_t p);
+size_t embed_join_lds_bytes(int64_t T);
+hipError_t launch_embed_join(const GhostArgs& args, int n_wg, bool bf16, int ct, hipStream_t s);
 size_t embed_grad_ws_bytes(int64_t n, int64_t p);
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
                              int64_t B, int64_t T, int64_t p, int64_t V, float* G, void* ws,

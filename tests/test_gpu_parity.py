@@ -17,6 +17,7 @@ import workloads as wl
 pytestmark = pytest.mark.gpu
 
 NORM_TOL = {torch.float32: 1e-5, torch.bfloat16: 2e-2}
+from tolerances import NORM_GUARD  # noqa: E402
 GRAD_TOL = {torch.float32: 1e-4, torch.bfloat16: 2e-2}
 DEV = "cuda"
 
@@ -170,6 +171,55 @@ def test_embed_norm_zipf_ids(bk):
     ref = oracle.embed_norm_sq(ids, g, 50257)
     out = bk.bk_embed_ghost_norm(ids.to(DEV), g.to(DEV), 50257).cpu().numpy()
     assert _rel(out, ref) <= 2e-2
+
+
+def _embed_norm_ref(ids, g, V):
+    """oracle.embed_norm_sq with the ids relabelled 0 .. (distinct - 1) (the
+    norm does not depend on which row an id selects) and tokens outside
+    [0, V) dropped (they select no row)."""
+    ids = ids.numpy()
+    valid = (ids >= 0) & (ids < V)
+    gv = g.float().numpy() * valid[..., None]
+    uniq, inv = np.unique(np.where(valid, ids, 0), return_inverse=True)
+    return oracle.embed_norm_sq(inv.reshape(ids.shape), gv, len(uniq))
+
+
+# Embedding norms with T > 128 run as a join on the token ids (sorted per
+# sample, each id's rows of g summed once); p % 8 != 0 or T past the join's
+# limit keep the masked Gram.
+@pytest.mark.parametrize("B,T,V,p,dtype,kind", [
+    (3, 129, 50, 64, torch.bfloat16, "zipf"),         # just past one 128-row super block
+    (2, 256, 50257, 1280, torch.bfloat16, "zipf"),    # the GPT-2-large embedding's shape
+    (2, 400, 300, 264, torch.bfloat16, "zipf"),       # 256-column chunks, the last one of 8 columns
+    (2, 1000, 7, 72, torch.float32, "uniform"),       # few ids, long runs, a ragged column chunk
+    (2, 4096, 50257, 64, torch.bfloat16, "zipf"),
+    (1, 16384, 1000, 8, torch.bfloat16, "uniform"),   # the longest T of the join
+    (3, 300, 5, 64, torch.bfloat16, "same"),          # one id per sample: one run over every segment
+    (2, 520, 100000, 64, torch.bfloat16, "distinct"), # every run one token long
+    (2, 700, 40, 64, torch.bfloat16, "bad"),          # ids outside [0, V) add nothing
+    (2, 300, 40, 60, torch.bfloat16, "uniform"),      # p % 8 != 0: the masked Gram
+    (1, 16385, 1000, 8, torch.bfloat16, "uniform"),   # past the join's T: the masked Gram
+])
+def test_embed_norm_join(bk, B, T, V, p, dtype, kind):
+    gen = torch.Generator().manual_seed(T + p)
+    if kind == "zipf":
+        ids = torch.from_numpy(wl.zipf_ids(B * T, V, 1.1, T)).view(B, T)
+    elif kind == "same":
+        ids = torch.full((B, T), 3, dtype=torch.int64)
+    elif kind == "distinct":
+        ids = torch.stack([torch.randperm(V, generator=gen)[:T] for _ in range(B)])
+    elif kind == "bad":
+        ids = torch.randint(-5, V + 5, (B, T), generator=gen)
+    else:
+        ids = torch.randint(0, V, (B, T), generator=gen)
+    g = (torch.randn(B, T, p, generator=gen) * 1e-2).to(dtype)
+    ref = _embed_norm_ref(ids, g, V)
+    out = bk.bk_embed_ghost_norm(ids.to(DEV), g.to(DEV), V)
+    again = bk.bk_embed_ghost_norm(ids.to(DEV), g.to(DEV), V)
+    assert torch.equal(out, again)                    # fixed summation order
+    e = _rel(out.cpu().numpy(), ref)
+    print(f"embed norm (T={T}, {kind}) rel err {e:.2e}")
+    assert e <= NORM_TOL[dtype] and e <= NORM_GUARD
 
 
 @pytest.mark.parametrize("mode,R,gamma", [(0, 1.0, 0.0), (0, 3.5, 0.0), (1, 1.0, 0.01), (1, 1.0, 0.0)])
