@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libbk.so")
 
-SOURCES = ["api.cpp", "ghost_norm.hip", "agemm.hip", "clip_noise.hip", "embed_grad.hip", "wsum.hip", "conv_prep.hip", "affine.hip", "noalloc.hip", "embed_join.hip"]
+SOURCES = ["api.cpp", "ghost_norm.hip", "agemm.hip", "clip_noise.hip", "embed_grad.hip", "wsum.hip", "conv_prep.hip", "affine.hip", "noalloc.hip", "embed_join.hip", "plan.cpp"]
 
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
 // The other workgroup on the CU covers this one's barriers.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kOut = 0xFFFFFFF0u;           // buffer offset that loads zeros
-constexpr int kBM = 256, kBN = 128, kBK = 64;
+constexpr int kBM = kWideM, kBN = kWideN, kBK = kWideK;
 constexpr int kSA = kBM * 2 + 64;                // bytes per staged k-row of a
 constexpr int kSB = kBN * 2 + 64;                // bytes per staged k-row of g
 
@@ -531,7 +531,7 @@ __global__ __launch_bounds__(256, 2) void agemm_bf16_kernel(const GemmArgs args,
 // clipped gradient runs here only for T >= 64 (a stage then spans at most two
 // samples, whose weights come through scalar loads).
 // ---------------------------------------------------------------------------
-constexpr int kNM = 256;
+constexpr int kNM = kNarrowM;
 constexpr int kNSY = 192;
 
 template <bool INST, int BN>
@@ -730,7 +730,7 @@ __global__ __launch_bounds__(256, 2) void anarrow_kernel(const GemmArgs args, in
 // LDS stores and the global loads into blocks, and the in-order issue of each
 // wave then leaves the MFMA pipe idle.  Only launched for T >= 64.
 // ---------------------------------------------------------------------------
-constexpr int kGM = 256, kGN = 256;
+constexpr int kGM = kGradM, kGN = kGradN;
 constexpr int kSG = 256 * 2 + 64;                // bytes per staged k-row (both operands)
 constexpr int kGOp = kBK * kSG;                  // one operand of one stage
 constexpr int kGStage = 2 * kGOp;
@@ -1257,37 +1257,6 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmArgs args) 
 }
 
 }  // namespace
-
-GemmGeom gemm_geom(GemmVariant v, int64_t d, int64_t p) {
-    auto cdiv = [](int64_t a, int64_t b) { return (a + b - 1) / b; };
-    switch (v) {
-        case GemmVariant::Grad:
-        case GemmVariant::GradDL: return {cdiv(d, kGM), cdiv(p, kGN), (int64_t)kGM * kGN, false};
-        case GemmVariant::Wide: return {cdiv(d, kBM), cdiv(p, kBN), (int64_t)kBM * kBN, false};
-        case GemmVariant::Narrow32:
-        case GemmVariant::Narrow64: {
-            const int64_t bn = v == GemmVariant::Narrow32 ? 32 : 64;
-            const bool sw = d < p;
-            return {cdiv(sw ? p : d, kNM), cdiv(sw ? d : p, bn), kNM * bn, sw};
-        }
-        default: return {cdiv(d, kTile), cdiv(p, kTile), (int64_t)kTile * kTile, false};
-    }
-}
-
-GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned) {
-    const int64_t es = bf16 ? 2 : 4;
-    const bool vec = aligned && (d * es) % 16 == 0 && (p * es) % 16 == 0;
-    if (!vec) return GemmVariant::Scalar;
-    // The wide and narrow kernels address one K stage of rows at a time with
-    // 32-bit buffer offsets (rows_rsrc): a stage must fit in 2^31 bytes.
-    (void)rows;
-    if (bf16 && 4 * kBK * std::max(d, p) * es < ((int64_t)1 << 31)) {
-        const int64_t lo = std::min(d, p), hi = std::max(d, p);
-        if (lo <= 64 && hi >= 128) return lo <= 32 ? GemmVariant::Narrow32 : GemmVariant::Narrow64;
-        return GemmVariant::Wide;
-    }
-    return GemmVariant::Vec;
-}
 
 hipError_t launch_split_reduce(const GemmArgs& args, int n_wg, bool inst_norm, GemmVariant v,
                                hipStream_t s) {

@@ -130,6 +130,12 @@ constexpr int kDMaxB = 4096;
 #endif
 constexpr int kDLStageRows = BK_DL_KS;   // k rows per stage of the GradDL kernel
 constexpr int kDLBuffers = BK_DL_NB;     // its LDS stage buffers
+// Output tiles of the a^T g kernels (plan.cpp and the kernels share them):
+// 256 x 128 with 64-row stages (Wide), 256 x 256 (Grad, GradDL), 256 along
+// the long side (Narrow); the Scalar / Vec tiles are kTile x kTile.
+constexpr int kWideM = 256, kWideN = 128, kWideK = 64;
+constexpr int kGradM = 256, kGradN = 256;
+constexpr int kNarrowM = 256;
 GemmVariant gemm_variant(bool bf16, int64_t d, int64_t p, int64_t rows, bool aligned);
 // Output tiles of a d x p layer on variant v: tm x tn tiles of tile_elems
 // floats (a K-split partial tile), rows along p when swap.
@@ -236,6 +242,13 @@ hipError_t launch_philox_raw(uint64_t seed, uint32_t tid, uint32_t step, uint64_
 // buffers and digit histograms, and the chunks' partial rows, about n p / 8
 // bytes).
 constexpr int64_t kEmbedMaxTokens = (int64_t)1 << 24;
+// Its workspace: radix tiles of kEmbedTileKeys keys, reduction chunks of
+// kEmbedChunk sorted positions, every part 256-byte aligned.
+constexpr int kEmbedTileKeys = 1024;
+constexpr int kEmbedChunk = 64;
+inline size_t embed_ws_align(size_t x) { return (x + 255) / 256 * 256; }
+inline int64_t embed_tiles_of(int64_t n) { return (n + kEmbedTileKeys - 1) / kEmbedTileKeys; }
+inline int64_t embed_chunks_of(int64_t n) { return (n + kEmbedChunk - 1) / kEmbedChunk; }
 
 // Embedding ghost norm as an id join (embed_join.hip): one 1024-thread
 // workgroup per (layer, sample, chunk of 8 ct columns of g), ct =
@@ -244,7 +257,11 @@ constexpr int64_t kEmbedMaxTokens = (int64_t)1 << 24;
 // of dynamic LDS); p % 8 == 0 and 16-byte aligned rows of g.  One partial
 // per chunk.
 constexpr int64_t kEmbedJoinMaxT = 16384;
+constexpr int kEmbedJoinThreads = 1024;
 int embed_join_ct(int64_t p);
+// Bytes of its keys / partial-sums region (16-byte multiple) and of its
+// whole dynamic LDS (the region and one flag per segment).
+size_t embed_join_region(int64_t T);
 size_t embed_join_lds_bytes(int64_t T);
 hipError_t launch_embed_join(const GhostArgs& args, int n_wg, bool bf16, int ct, hipStream_t s);
 size_t embed_grad_ws_bytes(int64_t n, int64_t p);

@@ -32,16 +32,15 @@
 namespace bk {
 namespace {
 
-constexpr int kTile = 1024;         // keys per radix tile
+constexpr int kTile = kEmbedTileKeys;   // keys per radix tile
 constexpr int kTileThreads = 256;
 constexpr int kPer = kTile / kTileThreads;   // rounds of one key per thread
-constexpr int kChunk = 64;          // sorted positions per reduction chunk
+constexpr int kChunk = kEmbedChunk;     // sorted positions per reduction chunk
 constexpr int kCols = 256;          // columns per reduction workgroup
 
-size_t ws_align(size_t x) { return (x + 255) / 256 * 256; }
-
-int64_t tiles_of(int64_t n) { return (n + kTile - 1) / kTile; }
-int64_t chunks_of(int64_t n) { return (n + kChunk - 1) / kChunk; }
+size_t ws_align(size_t x) { return embed_ws_align(x); }
+int64_t tiles_of(int64_t n) { return embed_tiles_of(n); }
+int64_t chunks_of(int64_t n) { return embed_chunks_of(n); }
 
 // Workspace for n tokens and rows of p columns: two key buffers [n] uint64,
 // the digit histograms [256 x tiles] int32, the partial rows of the chunks
@@ -287,12 +286,6 @@ __global__ __launch_bounds__(kCols) void embed_fixup_kernel(const uint64_t* __re
 }
 
 }  // namespace
-
-size_t embed_grad_ws_bytes(int64_t n, int64_t p) {
-    if (n <= 0) return 0;
-    return 2 * ws_align((size_t)n * sizeof(uint64_t)) + ws_align((size_t)(256 * tiles_of(n)) * sizeof(int32_t)) +
-           ws_align((size_t)(2 * chunks_of(n) * p) * sizeof(float)) + ws_align((size_t)chunks_of(n) * sizeof(int32_t));
-}
 
 hipError_t launch_embed_grad(const int64_t* ids, const void* g, const float* C, bool bf16,
                              int64_t B, int64_t T, int64_t p, int64_t V, float* G, void* ws, bool accum,

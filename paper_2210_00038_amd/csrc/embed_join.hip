@@ -29,10 +29,8 @@
 namespace bk {
 namespace {
 
-constexpr int kJoinThreads = 1024;
+constexpr int kJoinThreads = kEmbedJoinThreads;
 constexpr uint32_t kJoinBadId = 0x7FFFFFFFu;          // key id of ids outside [0, V)
-// LDS: the keys, later overlaid by every thread's head and tail sums.
-constexpr size_t kJoinSums = 2 * kJoinThreads * 8 * sizeof(float);
 
 // 8 consecutive elements of a row of g (16-byte aligned): loaded raw (Raw),
 // added to 8 floats (add).
@@ -210,23 +208,12 @@ __global__ __launch_bounds__(kJoinThreads) void embed_join_kernel(const GhostArg
 
 }  // namespace
 
-// Bytes of the keys / sums region (16-byte multiple), and of the whole
-// dynamic LDS (region + one flag per segment, at most 128).
-size_t join_region(int64_t T) {
-    int64_t tp = 1;
-    while (tp < T) tp <<= 1;
-    return std::max<size_t>((size_t)tp * 8, kJoinSums);
-}
-size_t embed_join_lds_bytes(int64_t T) { return join_region(T) + 128 * sizeof(int); }
-
-int embed_join_ct(int64_t p) { return p >= 256 ? 32 : 8; }
-
 hipError_t launch_embed_join(const GhostArgs& args, int n_wg, bool bf16, int ct, hipStream_t s) {
     if (n_wg <= 0) return hipSuccess;
     int64_t tmax = 1;
     for (int k = 0; k < args.n; ++k) tmax = std::max<int64_t>(tmax, args.L[k].T);
     if (tmax > kEmbedJoinMaxT || (ct != 8 && ct != 32)) return hipErrorInvalidValue;
-    const size_t region = join_region(tmax), lds = embed_join_lds_bytes(tmax);
+    const size_t region = embed_join_region(tmax), lds = embed_join_lds_bytes(tmax);
     const void* fn = bf16 ? (ct == 8 ? reinterpret_cast<const void*>(&embed_join_kernel<bf16_t, 8>)
                                      : reinterpret_cast<const void*>(&embed_join_kernel<bf16_t, 32>))
                           : (ct == 8 ? reinterpret_cast<const void*>(&embed_join_kernel<float, 8>)
