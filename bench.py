@@ -217,6 +217,7 @@ KERNEL_SOURCES = {"agrad_dl_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
                   "ghost_full_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
                   "ghost_long_kernel": "paper_2210_00038_amd/csrc/ghost_norm.hip",
                   "split_reduce_kernel": "paper_2210_00038_amd/csrc/agemm.hip",
+                  "embed_join_kernel": "paper_2210_00038_amd/csrc/embed_join.hip",
                   "conv_prep_kernel": "paper_2210_00038_amd/csrc/conv_prep.hip",
                   "noise_kernel": "paper_2210_00038_amd/csrc/clip_noise.hip"}
 
@@ -228,7 +229,8 @@ def _narrow(L) -> bool:
 def norm_kernel(L, dtype: str = "bf16") -> str:
     """Kernel that takes layer L's norm (the library's rule for 16-byte rows; a label only)."""
     if L.kind == "embed":
-        return "ghost_norm_kernel"
+        # T > 128 with 8 | p: the id join; else the masked Gram
+        return "embed_join_kernel" if 128 < L.T <= 16384 and L.p % 8 == 0 else "ghost_norm_kernel"
     if 2 * L.T * L.T < L.p * L.d:
         if dtype != "bf16" or L.T <= 128:
             return "ghost_norm_kernel"
