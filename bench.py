@@ -229,8 +229,8 @@ def _narrow(L) -> bool:
 def norm_kernel(L, dtype: str = "bf16") -> str:
     """Kernel that takes layer L's norm (the library's rule for 16-byte rows; a label only)."""
     if L.kind == "embed":
-        # T > 128 with 8 | p: the id join; else the masked Gram
-        return "embed_join_kernel" if 128 < L.T <= 16384 and L.p % 8 == 0 else "ghost_norm_kernel"
+        # 8 | p: the id join; else the masked Gram
+        return "embed_join_kernel" if L.T <= 16384 and L.p % 8 == 0 else "ghost_norm_kernel"
     if 2 * L.T * L.T < L.p * L.d:
         if dtype != "bf16" or L.T <= 128:
             return "ghost_norm_kernel"

@@ -233,8 +233,8 @@ bk_status bk_conv_prep(const bk_conv* convs, int64_t n, bk_dtype dt, int64_t B, 
  *   norm_sq[i] = sum_{t,t'} [x_it == x_it'] <g_it, g_it'>.
  *   ids [B,T] int64, g [B,T,p] (dtype dt), norm_sq [B] out.
  * An id outside [0, V) has an all-zero one-hot row: its token adds nothing
- * (here and in bk_embed_weighted_grad).  For 128 < T <= 16384 with p a
- * multiple of 8 and g 16-byte aligned it is computed as a join on the ids,
+ * (here and in bk_embed_weighted_grad).  For T <= 16384 with p a multiple
+ * of 8 and g 16-byte aligned it is computed as a join on the ids,
  * sum_v ||sum_{t : x_it = v} g_it||^2 (each row of g read once); otherwise
  * as the Gram of g masked by id equality. */
 bk_status bk_embed_ghost_norm(const int64_t* ids, const void* g, bk_dtype dt, int64_t B,

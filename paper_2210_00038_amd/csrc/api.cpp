@@ -164,11 +164,11 @@ void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
             np.var = L.T <= 2 * bk::kSuper ? 2 : 3;
             np.npart = np.var == 2 ? 1 : nsb * nsb;
         }
-        // An embedding with T > 128 (more than one super block): the id join
-        // (every row of g read once) instead of the masked Gram, one partial
-        // per chunk of 8 ct columns of g (variant 2: ct = 8, 3: ct = 32).
-        if (np.path == Path::Embed && L.T > bk::kSuper && L.T <= bk::kEmbedJoinMaxT && aligned16(L.g) &&
-            L.p % 8 == 0) {
+        // An embedding with rows of g in 16-byte multiples: the id join
+        // (every row of g read once, no T x T work) instead of the masked
+        // Gram, one partial per chunk of 8 ct columns of g (variant 2: ct =
+        // 8, 3: ct = 32).
+        if (np.path == Path::Embed && L.T >= 1 && L.T <= bk::kEmbedJoinMaxT && aligned16(L.g) && L.p % 8 == 0) {
             const int ct = bk::embed_join_ct(L.p);
             np.var = ct == 8 ? 2 : 3;
             np.npart = cdiv(L.p, 8 * ct);

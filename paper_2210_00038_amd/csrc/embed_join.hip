@@ -5,8 +5,9 @@
 //
 // Instead of the T x T Gram of g masked by id equality (2 T^2 p MFMA work,
 // ghost_norm.hip), the tokens of a sample are grouped by id and each group's
-// rows of g are summed once: T p additions, every row of g read once.  Used
-// for T > 128, where the masked Gram needs several super-block pairs.
+// rows of g are summed once: T p additions, every row of g read once.  The
+// masked Gram remains for rows of g that are not 16-byte multiples and for T
+// past the keys the LDS holds.
 //
 // One 1024-thread workgroup owns (layer, sample, chunk of 8 CT columns of g):
 //  1. the sample's keys (id << 32 | t) are sorted in LDS (bitonic); ids

@@ -75,7 +75,7 @@ hipError_t launch_embed_join(const GhostArgs& a, int n_wg, bool, int ct, hipStre
     monotone(a.L, a.n, kMaxGhost, n_wg, "join descriptors");
     need(ct == 8 || ct == 32, "join column threads");
     for (int k = 0; k < a.n; ++k) {
-        need(a.L[k].T > kSuper && a.L[k].T <= kEmbedJoinMaxT && a.L[k].p % 8 == 0, "join shape");
+        need(a.L[k].T >= 1 && a.L[k].T <= kEmbedJoinMaxT && a.L[k].p % 8 == 0, "join shape");
         need((int64_t)a.L[k].npairs * 8 * ct >= a.L[k].p, "join column chunks");
         in_ws(a.part, a.L[k].part_off, (int64_t)a.B * a.L[k].npairs, 4, "join partials");
     }

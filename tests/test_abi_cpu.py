@@ -75,10 +75,11 @@ def test_workspace_sizes():
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_WEIGHTED_GRAD, bk.BK_BF16, 16, 256, 50257, p) == \
         2 * al(n * 8) + al(256 * (n // 1024) * 4) + al(2 * (n // 64) * p * 4) + al((n // 64) * 4)
     # embedding norm: the larger of the masked Gram's super-block pairs (128-row blocks) and,
-    # for T > 128 with p % 8 == 0, the id join's column chunks of g (256 columns when p >= 256,
-    # else 64), whichever the alignment of g picks at the call
+    # with p % 8 == 0, the id join's column chunks of g (256 columns when p >= 256, else 64),
+    # whichever the alignment of g picks at the call
     al4 = lambda n: (n * 4 + 255) // 256 * 256
-    assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_BF16, 16, 128, 50257, 1280) == al4(16)
+    assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_BF16, 16, 128, 50257, 1280) == al4(16 * 5)
+    assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_BF16, 16, 128, 50257, 60) == al4(16)
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_BF16, 16, 256, 50257, 1280) == al4(16 * 5)
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_BF16, 16, 256, 50257, 200) == al4(16 * 4)
     assert bk.bk_workspace_size(bk.BK_OP_EMBED_GHOST_NORM, bk.BK_F32, 2, 1024, 1000, 72) == al4(2 * 36)

@@ -184,10 +184,12 @@ def _embed_norm_ref(ids, g, V):
     return oracle.embed_norm_sq(inv.reshape(ids.shape), gv, len(uniq))
 
 
-# Embedding norms with T > 128 run as a join on the token ids (sorted per
-# sample, each id's rows of g summed once); p % 8 != 0 or T past the join's
-# limit keep the masked Gram.
+# Embedding norms run as a join on the token ids (sorted per sample, each
+# id's rows of g summed once); p % 8 != 0 or T past the join's limit keep the
+# masked Gram.
 @pytest.mark.parametrize("B,T,V,p,dtype,kind", [
+    (4, 1, 9, 16, torch.bfloat16, "uniform"),         # one token per sample
+    (3, 40, 6, 24, torch.float32, "uniform"),         # fewer positions than segments
     (3, 129, 50, 64, torch.bfloat16, "zipf"),         # just past one 128-row super block
     (2, 256, 50257, 1280, torch.bfloat16, "zipf"),    # the GPT-2-large embedding's shape
     (2, 400, 300, 264, torch.bfloat16, "zipf"),       # 256-column chunks, the last one of 8 columns
