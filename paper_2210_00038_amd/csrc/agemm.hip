@@ -160,6 +160,56 @@ __device__ __forceinline__ void put_col16(float* out, size_t sm, size_t sn, int 
     }
 }
 
+// 4 x 4 transpose inside each quad of lanes (DPP quad permutations): lane j
+// of a quad holds v[r] = M[r][j] for the quad's four columns and ends with
+// v[c] = M[j][c].  Two exchange steps, between lanes j ^ 1 and then j ^ 2.
+__device__ __forceinline__ float dpp_xor1(float a) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a), 0xB1, 0xF, 0xF, false));   // [1,0,3,2]
+}
+__device__ __forceinline__ float dpp_xor2(float a) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a), 0x4E, 0xF, 0xF, false));   // [2,3,0,1]
+}
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int lane) {
+    const bool o1 = (lane & 1) != 0, o2 = (lane & 2) != 0;
+    const float p0 = dpp_xor1(v[0]), p1 = dpp_xor1(v[1]), p2 = dpp_xor1(v[2]), p3 = dpp_xor1(v[3]);
+    const float u0 = o1 ? p1 : v[0], u1 = o1 ? v[1] : p0, u2 = o1 ? p3 : v[2], u3 = o1 ? v[3] : p2;
+    const float q0 = dpp_xor2(u0), q1 = dpp_xor2(u1), q2 = dpp_xor2(u2), q3 = dpp_xor2(u3);
+    v[0] = o2 ? q2 : u0;
+    v[1] = o2 ? q3 : u1;
+    v[2] = o2 ? u2 : q0;
+    v[3] = o2 ? u3 : q1;
+}
+
+// put_col16 with 16-byte stores: the 32x32 accumulator block at (r0, c0) of
+// out (row stride ld floats) times `scale` (or added to out), rows below
+// rmax.  Each group of four rows is transposed inside the lane quads, so a
+// lane writes four consecutive columns of one row.  Needs out 16-byte aligned
+// and ld and c0 multiples of 4; columns past cmax (a multiple of 4) are
+// skipped.  Every element gets the same operations as in put_col16.
+__device__ __forceinline__ void put_acc_x4(float* out, size_t ld, int r0, int rmax, int c0, int cmax, int lane,
+                                           const f32x16_t& acc, float scale, bool add) {
+#pragma clang fp contract(off)
+    const int c = c0 + ((lane & 31) & ~3);
+    const int rl = 4 * ((lane >> 5) & 1) + (lane & 3);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        float v[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        quad_transpose(v, lane);
+        const int r = r0 + 8 * q + rl;
+        if (r < rmax && c < cmax) {
+            float4* dst = reinterpret_cast<float4*>(out + (size_t)r * ld + (size_t)c);
+            float4 o;
+            if (add) {
+                const float4 g = *dst;
+                o = make_float4(g.x + v[0] * scale, g.y + v[1] * scale, g.z + v[2] * scale, g.w + v[3] * scale);
+            } else {
+                o = make_float4(v[0] * scale, v[1] * scale, v[2] * scale, v[3] * scale);
+            }
+            *dst = o;
+        }
+    }
+}
+
 template <typename T, bool INST, bool VEC>
 __global__ __launch_bounds__(256) void agemm_kernel(const GemmArgs args) {
     using Cfg = GemmCfg<T>;
@@ -333,14 +383,11 @@ __device__ __forceinline__ uint2 frag_tr_half(const char* lds, int kb, int cb, i
 template <int TM, int TN>
 __device__ __forceinline__ void store_partial_tile(float* P, const f32x16_t (&acc)[4][2], int r0, int c0,
                                                    int lane, float scale) {
+    static_assert(TN % 4 == 0, "16-byte rows");
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) {
-            const int n = c0 + 32 * y + (lane & 31);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) P[(r0 + 32 * x + acc_row(i, lane)) * TN + n] = acc[x][y][i] * scale;
-        }
+        for (int y = 0; y < 2; ++y) put_acc_x4(P, TN, r0 + 32 * x, TM, c0 + 32 * y, TN, lane, acc[x][y], scale, false);
 }
 
 // Two bf16 in one word, each multiplied by c, rounded to nearest even.
@@ -1183,6 +1230,16 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     }
     float* G = L.G;
     const bool add = L.accum != 0;
+    // 16-byte stores when G allows them (p is a multiple of 8 here).
+    if ((reinterpret_cast<uintptr_t>(G) & 15u) == 0) {
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+                put_acc_x4(G, (size_t)p, m0 + 128 * wm + 32 * x, d, n0 + 64 * wn + 32 * y, p, lane, acc[x][y], c_last,
+                           add);
+        return;
+    }
 #pragma unroll
     for (int x = 0; x < 4; ++x)
 #pragma unroll
