@@ -24,6 +24,8 @@
 //  4. a fixed-order block sum gives the chunk's partial; the host's
 //     reduction adds the chunks of a sample in order.
 // Every step has a fixed order: the result is bitwise reproducible.
+#include <atomic>
+
 #include "bk_device.h"
 #include "bk_kernels.h"
 
@@ -219,9 +221,15 @@ hipError_t launch_embed_join(const GhostArgs& args, int n_wg, bool bf16, int ct,
                                      : reinterpret_cast<const void*>(&embed_join_kernel<bf16_t, 32>))
                           : (ct == 8 ? reinterpret_cast<const void*>(&embed_join_kernel<float, 8>)
                                      : reinterpret_cast<const void*>(&embed_join_kernel<float, 32>));
-    if (lds > 65536) {
+    // Dynamic LDS past 64 KB is allowed per kernel once (the largest size
+    // granted so far is remembered, so a call under stream capture sets
+    // nothing).
+    static std::atomic<size_t> granted[4];
+    std::atomic<size_t>& gr = granted[(bf16 ? 2 : 0) + (ct == 8 ? 0 : 1)];
+    if (lds > 65536 && lds > gr.load(std::memory_order_relaxed)) {
         const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
+        gr.store(lds, std::memory_order_relaxed);
     }
     const dim3 grid(n_wg), block(kJoinThreads);
     if (bf16) {
