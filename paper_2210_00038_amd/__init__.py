@@ -423,9 +423,10 @@ def make_layers(specs: Sequence[dict]):
     accumulate (optional bool)}.
 
     x is a [B,T,d] for a linear layer, int64 ids [B,T] for an embedding, or the
-    normalized input [B,T,p] of an affine layer; the tensors must stay alive
-    while the array is used."""
+    normalized input [B,T,p] of an affine layer.  The array holds references
+    to the tensors, so they stay allocated while it is in use."""
     arr = (bk_layer * max(1, len(specs)))()
+    arr._tensors = [s.get(k) for s in specs for k in ("x", "g", "G", "P", "Gb", "Pb") if s.get(k) is not None]
     for k, s in enumerate(specs):
         x, g = _dev(s["x"], "x"), _dev(s["g"], "g")
         G = s.get("G")

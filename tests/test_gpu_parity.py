@@ -124,7 +124,8 @@ def test_long_ghost_norm(bk, B, T, d, p):
     assert out[B - 1] == 0.0
     assert _rel(out[:B - 1], ref[:B - 1]) <= 1e-4
     a2, g2 = _pair(B, 200, 768, 256, torch.bfloat16, seed=T + 5)
-    arr = bk.make_layers([{"kind": bk.BK_LINEAR, "x": x, "g": y} for x, y in ((da, dg), (a2.to(DEV), g2.to(DEV)))])
+    da2, dg2 = a2.to(DEV), g2.to(DEV)
+    arr = bk.make_layers([{"kind": bk.BK_LINEAR, "x": x, "g": y} for x, y in ((da, dg), (da2, dg2))])
     norm_sq = torch.empty(2, B, device=DEV)
     bk.bk_layer_norms(arr, 2, bk.BK_BF16, B, norm_sq)
     got = norm_sq.cpu().numpy()
