@@ -6,12 +6,14 @@
 #include <cstdio>
 #include <cstdlib>
 #include <random>
+#include <map>
 #include <vector>
 
 #include "bk.h"
 
 extern uintptr_t g_ws_lo, g_ws_hi;
 extern long g_launches;
+extern std::map<uintptr_t, int> g_noised;
 
 namespace {
 std::mt19937_64 rng(20221001);
@@ -25,6 +27,23 @@ void* set_ws(size_t bytes) {
 int64_t dim() { return pick({1, 2, 7, 8, 16, 24, 32, 60, 64, 100, 128, 256, 264, 300, 768, 1024, 1280, 3072, 4096}); }
 int64_t tlen() { return pick({0, 1, 16, 49, 64, 70, 100, 128, 129, 197, 256, 300, 784, 1000, 1024, 4096, 16385}); }
 }  // namespace
+
+// Every weight and bias gradient with elements got its noise from exactly one
+// launch (none without noise), and nothing else got any.
+bool noised_once(const std::vector<bk_layer>& L, float sig) {
+    std::map<uintptr_t, int> want;
+    if (sig != 0.f)
+        for (const bk_layer& y : L) {
+            if ((y.kind == BK_NORM_AFFINE ? y.p : y.d * y.p) > 0) ++want[reinterpret_cast<uintptr_t>(y.G)];
+            if ((y.flags & BK_LAYER_BIAS) && y.p > 0) ++want[reinterpret_cast<uintptr_t>(y.Gb)];
+        }
+    if (want != g_noised) {
+        std::fprintf(stderr, "noise launches per tensor: %zu tensors expected, %zu noised\n", want.size(),
+                     g_noised.size());
+        return false;
+    }
+    return true;
+}
 
 int main() {
     // 1. workspace queries: random, edge and invalid sizes for every op
@@ -82,8 +101,11 @@ int main() {
         ++calls;
         ok_calls += bk_layer_norms(L.data(), n, dt, B, norm, set_ws(wn), wn, nullptr) == BK_OK;
         (void)bk_weighted_grads(L.data(), n, C, dt, B, set_ws(wg), wg, nullptr);
-        (void)bk_private_grad(L.data(), n, dt, B, (bk_clip)(rng() % 2), 1.f, 0.01f, rng() % 2 ? 1.f : 0.f, 7,
-                              (uint32_t)it, norm, C, tot, set_ws(wp), wp, nullptr);
+        const float sig = rng() % 2 ? 1.f : 0.f;
+        g_noised.clear();
+        const bk_status pst = bk_private_grad(L.data(), n, dt, B, (bk_clip)(rng() % 2), 1.f, 0.01f, sig, 7,
+                                              (uint32_t)it, norm, C, tot, set_ws(wp), wp, nullptr);
+        if (pst == BK_OK && !noised_once(L, sig)) return 1;
         if (wp > 0 && bk_private_grad(L.data(), n, dt, B, BK_CLIP_AUTO, 1.f, 0.01f, 1.f, 7, 0, norm, C, tot,
                                       set_ws(wp), wp - 1, nullptr) == BK_OK) {
             std::fprintf(stderr, "a short workspace was accepted\n");

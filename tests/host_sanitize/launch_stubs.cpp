@@ -4,16 +4,20 @@
 // GPU.  Each launcher checks what the host hands to the kernels: descriptor
 // counts within the argument tables, first-workgroup offsets that never
 // decrease, and every workspace range the kernels would write inside the
-// workspace the caller passed (set by the driver).
+// workspace the caller passed (set by the driver).  The noise launcher also
+// counts, per tensor, the launches that add Gaussian noise to it, so that the
+// driver can check that every gradient gets its noise exactly once.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
 #include <cstdlib>
+#include <map>
 
 #include "bk_kernels.h"
 
 uintptr_t g_ws_lo = 0, g_ws_hi = 0;   // [lo, hi): the caller's workspace
 long g_launches = 0;
+std::map<uintptr_t, int> g_noised;    // tensor -> launches that add noise to it
 
 namespace {
 void need(bool ok, const char* what) {
@@ -127,6 +131,7 @@ hipError_t launch_noise(const NoiseArgs& a, int n_wg, hipStream_t) {
     for (int k = 0; k < a.n; ++k) {
         need(a.L[k].wg_begin >= prev && (int64_t)a.L[k].wg_begin < n_wg && a.L[k].n > 0, "noise layers");
         prev = a.L[k].wg_begin;
+        ++g_noised[reinterpret_cast<uintptr_t>(a.L[k].G)];
     }
     return hipSuccess;
 }
