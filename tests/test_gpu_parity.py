@@ -590,6 +590,8 @@ def test_weighted_grad_k_split(bk, B, T, d, p, zero):
     ([(768, 4096)] * 6, 16, 70, [3]),         # register-staged kernel (64-row stages)
     ([(768, 768)], 40, 70, []),               # the same, all split
     ([(768, 768)], 3, 200, []),               # too few stages per slice: not split
+    ([(4096, 6400)], 2, 128, [1]),            # 400 tiles of 8 stages: a last round over half full, not split
+    ([(4096, 6400)], 1, 64, []),              # tiles of 2 stages (the prologue loads one past the end)
 ])
 def test_weighted_grads_tail_split(bk, shapes, B, T, zero):
     gen = torch.Generator().manual_seed(B * T + len(shapes))
