@@ -221,15 +221,20 @@ hipError_t launch_embed_join(const GhostArgs& args, int n_wg, bool bf16, int ct,
                                      : reinterpret_cast<const void*>(&embed_join_kernel<bf16_t, 32>))
                           : (ct == 8 ? reinterpret_cast<const void*>(&embed_join_kernel<float, 8>)
                                      : reinterpret_cast<const void*>(&embed_join_kernel<float, 32>));
-    // Dynamic LDS past 64 KB is allowed per kernel once (the largest size
-    // granted so far is remembered, so a call under stream capture sets
-    // nothing).
-    static std::atomic<size_t> granted[4];
-    std::atomic<size_t>& gr = granted[(bf16 ? 2 : 0) + (ct == 8 ? 0 : 1)];
-    if (lds > 65536 && lds > gr.load(std::memory_order_relaxed)) {
-        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        gr.store(lds, std::memory_order_relaxed);
+    // Dynamic LDS past 64 KB is allowed per kernel and device once (the
+    // largest size granted so far on the current device is remembered, so a
+    // later call, under stream capture for instance, sets nothing).
+    constexpr int kMaxDev = 64;
+    static std::atomic<size_t> granted[kMaxDev][4];
+    if (lds > 65536) {
+        int dev = -1;
+        const bool known = hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxDev;
+        std::atomic<size_t>* gr = known ? &granted[dev][(bf16 ? 2 : 0) + (ct == 8 ? 0 : 1)] : nullptr;
+        if (!gr || lds > gr->load(std::memory_order_relaxed)) {
+            const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            if (gr) gr->store(lds, std::memory_order_relaxed);
+        }
     }
     const dim3 grid(n_wg), block(kJoinThreads);
     if (bf16) {
