@@ -152,6 +152,14 @@ def test_empty_batch_and_tokens(bk):
     C = torch.ones(3, device=DEV)
     G = bk.bk_weighted_grad(a, g, C)
     assert G.shape == (8, 4) and torch.count_nonzero(G).item() == 0
+    # bf16: no samples on the LDS-DMA kernel (its tiles run no stage), no tokens on the wide one
+    for B, T in [(0, 128), (2, 0)]:
+        a = torch.zeros(B, T, 768, dtype=torch.bfloat16, device=DEV)
+        g = torch.zeros(B, T, 512, dtype=torch.bfloat16, device=DEV)
+        G = torch.full((768, 512), float("nan"), device=DEV)
+        bk.bk_weighted_grad(a, g, torch.ones(B, device=DEV), G=G)
+        assert torch.count_nonzero(G).item() == 0, (B, T)
+        assert bk.bk_ghost_norm(a, g).cpu().tolist() == [0.0] * B
 
 
 @pytest.mark.parametrize("B,T,V,p,dtype", [
