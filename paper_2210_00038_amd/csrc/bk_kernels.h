@@ -122,14 +122,8 @@ constexpr int kNoiseBlocksPerWG = 4 * 256;   // most counter blocks handled by o
 enum class GemmVariant { Scalar = 0, Vec = 1, Wide = 2, Grad = 3, GradDL = 4, Narrow32 = 5, Narrow64 = 6 };
 constexpr int kGemmVariants = 7;
 constexpr int kDMaxB = 4096;
-#ifndef BK_DL_KS
-#define BK_DL_KS 32
-#endif
-#ifndef BK_DL_NB
-#define BK_DL_NB 4
-#endif
-constexpr int kDLStageRows = BK_DL_KS;   // k rows per stage of the GradDL kernel
-constexpr int kDLBuffers = BK_DL_NB;     // its LDS stage buffers
+constexpr int kDLStageRows = 32;   // k rows per stage of the GradDL kernel
+constexpr int kDLBuffers = 4;      // its LDS stage buffers (the ping-pong schedule takes four)
 // Output tiles of the a^T g kernels (plan.cpp and the kernels share them):
 // 256 x 128 with 64-row stages (Wide), 256 x 256 (Grad, GradDL), 256 along
 // the long side (Narrow); the Scalar / Vec tiles are kTile x kTile.
