@@ -103,10 +103,11 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // Wait until at most N of this wave's vector-memory operations (loads,
-// including loads into LDS) are outstanding.  They complete in order.
+// including loads into LDS, and stores) are outstanding.  They complete in
+// order.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 16, "vmcnt immediate");
+    static_assert(N >= 0 && N < 64, "vmcnt immediate (6 bits)");
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
