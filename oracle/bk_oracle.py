@@ -12,6 +12,11 @@ What is computed, and where the paper defines it
 ------------------------------------------------
 * use_ghost             -- Section 3.2 (layerwise decision / mixed ghost norm):
                            ghost norm iff 2 T^2 < p d, instantiate otherwise.
+* use_ghost_time        -- the same decision by time instead of space (Table
+                           "block complexity", time row: 2BT^2(p+d) for the
+                           ghost norm, 2BTpd for instantiation): ghost norm
+                           iff T (p + d) < p d.  An option beside the paper's
+                           rule; both give the same norms.
 * linear_norm_sq        -- per-sample squared gradient norm ||a_i^T g_i||_F^2,
                            the left-hand side of eq. (ghost norm) in Section 2.1
                            and the per-sample gradient of App. B.4.1.  This is
@@ -81,7 +86,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
-    "use_ghost", "linear_norm_sq", "linear_norm_sq_gram", "linear_norm_sq_bruteforce",
+    "use_ghost", "use_ghost_time", "linear_norm_sq", "linear_norm_sq_gram", "linear_norm_sq_bruteforce",
     "embed_norm_sq", "embed_norm_sq_pairs", "aggregate", "clip_factors", "weighted_grad",
     "embed_weighted_grad", "philox4x32_10", "philox_words", "uniforms_from_words",
     "box_muller", "noise", "noise_at", "add_noise", "PHILOX_M0", "PHILOX_M1", "PHILOX_W0", "PHILOX_W1",
@@ -121,6 +126,13 @@ def use_ghost(T: int, d: int, p: int) -> bool:
     """Ghost norm iff 2 T^2 < p d (space of the two Grams vs one per-sample
     gradient, Table "block complexity"); ties instantiate."""
     return 2 * int(T) * int(T) < int(p) * int(d)
+
+
+def use_ghost_time(T: int, d: int, p: int) -> bool:
+    """Ghost norm iff T (p + d) < p d: the time of forming the two T x T Grams,
+    2 B T^2 (p + d), against that of instantiating every per-sample gradient,
+    2 B T p d (Table "block complexity", time row); ties instantiate."""
+    return int(T) * (int(p) + int(d)) < int(p) * int(d)
 
 
 # --------------------------------------------------------------------------
@@ -479,7 +491,7 @@ def bk_layer_norm(layer_kind: str, x, g, V: int = 0, bias: bool = False) -> np.n
 
 
 def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed: int,
-             step: int = 0, with_noise: bool = True, mixopt: bool = False):
+             step: int = 0, with_noise: bool = True, mixopt: bool = False, rule=None):
     """layers: objects with .kind, .T, .d, .p; inputs: list of (a or ids, g).
 
     Returns dict with per-layer norms [L, B], totals [B], C [B], the clipped
@@ -487,10 +499,14 @@ def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed
     mixopt: BK-MixOpt -- a linear layer that instantiates (2 T^2 >= p d) keeps
     its per-sample gradients and forms G_l as their weighted sum (App. B.5);
     every other layer takes the book-keeping GEMM a^T diag(C) g.
+    rule: the layerwise decision (default use_ghost; use_ghost_time for the
+    decision by time).  It changes which way a layer is computed, and the
+    "paths" entry, not the values.
     A layer with a true .bias attribute also has a bias (a "norm" layer: a
     beta); its clipped gradient sum_i C_i s_i is returned in Gb[l] (None
     otherwise) and noised with tensor id BIAS_TENSOR | l.  A "norm" layer's
     G_l is its gamma gradient sum_i C_i u_i."""
+    rule = use_ghost if rule is None else rule
     bias = [bool(getattr(L, "bias", False)) for L in layers]
     norms = np.stack([bk_layer_norm(L.kind, x, g, L.d, b) for L, (x, g), b in zip(layers, inputs, bias)])
     total = aggregate(norms)
@@ -501,7 +517,7 @@ def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed
             Gl = embed_weighted_grad(x, g, C, L.d)
         elif L.kind == "norm":
             Gl = weighted_sum(norm_affine_sums(x, g)[0], C)
-        elif mixopt and not use_ghost(L.T, L.d, L.p):
+        elif mixopt and not rule(L.T, L.d, L.p):
             Gl = weighted_sum(per_sample_grads(x, g), C)
         else:
             Gl = weighted_grad(x, g, C)
@@ -513,7 +529,7 @@ def bk_stack(layers, inputs, mode: str, R: float, gamma: float, std: float, seed
             Gbhat.append(add_noise(Gbl, std, seed, BIAS_TENSOR | l, step) if bias[l] else None)
     return {"norms": norms, "total": total, "C": C, "G": G, "Ghat": Ghat, "Gb": Gb, "Gbhat": Gbhat,
             "paths": [("embed" if L.kind == "embed" else "norm" if L.kind == "norm" else
-                       ("ghost" if use_ghost(L.T, L.d, L.p) else "inst")) for L in layers]}
+                       ("ghost" if rule(L.T, L.d, L.p) else "inst")) for L in layers]}
 
 
 def logical_batch(layers, batches, mode: str, R: float, gamma: float, std: float, seed: int,

@@ -125,6 +125,85 @@ def test_use_ghost_rule_and_tie():
     assert oracle.use_ghost(31, 32, 64)
 
 
+def _counted_norms(a, g):
+    """One sample's squared gradient norm both ways in counted loops: the two
+    Grams and their inner product, and the instantiated gradient and its
+    squared sum.  Returns (ghost value, instantiated value, multiply-adds of
+    the Grams, multiply-adds of the gradient)."""
+    T, d, p = len(a), len(a[0]), len(g[0])
+    mac_gram = mac_inst = 0
+    Ga = [[0.0] * T for _ in range(T)]
+    Gg = [[0.0] * T for _ in range(T)]
+    for i in range(T):
+        for j in range(T):
+            for k in range(d):
+                Ga[i][j] += a[i][k] * a[j][k]
+                mac_gram += 1
+            for q in range(p):
+                Gg[i][j] += g[i][q] * g[j][q]
+                mac_gram += 1
+    ghost = sum(Ga[i][j] * Gg[i][j] for i in range(T) for j in range(T))
+    inst = 0.0
+    for k in range(d):
+        for q in range(p):
+            s = 0.0
+            for t in range(T):
+                s += a[t][k] * g[t][q]
+                mac_inst += 1
+            inst += s * s
+    return ghost, inst, mac_gram, mac_inst
+
+
+def test_use_ghost_time_picks_fewer_counted_multiply_adds():
+    # The time rule takes the ghost norm exactly when forming the two Grams
+    # costs fewer multiply-adds than forming the per-sample gradient (ties
+    # instantiate); both ways give the norm of the definition.
+    seen = set()
+    for T in (1, 2, 3, 4, 6):
+        for d in (1, 2, 3, 4, 6, 12):
+            for p in (1, 2, 4, 6, 12):
+                a, g = _rand(T, d), _rand(T, p)
+                ghost, inst, mg, mi = _counted_norms(a.tolist(), g.tolist())
+                ref = oracle.linear_norm_sq(a[None], g[None])[0]
+                assert ghost == pytest.approx(ref, rel=1e-12) and inst == pytest.approx(ref, rel=1e-12)
+                assert oracle.use_ghost_time(T, d, p) == (mg < mi), (T, d, p)
+                seen.add((mg < mi, mg == mi))
+    assert seen == {(True, False), (False, False), (False, True)}   # both outcomes and a tie
+
+
+def test_use_ghost_time_closed_forms_and_space_rule():
+    # d == p: ghost iff T < d / 2; T == 1: ghost iff p + d < p d.
+    for d in range(1, 40):
+        for T in range(0, 40):
+            assert oracle.use_ghost_time(T, d, d) == (2 * T < d)
+    for d in range(1, 12):
+        for p in range(1, 12):
+            assert oracle.use_ghost_time(1, d, p) == (p + d < p * d)
+    # T (p + d) < p d forces T < min(p, d) and then 2 T^2 < p d / 2: ghost by
+    # time is ghost by space, never the other way round.
+    rs = np.random.default_rng(7)
+    for _ in range(20000):
+        T, d, p = (int(v) for v in rs.integers(0, 5000, 3))
+        if oracle.use_ghost_time(T, d, p):
+            assert oracle.use_ghost(T, d, p)
+    # GPT-2 MLP up-projection at T = 1024: ghost by space, instantiated by time.
+    assert oracle.use_ghost(1024, 768, 3072) and not oracle.use_ghost_time(1024, 768, 3072)
+    assert not oracle.use_ghost_time(2, 4, 4)          # tie 16 == 16 instantiates
+    assert oracle.use_ghost_time(1, 4, 4)
+
+
+def test_stack_rule_changes_paths_not_values():
+    class L:
+        kind, T, d, p = "linear", 4, 6, 6         # space: ghost (32 < 36); time: inst (48 >= 36)
+    a, g = _rand(3, 4, 6), _rand(3, 4, 6)
+    r_space = oracle.bk_stack([L], [(a, g)], "auto", 1.0, 0.01, 0.0, 1, with_noise=False, mixopt=True)
+    r_time = oracle.bk_stack([L], [(a, g)], "auto", 1.0, 0.01, 0.0, 1, with_noise=False, mixopt=True,
+                             rule=oracle.use_ghost_time)
+    assert r_space["paths"] == ["ghost"] and r_time["paths"] == ["inst"]
+    np.testing.assert_allclose(r_time["G"][0], r_space["G"][0], rtol=1e-12)
+    np.testing.assert_array_equal(r_time["norms"], r_space["norms"])
+
+
 def _ghost_term(d, blocks, T, B, rule):
     tot = 0
     for (di, pi) in [(d, 3 * d), (d, d), (d, 4 * d), (4 * d, d)]:
