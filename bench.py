@@ -16,7 +16,7 @@ dominant kernel measured with HIP events on the launch stream over the timed
 steps, and the float64 CPU oracle timed on a bounded sample of the same
 workload on the host.
 
-    python bench.py [--steps K] [--warmup W] [--workload N] [--mixopt] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--workload N] [--mixopt] [--time-rule] [--gpus 1]
 
 Defaults: 50 timed steps.  Before them a ramp of untimed steps fills 100 ms of
 GPU time (reported as `warmup_ramp`), then --warmup more untimed steps run
@@ -48,7 +48,13 @@ def true_d(L: wl.Layer) -> int:
     return L.conv[0] * L.conv[1] ** 2 if L.kind == "conv" else L.d
 
 
-def algorithmic_work(w: wl.Workload, mixopt: bool = False):
+def is_ghost(L, time_rule: bool = False) -> bool:
+    """The layerwise decision on the padded width: by space, 2T^2 < pd (the
+    paper's), or by time, T(p+d) < pd (the option BK_LAYER_TIME_RULE)."""
+    return L.T * (L.p + L.d) < L.p * L.d if time_rule else 2 * L.T * L.T < L.p * L.d
+
+
+def algorithmic_work(w: wl.Workload, mixopt: bool = False, time_rule: bool = False):
     """Per-step algorithmic flops / bytes of each phase (paper's per-module costs).
     mixopt: instantiated layers keep their per-sample gradients (written by the
     norm phase, 4Bpd bytes) and form G as their weighted sum (2Bpd flops,
@@ -87,7 +93,7 @@ def algorithmic_work(w: wl.Workload, mixopt: bool = False):
             out["norm_bytes"] += B * L.T * (L.p * es + 8)
             out["gemm_bytes"] += B * L.T * (L.p * es + 8) + 4.0 * L.d * L.p
         else:
-            ghost = 2 * L0.T * L0.T < L0.p * L0.d        # the decision sees the padded width
+            ghost = is_ghost(L0, time_rule)              # the decision sees the padded width
             if ghost:
                 out["ghost_layers"] += 1
                 out["norm_flops"] += 2.0 * B * L.T * L.T * (L.p + L.d)       # ghost norm, App. B.4
@@ -226,12 +232,12 @@ def _narrow(L) -> bool:
     return min(L.d, L.p) <= 64 and max(L.d, L.p) >= 128
 
 
-def norm_kernel(L, dtype: str = "bf16") -> str:
+def norm_kernel(L, dtype: str = "bf16", time_rule: bool = False) -> str:
     """Kernel that takes layer L's norm (the library's rule for 16-byte rows; a label only)."""
     if L.kind == "embed":
         # 8 | p: the id join; else the masked Gram
         return "embed_join_kernel" if L.T <= 16384 and L.p % 8 == 0 else "ghost_norm_kernel"
-    if 2 * L.T * L.T < L.p * L.d:
+    if is_ghost(L, time_rule):
         if dtype != "bf16" or L.T <= 128:
             return "ghost_norm_kernel"
         return "ghost_full_kernel" if L.T <= 256 else "ghost_long_kernel"
@@ -254,12 +260,12 @@ def grad_kernel(L, dtype: str = "bf16") -> str:
     return "agrad_dl_kernel" if 8 * (-(-L.T // 16) * 16) <= 9 * L.T else "agrad_bf16_kernel"
 
 
-def dominant_kernel(w: wl.Workload, phase: str) -> str:
+def dominant_kernel(w: wl.Workload, phase: str, time_rule: bool = False) -> str:
     """Kernel with the largest share of a phase's paper-count flops."""
     share = {}
     for L in w.layers:
         if phase == "norms":
-            k = norm_kernel(L, w.dtype)
+            k = norm_kernel(L, w.dtype, time_rule)
             f = 2.0 * L.T * L.T * (L.p + L.d) if k.startswith("ghost_") else 2.0 * L.T * L.p * L.d
         else:
             k, f = grad_kernel(L, w.dtype), 2.0 * L.T * L.p * L.d
@@ -344,6 +350,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-plain-gemm", action="store_true",
                     help="skip the hipBLASLt plain-GEMM denominator (keeps a kernel trace to the library)")
+    ap.add_argument("--time-rule", action="store_true",
+                    help="choose ghost norm vs instantiation by time, T(p+d) < pd, instead of by space")
     ap.add_argument("--mixopt", action="store_true",
                     help="BK-MixOpt: instantiated layers keep per-sample gradients and sum them")
     ap.add_argument("--accumulate", type=int, default=1,
@@ -375,7 +383,8 @@ def main():
 
     ins, raw, Gs = make_inputs(w, dev)
     K = max(1, args.accumulate)
-    keep = [args.mixopt and L.kind in ("linear", "conv") and not bk.bk_use_ghost(L.T, L.d, L.p)
+    use_ghost = bk.bk_use_ghost_time if args.time_rule else bk.bk_use_ghost
+    keep = [args.mixopt and L.kind in ("linear", "conv") and not use_ghost(L.T, L.d, L.p)
             for L in w.layers]
     Ps = [torch.empty(B, L.p, device=dev) if L.kind == "norm" else
           (torch.empty(B, L.d, L.p, device=dev) if k else None) for L, k in zip(w.layers, keep)]
@@ -386,7 +395,7 @@ def main():
     def layer_array(accumulate: bool):
         return bk.make_layers([{"kind": kinds.get(L.kind, bk.BK_LINEAR), "x": x, "g": g, "G": G, "V": L.d,
                                 "mixopt": args.mixopt, "P": P, "bias": L.bias, "Gb": Gb, "Pb": Pb,
-                                "accumulate": accumulate}
+                                "accumulate": accumulate, "time_rule": args.time_rule}
                                for L, (x, g), G, P, Gb, Pb in zip(w.layers, ins, Gs, Ps, Gbs, Pbs)])
     arr = layer_array(False)
     arr_acc = layer_array(True)      # physical batches 2..K of a logical batch add to G
@@ -473,7 +482,7 @@ def main():
         return out
     ph_ms = np.array([phase_ms(e) for e in evs]).mean(axis=0)
     step_ev = np.array([e[0].elapsed_time(e[-1]) for e in evs])
-    work = algorithmic_work(w, args.mixopt)
+    work = algorithmic_work(w, args.mixopt, args.time_rule)
     work = {k: (v * K if k in ("norm_flops", "norm_bytes", "gemm_flops", "gemm_bytes", "prep_bytes") else v)
             for k, v in work.items()}
     ms_step = elapsed * 1e3 / args.steps
@@ -502,8 +511,9 @@ def main():
     if dom == "prep":
         gk, what = "conv_prep_kernel", "unfold + token-major transpose of every conv layer, one launch"
     else:
-        gk = dominant_kernel(w, dom)
-        kinds = {(grad_kernel if dom == "weighted_grads" else norm_kernel)(L, w.dtype) for L in w.layers}
+        gk = dominant_kernel(w, dom, args.time_rule)
+        kinds = {grad_kernel(L, w.dtype) if dom == "weighted_grads" else norm_kernel(L, w.dtype, args.time_rule)
+                 for L in w.layers}
         what = ("clipped gradients" if dom == "weighted_grads" else "per-sample norms") + \
                (", all layers in one launch" if len(kinds) == 1 else ", one launch per kernel variant")
         if dom == "weighted_grads" and len(kinds) == 1 and all(L.kind != "embed" for L in w.layers) and \
@@ -533,6 +543,7 @@ def main():
         "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "variant": "BK-MixOpt" if args.mixopt else "BK",
+                   "rule": "time" if args.time_rule else "space",
                    "accumulate": K, "logical_batch": K * B,
                    "B": B, "layers": n, "T": sorted({L.T for L in w.layers}),
                    "clip": w.clip, "sigma": w.sigma, "paths": {"ghost": work["ghost_layers"],

@@ -97,8 +97,13 @@ typedef enum { BK_LINEAR = 0, BK_EMBEDDING = 1, BK_NORM_AFFINE = 2 } bk_layer_ki
  *   step's clipped gradients to G (and Gb) instead of overwriting them, each
  *   element in one fixed-order addition.  Each physical batch is clipped on
  *   its own; the caller draws the noise once per logical batch (noise_std 0
- *   in bk_private_grad on all but the last physical batch). */
-enum { BK_LAYER_MIXOPT = 1, BK_LAYER_BIAS = 2, BK_LAYER_ACCUMULATE = 4 };
+ *   in bk_private_grad on all but the last physical batch).
+ *   BK_LAYER_TIME_RULE: a linear layer takes the ghost norm or instantiation
+ *   by bk_use_ghost_time (the time of the two ways) instead of the paper's
+ *   bk_use_ghost (their space).  The norms are the same up to rounding; a
+ *   BK_LAYER_MIXOPT layer keeps P exactly when this rule instantiates.  Other
+ *   kinds ignore the flag. */
+enum { BK_LAYER_MIXOPT = 1, BK_LAYER_BIAS = 2, BK_LAYER_ACCUMULATE = 4, BK_LAYER_TIME_RULE = 8 };
 
 /* One layer of a stack (used by the grouped calls).
  *   kind == BK_LINEAR     : x = a [B, T, d] of dtype dt, g [B, T, p], G [d, p]
@@ -148,6 +153,14 @@ typedef enum {
  * for ghost, 0 for instantiation, -1 for negative sizes.
  * ------------------------------------------------------------------------- */
 int bk_use_ghost(int64_t T, int64_t d, int64_t p);
+
+/* The same decision by time, an option beside the paper's rule (per layer:
+ * BK_LAYER_TIME_RULE): Table "block complexity" prices the ghost norm at
+ * 2BT^2(p+d) and instantiation at 2BTpd, so the ghost norm is used iff
+ * T (p + d) < p d.  Ties instantiate.  A layer this rule sends to the ghost
+ * norm is also sent there by bk_use_ghost, not the other way round.  Pure
+ * host function: 1 ghost, 0 instantiation, -1 for negative sizes. */
+int bk_use_ghost_time(int64_t T, int64_t d, int64_t p);
 
 /* Workspace bytes `op` needs for one layer of these sizes (d = V for the
  * embedding ops).  Returns 0 for an invalid request. */
@@ -306,8 +319,8 @@ bk_status bk_philox_raw(uint64_t seed, uint32_t tensor_id, uint32_t step, uint64
  * ------------------------------------------------------------------------- */
 
 /* Norms of every layer: ghost or instantiated per bk_use_ghost for linear
- * layers, the embedding ghost norm for embedding layers.  norm_sq [n,B] out,
- * row l for layer l. */
+ * layers (bk_use_ghost_time with BK_LAYER_TIME_RULE), the embedding ghost
+ * norm for embedding layers.  norm_sq [n,B] out, row l for layer l. */
 size_t bk_layer_norms_workspace_size(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B);
 bk_status bk_layer_norms(const bk_layer* layers, int64_t n, bk_dtype dt, int64_t B,
                          float* norm_sq, void* ws, size_t ws_bytes, void* stream);

@@ -22,11 +22,11 @@ import torch
 __all__ = [
     "BK_OK", "BK_ERR_INVALID_VALUE", "BK_ERR_NOT_SUPPORTED", "BK_ERR_WORKSPACE", "BK_ERR_LAUNCH",
     "BK_F32", "BK_BF16", "BK_CLIP_ABADI", "BK_CLIP_AUTO", "BK_LINEAR", "BK_EMBEDDING", "BK_NORM_AFFINE",
-    "BK_LAYER_MIXOPT", "BK_LAYER_BIAS", "BK_LAYER_ACCUMULATE", "BK_BIAS_TENSOR",
+    "BK_LAYER_MIXOPT", "BK_LAYER_BIAS", "BK_LAYER_ACCUMULATE", "BK_LAYER_TIME_RULE", "BK_BIAS_TENSOR",
     "BK_OP_GHOST_NORM", "BK_OP_INST_NORM", "BK_OP_EMBED_GHOST_NORM", "BK_OP_WEIGHTED_GRAD",
     "BK_OP_EMBED_WEIGHTED_GRAD", "BKError", "bk_layer", "lib", "LIB_PATH", "EXPORTS",
-    "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
-    "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv",
+    "bk_use_ghost", "bk_use_ghost_time", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm",
+    "bk_embed_ghost_norm", "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv",
     "bk_conv_prep", "make_convs",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise", "bk_philox_raw",
     "bk_add_noise_grouped", "bk_layer_norms", "bk_weighted_grads", "bk_private_grad",
@@ -40,7 +40,7 @@ BK_OK, BK_ERR_INVALID_VALUE, BK_ERR_NOT_SUPPORTED, BK_ERR_WORKSPACE, BK_ERR_LAUN
 BK_F32, BK_BF16 = 0, 1
 BK_CLIP_ABADI, BK_CLIP_AUTO = 0, 1
 BK_LINEAR, BK_EMBEDDING, BK_NORM_AFFINE = 0, 1, 2
-BK_LAYER_MIXOPT, BK_LAYER_BIAS, BK_LAYER_ACCUMULATE = 1, 2, 4
+BK_LAYER_MIXOPT, BK_LAYER_BIAS, BK_LAYER_ACCUMULATE, BK_LAYER_TIME_RULE = 1, 2, 4, 8
 BK_BIAS_TENSOR = 0x80000000
 BK_NOALLOC_SCRATCH_BYTES = 64 << 20
 (BK_OP_GHOST_NORM, BK_OP_INST_NORM, BK_OP_EMBED_GHOST_NORM, BK_OP_WEIGHTED_GRAD,
@@ -50,7 +50,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbk.so")
 
 # Every symbol include/bk.h declares.
 EXPORTS = (
-    "bk_use_ghost", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
+    "bk_use_ghost", "bk_use_ghost_time", "bk_workspace_size", "bk_ghost_norm", "bk_inst_norm", "bk_embed_ghost_norm",
     "bk_per_sample_grads", "bk_weighted_sum", "bk_unfold", "bk_tokens_from_nchw", "bk_conv_prep",
     "bk_clip_factors", "bk_weighted_grad", "bk_embed_weighted_grad", "bk_add_noise",
     "bk_add_noise_grouped", "bk_philox_raw", "bk_layer_norms_workspace_size", "bk_layer_norms", "bk_weighted_grads_workspace_size",
@@ -92,6 +92,7 @@ _st = ctypes.c_int
 _P = ctypes.POINTER(bk_layer)
 _SIG = {
     "bk_use_ghost": (ctypes.c_int, [_i64, _i64, _i64]),
+    "bk_use_ghost_time": (ctypes.c_int, [_i64, _i64, _i64]),
     "bk_workspace_size": (_sz, [ctypes.c_int, ctypes.c_int, _i64, _i64, _i64, _i64]),
     "bk_ghost_norm": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
     "bk_inst_norm": (_st, [_vp, _vp, ctypes.c_int, _i64, _i64, _i64, _i64, _vp, _vp, _sz, _vp]),
@@ -200,6 +201,13 @@ def _out(t: Optional[torch.Tensor], shape, device, dtype=torch.float32) -> torch
 # ------------------------------------------------------------------ per layer
 def bk_use_ghost(T: int, d: int, p: int) -> bool:
     r = lib.bk_use_ghost(T, d, p)
+    if r < 0:
+        raise ValueError("negative size")
+    return bool(r)
+
+
+def bk_use_ghost_time(T: int, d: int, p: int) -> bool:
+    r = lib.bk_use_ghost_time(T, d, p)
     if r < 0:
         raise ValueError("negative size")
     return bool(r)
@@ -420,7 +428,8 @@ def make_layers(specs: Sequence[dict]):
     """ctypes bk_layer array from dicts {kind, x, g, G (optional), V (embedding),
     mixopt (optional bool), P (optional float32 [B,d,p], BK-MixOpt store; [B,p] gamma
     store of an affine layer), bias (optional bool) with Gb [p] and Pb [B,p],
-    accumulate (optional bool)}.
+    accumulate (optional bool), time_rule (optional bool: the layerwise decision
+    by time, bk_use_ghost_time)}.
 
     x is a [B,T,d] for a linear layer, int64 ids [B,T] for an embedding, or the
     normalized input [B,T,p] of an affine layer.  The array holds references
@@ -439,7 +448,8 @@ def make_layers(specs: Sequence[dict]):
             d = x.shape[2]
         arr[k].kind = kind
         arr[k].flags = ((BK_LAYER_MIXOPT if s.get("mixopt") else 0) | (BK_LAYER_BIAS if s.get("bias") else 0) |
-                        (BK_LAYER_ACCUMULATE if s.get("accumulate") else 0))
+                        (BK_LAYER_ACCUMULATE if s.get("accumulate") else 0) |
+                        (BK_LAYER_TIME_RULE if s.get("time_rule") else 0))
         arr[k].T = g.shape[1]
         arr[k].d = d
         arr[k].p = g.shape[2]

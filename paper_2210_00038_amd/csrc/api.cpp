@@ -211,6 +211,12 @@ int32_t ghost_nsb(int64_t T, int var) {
     return (int32_t)cdiv(T, var == 2 ? bk::kFullSub : var == 3 ? bk::kLongSuper : bk::kSuper);
 }
 
+// The layerwise decision of a linear layer: the paper's rule by space, or by
+// time with BK_LAYER_TIME_RULE.
+bool layer_ghost(const bk_layer& L) {
+    return ((L.flags & BK_LAYER_TIME_RULE) ? bk_use_ghost_time(L.T, L.d, L.p) : bk_use_ghost(L.T, L.d, L.p)) == 1;
+}
+
 NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     NormPlan np{};
     if (L.kind == BK_EMBEDDING) {
@@ -218,7 +224,7 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     } else if (L.kind == BK_NORM_AFFINE) {
         np.path = Path::Affine;
     } else {
-        np.path = bk_use_ghost(L.T, L.d, L.p) == 1 ? Path::Ghost : Path::Inst;
+        np.path = layer_ghost(L) ? Path::Ghost : Path::Inst;
     }
     set_norm_variant(np, L, dt);
     finish_norm_plan(np, L, B);
@@ -258,7 +264,7 @@ size_t embed_grad_ws_bytes(int64_t B, int64_t T, int64_t p) { return bk::embed_g
 
 // BK-MixOpt layer that keeps its instantiated per-sample gradients in P.
 bool keeps_grads(const bk_layer& L) {
-    return L.kind == BK_LINEAR && (L.flags & BK_LAYER_MIXOPT) && bk_use_ghost(L.T, L.d, L.p) != 1;
+    return L.kind == BK_LINEAR && (L.flags & BK_LAYER_MIXOPT) && !layer_ghost(L);
 }
 
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -266,7 +272,7 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 bk_status check_layer(const char* fn, const bk_layer& L, int64_t l, int64_t B, bool need_G) {
     if (L.kind != BK_LINEAR && L.kind != BK_EMBEDDING && L.kind != BK_NORM_AFFINE)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld has unknown kind %d", fn, (long long)l, L.kind);
-    if ((L.flags & ~(BK_LAYER_MIXOPT | BK_LAYER_BIAS | BK_LAYER_ACCUMULATE)) != 0)
+    if ((L.flags & ~(BK_LAYER_MIXOPT | BK_LAYER_BIAS | BK_LAYER_ACCUMULATE | BK_LAYER_TIME_RULE)) != 0)
         return fail(BK_ERR_INVALID_VALUE, "%s: layer %lld: unknown flags 0x%x", fn, (long long)l, L.flags);
     bk_status s = check_dims(fn, B, L.T, L.d, L.p);
     if (s != BK_OK) return s;
@@ -904,6 +910,14 @@ int bk_use_ghost(int64_t T, int64_t d, int64_t p) {
     if (T < 0 || d < 0 || p < 0) return -1;
     // 2 T^2 < p d, evaluated without overflow (128-bit products).
     const __int128 lhs = (__int128)2 * T * T;
+    const __int128 rhs = (__int128)p * d;
+    return lhs < rhs ? 1 : 0;
+}
+
+int bk_use_ghost_time(int64_t T, int64_t d, int64_t p) {
+    if (T < 0 || d < 0 || p < 0) return -1;
+    // T (p + d) < p d in 128-bit arithmetic (p + d < 2^64, T < 2^63).
+    const __int128 lhs = (__int128)T * ((__int128)p + d);
     const __int128 rhs = (__int128)p * d;
     return lhs < rhs ? 1 : 0;
 }

@@ -55,7 +55,12 @@ int main() {
         const int64_t d = pick({-1, 0, 1, 8, 60, 768, 50257, 8192, (int64_t)1 << 40});
         const int64_t p = pick({0, 1, 8, 60, 64, 264, 1280, 3072});
         (void)bk_workspace_size(op, dt, B, T, d, p);
-        (void)bk_use_ghost(T, d, p);
+        const int gs = bk_use_ghost(T, d, p), gt = bk_use_ghost_time(T, d, p);
+        if (gt == 1 && gs != 1) {
+            std::fprintf(stderr, "time rule ghost where the space rule is not (T=%lld d=%lld p=%lld)\n",
+                         (long long)T, (long long)d, (long long)p);
+            return 1;
+        }
     }
 
     // 2. random stacks through the grouped calls
@@ -83,6 +88,7 @@ int main() {
                 y.Pb = static_cast<float*>(fake(0x200000 + l));
             }
             if (rng() % 4 == 0) y.flags |= BK_LAYER_ACCUMULATE;
+            if (rng() % 3 == 0) y.flags |= BK_LAYER_TIME_RULE;
             if (y.kind == BK_NORM_AFFINE || (y.kind == BK_LINEAR && rng() % 5 == 0)) {
                 if (y.kind == BK_LINEAR) y.flags |= BK_LAYER_MIXOPT;
                 y.P = static_cast<float*>(fake(0x300000 + l));

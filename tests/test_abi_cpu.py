@@ -40,6 +40,44 @@ def test_use_ghost_rule():
     assert bk.bk_use_ghost(1, 1 << 40, 1 << 40)
 
 
+def test_use_ghost_time_rule():
+    # Table "block complexity" time row: ghost iff T (p + d) < p d; ties instantiate
+    oracle = pytest.importorskip("oracle")
+    for T in (0, 1, 2, 3, 7, 64, 255, 256, 257, 1024):
+        for d in (0, 1, 2, 4, 8, 384, 512, 768, 3072):
+            for p in (0, 1, 4, 8, 512, 768, 3072):
+                assert bk.bk_use_ghost_time(T, d, p) == oracle.use_ghost_time(T, d, p), (T, d, p)
+    assert not bk.bk_use_ghost_time(1024, 768, 3072) and bk.bk_use_ghost(1024, 768, 3072)
+    assert not bk.bk_use_ghost_time(2, 4, 4)              # tie instantiates
+    assert bk.lib.bk_use_ghost_time(1, -2, 3) == -1
+    # no overflow: T (p + d) near 2^127
+    big = (1 << 63) - 1
+    assert not bk.bk_use_ghost_time(big, big, big)
+    assert bk.bk_use_ghost_time(1, big, big)
+    assert not bk.bk_use_ghost_time(big, 1, big)
+
+
+def test_time_rule_flag_switches_the_norm_path():
+    """A layer ghost by space and instantiated by time: with BK_LAYER_TIME_RULE
+    a BK-MixOpt layer needs its store P, and the workspace follows the plan."""
+    arr = (bk.bk_layer * 1)()
+    arr[0].kind, arr[0].T, arr[0].d, arr[0].p = bk.BK_LINEAR, 256, 384, 384   # 131072 < 147456; 196608 >= 147456
+    arr[0].x = arr[0].g = arr[0].G = 0x10000
+    arr[0].flags = bk.BK_LAYER_MIXOPT
+    ws_space = bk.bk_layer_norms_workspace_size(arr, 1, bk.BK_BF16, 4)
+    need = bk.bk_layer_norms_workspace_size(arr, 1, bk.BK_BF16, 4)
+    assert bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, need - 1, None) == bk.BK_ERR_WORKSPACE
+    arr[0].flags = bk.BK_LAYER_MIXOPT | bk.BK_LAYER_TIME_RULE
+    st = bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    assert st == bk.BK_ERR_INVALID_VALUE and "needs P" in bk.bk_last_error()
+    ws_time = bk.bk_layer_norms_workspace_size(arr, 1, bk.BK_BF16, 4)
+    assert ws_time == bk.bk_workspace_size(bk.BK_OP_INST_NORM, bk.BK_BF16, 4, 256, 384, 384)
+    assert ws_space == bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_BF16, 4, 256, 384, 384)
+    arr[0].flags = 16                                            # unknown bit
+    st = bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+    assert st == bk.BK_ERR_INVALID_VALUE and "unknown flags" in bk.bk_last_error()
+
+
 def test_workspace_sizes():
     ws = bk.bk_workspace_size(bk.BK_OP_GHOST_NORM, bk.BK_BF16, 32, 128, 768, 768)
     assert ws == 256 and ws >= 32 * 4           # one partial per sample, padded to 256 B
@@ -156,7 +194,7 @@ def test_grouped_validation():
     for k in range(2):
         arr[k].kind, arr[k].T, arr[k].d, arr[k].p = bk.BK_LINEAR, 8, 16, 16
         arr[k].x = arr[k].g = arr[k].G = 0x10000
-    arr[1].flags = 8                                        # not a known flag
+    arr[1].flags = 16                                       # not a known flag
     st = bk.lib.bk_layer_norms(arr, 2, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
     assert st == bk.BK_ERR_INVALID_VALUE and "flags" in bk.bk_last_error()
     arr[1].flags = 0

@@ -458,6 +458,53 @@ def test_private_grad_stack_matches_oracle(bk, dtype):
                 assert _frob(G[l], want) <= GRAD_TOL[dtype], l
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_time_rule_stack_matches_oracle(bk, dtype):
+    """BK_LAYER_TIME_RULE: the layerwise decision by time (ghost iff T(p+d) <
+    pd).  Two layers change path against the space rule (one by a tie); each
+    layer's norms are bitwise those of the per-layer call of the path the rule
+    picks, and the whole path with BK-MixOpt (a store on every layer the time
+    rule instantiates) matches the oracle run with the same rule."""
+    Lr = wl.Layer
+    layers = [Lr("linear", 256, 384, 384),    # space ghost (131072 < 147456), time inst
+              Lr("linear", 128, 256, 256),    # space ghost, time tie 65536 == 65536: inst
+              Lr("linear", 32, 256, 520),     # ghost both ways
+              Lr("linear", 200, 96, 136)]     # inst both ways
+    B = 3
+    ins = _stack_inputs(layers, B, dtype, seed=77)
+    time_ghost = [bk.bk_use_ghost_time(L.T, L.d, L.p) for L in layers]
+    assert time_ghost == [False, False, True, False]
+    assert [bk.bk_use_ghost(L.T, L.d, L.p) for L in layers] == [True, True, True, False]
+    dev_ins = [(x.to(DEV), g.to(DEV)) for x, g in ins]
+    Gs = [torch.empty(L.d, L.p, device=DEV) for L in layers]
+    Ps = [None if tg else torch.empty(B, L.d, L.p, device=DEV) for L, tg in zip(layers, time_ghost)]
+    specs = [{"kind": bk.BK_LINEAR, "x": x, "g": g, "G": G, "P": P, "mixopt": True, "time_rule": True}
+             for (x, g), G, P in zip(dev_ins, Gs, Ps)]
+    arr = bk.make_layers(specs)
+    n = len(layers)
+    dt = bk.BK_BF16 if dtype == torch.bfloat16 else bk.BK_F32
+    norm_sq = torch.empty(n, B, device=DEV)
+    bk.bk_layer_norms(arr, n, dt, B, norm_sq)
+    torch.cuda.synchronize()
+    for l, ((x, g), tg) in enumerate(zip(dev_ins, time_ghost)):
+        one = (bk.bk_ghost_norm if tg else bk.bk_inst_norm)(x, g)
+        torch.cuda.synchronize()
+        assert torch.equal(norm_sq[l], one), l
+    C = torch.empty(B, device=DEV)
+    tot = torch.empty(B, device=DEV)
+    bk.bk_private_grad(arr, n, dt, B, bk.BK_CLIP_AUTO, 1.0, 0.01, 0.0, 5, 0, norm_sq, C, tot)
+    torch.cuda.synchronize()
+    ref = oracle.bk_stack(layers, ins, "auto", 1.0, 0.01, 0.0, seed=5, with_noise=False, mixopt=True,
+                          rule=oracle.use_ghost_time)
+    assert ref["paths"] == ["inst", "inst", "ghost", "inst"]
+    guard = NORM_GUARD if dtype == torch.bfloat16 else NORM_TOL[dtype]
+    assert _rel(norm_sq.cpu().numpy(), ref["norms"]) <= guard
+    assert _rel(tot.cpu().numpy(), ref["total"]) <= guard
+    assert _rel(C.cpu().numpy(), ref["C"]) <= guard
+    for l in range(n):
+        assert _frob(Gs[l].cpu().numpy(), ref["G"][l]) <= GRAD_TOL[dtype], l
+
+
 def test_config1_single_layer(bk):
     """Single fp32 linear layer, B=4, T=16, d=p=64, Abadi R=1, sigma=1: the
     ghost path against brute-force per-sample gradients."""
