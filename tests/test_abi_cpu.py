@@ -359,3 +359,29 @@ def test_noalloc_rejects_stacks_beyond_its_scratch():
     st = bk.lib.bk_private_grad_noalloc(arr, n, bk.BK_BF16, w.B, bk.BK_CLIP_AUTO, 1.0, 0.01, 1.0, 0, 0,
                                         FAKE, FAKE, None, None)
     assert st == bk.BK_ERR_NOT_SUPPORTED and "scratch" in bk.bk_last_error()
+
+
+def test_last_error_is_per_thread():
+    """bk_last_error() reports the calling thread's own last failure while other
+    threads fail at the same time (the ctypes calls release the GIL)."""
+    import threading
+    errors = []
+
+    def worker(k):
+        arr = (bk.bk_layer * 1)()
+        arr[0].T, arr[0].d, arr[0].p = 8, 16, 16
+        arr[0].x = arr[0].g = arr[0].G = 0x10000
+        arr[0].kind = 10 + k                                  # a distinct unknown kind per thread
+        for _ in range(300):
+            st = bk.lib.bk_layer_norms(arr, 1, bk.BK_BF16, 4, FAKE, FAKE, 1 << 20, None)
+            msg = bk.bk_last_error()
+            if st != bk.BK_ERR_INVALID_VALUE or f"unknown kind {10 + k}" not in msg:
+                errors.append((k, st, msg))
+                return
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(8)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors[:3]
