@@ -1,10 +1,13 @@
 """Pins of the oracle's Gaussian-noise generator (CPU only).
 
-* Philox4x32-10 words against rocRAND's independent implementation of the same
-  published generator (its header-only engine, compiled here for the host).
+* Philox4x32-10 words against the known-answer vectors published with the
+  generator (tests/golden/philox4x32_10_kat.json), and against rocRAND's
+  independent implementation of it (its header-only engine, compiled here for
+  the host) on many counters.
 * The uniform mapping and Box-Muller transform against their definitions and
   the standard normal law (moments, Kolmogorov-Smirnov).
 """
+import json
 import os
 import shutil
 import subprocess
@@ -17,6 +20,24 @@ from scipy import stats
 import oracle
 
 HERE = os.path.dirname(os.path.abspath(__file__))
+KAT = os.path.join(HERE, "golden", "philox4x32_10_kat.json")
+
+
+def _kat():
+    return [([int(x, 16) for x in v["counter"]], [int(x, 16) for x in v["key"]], [int(x, 16) for x in v["out"]])
+            for v in json.load(open(KAT))["vectors"]]
+
+
+def test_philox_known_answer_vectors():
+    for ctr, key, out in _kat():
+        got = [int(w) for w in oracle.philox4x32_10(ctr, key)]
+        assert got == out, (ctr, key)
+    # the library's counter layout: block q of (seed, tensor, step) is the
+    # counter (q lo, q hi, tensor, step) under the key (seed lo, seed hi)
+    for ctr, key, out in _kat():
+        seed, q = key[0] | (key[1] << 32), ctr[0] | (ctr[1] << 32)
+        words = oracle.philox_words(seed, ctr[2], ctr[3], q, 1)
+        assert [int(w) for w in np.asarray(words).reshape(-1)] == out
 
 
 @pytest.fixture(scope="module")
