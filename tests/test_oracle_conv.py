@@ -62,3 +62,54 @@ def test_conv_per_sample_grads_and_norms_match_autograd():
     s = torch.nn.functional.conv2d(x, Wv, stride=stride, padding=pad)
     (s * dy * torch.tensor(C).view(B, 1, 1, 1)).sum().backward()
     np.testing.assert_allclose(G, Wv.grad.reshape(Cout, -1).numpy().T, rtol=1e-12, atol=1e-12)
+
+
+def _printed(x, v, sig):
+    """x rounds to the printed value v (sig significant figures)."""
+    if v == int(v) and v < 10:
+        return x == v
+    e = int(np.floor(np.log10(abs(v)))) - (sig - 1)
+    return abs(x - v) <= 0.5 * 10.0 ** e
+
+
+def test_resnet18_stack_reproduces_the_layerwise_decision_table():
+    """The ResNet-18 stack at 224 x 224 (workload 6 without its three 1 x 1
+    downsampling convolutions, which the paper's table leaves out): the output
+    sizes from conv_out_size, the space of both ways (2T^2 with T = H_out W_out,
+    p d with d = C_in k^2), the layer counts, the choice of use_ghost and the
+    three totals reproduce the printed 18-layer column of Table "layerwise
+    decision"."""
+    import json
+    import os
+    import workloads as wl
+    tab = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "layerwise_decision_resnet18.json")))
+    layers = [L for L in wl.get(6).layers if L.kind != "conv" or L.conv[1] != 1]
+    assert len(layers) == 18
+    rows = []
+    for L in layers:
+        if L.kind == "conv":
+            cin, k, stride, pad, hin = L.conv
+            ho = oracle.conv_out_size(hin, k, stride, pad)
+            assert ho * ho == L.T
+            d = cin * k * k
+        else:
+            ho, d = 1, L.d
+        ghost = oracle.use_ghost(L.T, d, L.p)
+        assert oracle.use_ghost(L.T, L.d, L.p) == ghost          # padding d to 8 changes no choice here
+        rows.append((ho, 2 * L.T * L.T, d * L.p, ghost))
+    for st in tab["stages"]:
+        mine = [r for r in rows if r[0] == st["hout"]]
+        for key, col in (("ghost", 1), ("inst", 2)):
+            printed = [(v, c) for v, c in st[key]]
+            assert sum(c for _, c in printed) == len(mine), st["name"]
+            vals = [r[col] for r in mine]
+            for v, c in printed:                 # each printed group matches c layers of the stage
+                hit = [x for x in vals if _printed(x, v, 2)]
+                assert len(hit) == c, (st["name"], key, v)
+        assert all(r[3] == (st["bold"] == "ghost") for r in mine), st["name"]
+    tot_g = sum(r[1] for r in rows)
+    tot_i = sum(r[2] for r in rows)
+    tot_m = sum(min(r[1], r[2]) for r in rows)
+    assert _printed(tot_g, *tab["total_ghost"])
+    assert _printed(tot_i, *tab["total_inst"])
+    assert _printed(tot_m, *tab["total_mixed"])
