@@ -232,7 +232,7 @@ def _narrow(L) -> bool:
     return min(L.d, L.p) <= 64 and max(L.d, L.p) >= 128
 
 
-def norm_kernel(L, dtype: str = "bf16", time_rule: bool = False) -> str:
+def norm_kernel(L, dtype: str = "bf16", time_rule: bool = False, B: int = 1) -> str:
     """Kernel that takes layer L's norm (the library's rule for 16-byte rows; a label only)."""
     if L.kind == "embed":
         # 8 | p: the id join; else the masked Gram
@@ -243,7 +243,13 @@ def norm_kernel(L, dtype: str = "bf16", time_rule: bool = False) -> str:
         return "ghost_full_kernel" if L.T <= 256 else "ghost_long_kernel"
     if dtype != "bf16":
         return "agemm_kernel"
-    return "anarrow_kernel" if _narrow(L) else "agemm_bf16_kernel"
+    if _narrow(L):
+        return "anarrow_kernel"
+    # whole 256 x 256 tiles on the DMA kernel when the layer gives at least 128 of them
+    tiles = -(-L.d // 256) * -(-L.p // 256)
+    if L.T >= 64 and 8 * (-(-L.T // 16) * 16) <= 9 * L.T and B * tiles >= 128:
+        return "agrad_dl_kernel"
+    return "agemm_bf16_kernel"
 
 
 def grad_kernel(L, dtype: str = "bf16") -> str:
@@ -265,7 +271,7 @@ def dominant_kernel(w: wl.Workload, phase: str, time_rule: bool = False) -> str:
     share = {}
     for L in w.layers:
         if phase == "norms":
-            k = norm_kernel(L, w.dtype, time_rule)
+            k = norm_kernel(L, w.dtype, time_rule, w.B)
             f = 2.0 * L.T * L.T * (L.p + L.d) if k.startswith("ghost_") else 2.0 * L.T * L.p * L.d
         else:
             k, f = grad_kernel(L, w.dtype), 2.0 * L.T * L.p * L.d
@@ -512,7 +518,7 @@ def main():
         gk, what = "conv_prep_kernel", "unfold + token-major transpose of every conv layer, one launch"
     else:
         gk = dominant_kernel(w, dom, args.time_rule)
-        kinds = {grad_kernel(L, w.dtype) if dom == "weighted_grads" else norm_kernel(L, w.dtype, args.time_rule)
+        kinds = {grad_kernel(L, w.dtype) if dom == "weighted_grads" else norm_kernel(L, w.dtype, args.time_rule, w.B)
                  for L in w.layers}
         what = ("clipped gradients" if dom == "weighted_grads" else "per-sample norms") + \
                (", all layers in one launch" if len(kinds) == 1 else ", one launch per kernel variant")

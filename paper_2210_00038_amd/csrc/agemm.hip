@@ -1038,6 +1038,12 @@ struct StagePos {
 // instructions of the stage three ahead among the first eight), and every
 // phase ends at a workgroup barrier.  Waves 4-7 run one phase behind waves
 // 0-3, so that on every SIMD one wave issues MFMAs while the other reads.
+//
+// INST (per-sample gradient instantiation, App. B.4.1): workgroup = (sample,
+// tile), its stages those of the one sample, no weights (every other stage
+// loads zeros); the epilogue sums the squares of the tile's d x p entries
+// into one norm partial per (sample, tile) and, when L.G is set (BK-MixOpt),
+// stores the tile of the sample's gradient into L.G + sample d p.
 // The buffer refilled during the MFMA phase of stage s, (s + 3) mod 4, was
 // last read in the memory phases of stage s - 1, which both halves have
 // passed; a stage's buffer is complete once every wave has waited for its
@@ -1048,9 +1054,10 @@ constexpr int kDStage = 2 * kDOp;
 constexpr int kDKK = kDKS / 16;                  // 16-row MFMA steps per stage
 constexpr int kDPW = kDKS / 8;                   // DMA instructions per wave per stage
 
+template <bool INST>
 __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, int n_remap) {
     __shared__ __attribute__((aligned(16))) char lds[kDNB * kDStage];
-    __shared__ float ctab[kDMaxB + 1];
+    __shared__ float ctab[INST ? 8 : kDMaxB + 1];   // INST: the epilogue's wave sums
 
     // The first n_remap workgroups in contiguous runs per XCD; the tail (the
     // K slices of the last round's tiles) in launch order, so that it is
@@ -1060,11 +1067,13 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     const GemmLayer& L = args.L[l];
     const int nT = L.T, d = L.d, p = L.p, tn = L.tn;
     const int local = wg - L.wg_begin, sf = L.split_from;
-    // Tiles below split_from whole, the others in ksplit slices.
-    const int ks = local < sf ? 1 : max(L.ksplit, 1);
-    const int rel = local < sf ? 0 : (local - sf) / ks;              // split tile, from split_from
-    const int tile = local < sf ? local : sf + rel;
-    const int slice = local < sf ? 0 : (local - sf) - rel * ks;
+    // Clipped gradient: tiles below split_from whole, the others in ksplit
+    // slices.  INST: workgroup = sample * tiles + tile, never split.
+    const int sample = INST ? local / (L.tm * tn) : 0;
+    const int ks = INST || local < sf ? 1 : max(L.ksplit, 1);
+    const int rel = INST || local < sf ? 0 : (local - sf) / ks;      // split tile, from split_from
+    const int tile = INST ? local - sample * (L.tm * tn) : local < sf ? local : sf + rel;
+    const int slice = INST || local < sf ? 0 : (local - sf) - rel * ks;
     const int mt = tile / tn, nt = tile - mt * tn;
     const int m0 = mt * kGM, n0 = nt * kGN;
 
@@ -1079,7 +1088,8 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 2, wn = wave & 3;
     // Clip weights, and a zero for the stages past the batch.
-    for (int i = tid; i <= B; i += 512) ctab[i] = i < B ? args.C[i] : 0.f;
+    if constexpr (!INST)
+        for (int i = tid; i <= B; i += 512) ctab[i] = i < B ? args.C[i] : 0.f;
 
     // DMA: each operand stage is KS / 2 instructions of 1 KB (two rows); wave
     // w (of 8) issues numbers j = 8 i + w, i < KS / 16, and lane l moves
@@ -1123,11 +1133,16 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // The last stage of a sample holds at most 16 rows (16-row MFMA steps,
     // the second one all zeros): its second step is skipped.
     const bool short_last = (uint32_t)nT - (spt - 1) * kDKS <= 16u;
-    // This workgroup's stages (K slice `slice` of `ks`).
-    const uint32_t st_begin = (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
-    const uint32_t st_end = (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
-    // Weight of the stage at `pos` (0 past the batch).
-    auto cw_of = [&](const StagePos& pos) { return ctab[min(pos.smp, (uint32_t)B)]; };
+    // This workgroup's stages (K slice `slice` of `ks`; INST: its sample's).
+    const uint32_t st_begin = INST ? (uint32_t)sample * spt : (uint32_t)((uint64_t)slice * nst_all / (uint32_t)ks);
+    const uint32_t st_end = INST ? (uint32_t)(sample + 1) * spt
+                                 : (uint32_t)((uint64_t)(slice + 1) * nst_all / (uint32_t)ks);
+    // Weight of the stage at `pos` (0 past the batch; INST: 1 in the sample,
+    // 0 elsewhere).
+    auto cw_of = [&](const StagePos& pos) {
+        if constexpr (INST) return pos.smp == (uint32_t)sample ? 1.f : 0.f;
+        else return ctab[min(pos.smp, (uint32_t)B)];
+    };
 
     float c_last = 0.f;   // weight of the last sample with a nonzero weight
     static_assert(kDNB == 4 && kDKK == 2 && kDPW == 4, "ping-pong ring");
@@ -1171,7 +1186,7 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
 #pragma unroll
                 for (int h = 0; h < 2; ++h) fb[kk][y][h] = frag_dl_half(Bt, 16 * kk, 64 * wn + 32 * y, lane, h);
         }
-        if (pos0.in == 0u || st == st_begin) {
+        if (!INST && (pos0.in == 0u || st == st_begin)) {
             const float c = cw_of(pos0);
             const bool nz = c != 0.f;
             const float r = nz ? c_last / c : 1.f;
@@ -1223,6 +1238,45 @@ __global__ __launch_bounds__(512, 1) void agrad_dl_kernel(const GemmArgs args, i
     // Drain the DMA past the end before the workgroup exits.
     wait_vmcnt<0>();
 
+    if constexpr (INST) {
+        // Rows and columns past d and p loaded zeros, so their entries are 0.
+        float sq = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) sq += acc[x][y][e] * acc[x][y][e];
+        sq = wave_sum(sq);
+        if (lane == 0) ctab[wave] = sq;
+        __syncthreads();
+        if (tid == 0) {
+            float t = 0.f;
+#pragma unroll
+            for (int w = 0; w < 8; ++w) t += ctab[w];
+            args.part[(size_t)L.part_off + (size_t)sample * (L.tm * tn) + tile] = t;
+        }
+        if (L.G) {   // BK-MixOpt: the sample's gradient a_i^T g_i [d, p]
+            float* P = L.G + (size_t)sample * d * p;
+            if ((reinterpret_cast<uintptr_t>(P) & 15u) == 0) {
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+#pragma unroll
+                    for (int y = 0; y < 2; ++y)
+                        put_acc_x4(P, (size_t)p, m0 + 128 * wm + 32 * x, d, n0 + 64 * wn + 32 * y, p, lane,
+                                   acc[x][y], 1.f, false);
+            } else {
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+#pragma unroll
+                    for (int y = 0; y < 2; ++y) {
+                        const int n = n0 + 64 * wn + 32 * y + (lane & 31);
+                        if (n < p) put_col16(P, (size_t)p, 1, m0 + 128 * wm + 32 * x, d, n, lane, acc[x][y], 1.f, false);
+                    }
+            }
+        }
+        return;
+    }
     if (ks > 1) {
         store_partial_tile<kGM, kGN>(args.tiles + L.ptile_off + ((size_t)rel * ks + slice) * (kGM * kGN),
                                      acc, 128 * wm, 64 * wn, lane, c_last);
@@ -1346,9 +1400,9 @@ hipError_t launch_gemm(const GemmArgs& args, int n_wg, bool bf16, bool inst_norm
         return hipGetLastError();
     }
     if (v == GemmVariant::GradDL) {
-        if (inst_norm) return hipErrorInvalidValue;
         const int nr = n_remap > 0 && n_remap < n_wg ? n_remap : n_wg;
-        hipLaunchKernelGGL(agrad_dl_kernel, grid, dim3(512), 0, s, args, nr);
+        if (inst_norm) hipLaunchKernelGGL(agrad_dl_kernel<true>, grid, dim3(512), 0, s, args, nr);
+        else hipLaunchKernelGGL(agrad_dl_kernel<false>, grid, dim3(512), 0, s, args, nr);
         return hipGetLastError();
     }
     if (v == GemmVariant::Wide) {

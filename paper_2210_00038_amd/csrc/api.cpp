@@ -133,13 +133,28 @@ int64_t narrow_grad_ksplit(int64_t tiles, int64_t nst) {
     return std::min<int64_t>(64, cdiv(nst, 16));
 }
 
-void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt) {
+// Stages per sample of the GradDL kernel: every sample starts a stage, its
+// last stage padded with zero rows.  The MFMAs run over T rounded up to
+// 16-row steps (a last stage of at most 16 rows skips its second step).
+int64_t dl_stages_per_sample(int64_t T) { return cdiv(T, bk::kDLStageRows); }
+bool dl_padding_ok(int64_t T) { return 8 * (cdiv(T, 16) * 16) <= 9 * T; }   // at most 1/8 padding
+
+void set_norm_variant(NormPlan& np, const bk_layer& L, bk_dtype dt, int64_t B) {
     const size_t es = elem_bytes(dt);
     if (np.path == Path::Affine) {
         np.npart = 0;
         np.var = 0;
     } else if (np.path == Path::Inst) {
-        const auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
+        auto v = bk::gemm_variant(dt == BK_BF16, L.d, L.p, L.T, aligned16(L.x) && aligned16(L.g));
+        // 256 x 256 tiles on the LDS-DMA kernel (one workgroup per sample and
+        // tile) when the layer gives at least 128 of them: the wide kernel's
+        // 256 x 128 tiles at two workgroups per CU fill the chip no better,
+        // and below that it can split K.  Each sample is padded to 16-row
+        // steps by at most 1/8, and B T rows stay below 2^31.
+        if (v == bk::GemmVariant::Wide && L.T >= 64 && dl_padding_ok(L.T) && B * L.T < ((int64_t)1 << 31)) {
+            const bk::GemmGeom dl = bk::gemm_geom(bk::GemmVariant::GradDL, L.d, L.p);
+            if (B * dl.tm * dl.tn >= 128) v = bk::GemmVariant::GradDL;
+        }
         const bk::GemmGeom geo = bk::gemm_geom(v, L.d, L.p);
         np.var = (int)v;
         np.tiles = geo.tm * geo.tn;
@@ -226,7 +241,7 @@ NormPlan norm_plan(const bk_layer& L, bk_dtype dt, int64_t B) {
     } else {
         np.path = layer_ghost(L) ? Path::Ghost : Path::Inst;
     }
-    set_norm_variant(np, L, dt);
+    set_norm_variant(np, L, dt, B);
     finish_norm_plan(np, L, B);
     return np;
 }
@@ -518,12 +533,6 @@ bk_status layer_norms(const char* fn, const bk_layer* layers, int64_t n, bk_dtyp
     }
     return BK_OK;
 }
-
-// Stages per sample of the GradDL kernel: every sample starts a stage, its
-// last stage padded with zero rows.  The MFMAs run over T rounded up to
-// 16-row steps (a last stage of at most 16 rows skips its second step).
-int64_t dl_stages_per_sample(int64_t T) { return cdiv(T, bk::kDLStageRows); }
-bool dl_padding_ok(int64_t T) { return 8 * (cdiv(T, 16) * 16) <= 9 * T; }   // at most 1/8 padding
 
 // Kernel variant of a linear layer's clipped gradient: narrow layers with
 // T >= 64 run on the narrow kernel (shorter T on the wide one), the other
@@ -840,7 +849,7 @@ bk_status single_norm(const char* fn, Path want, const bk_layer& L, bk_dtype dt,
     if (B > 0 && !norm_sq) return fail(BK_ERR_INVALID_VALUE, "%s: NULL norm output", fn);
     std::vector<NormPlan> one(1);
     one[0].path = want;
-    set_norm_variant(one[0], L, dt);
+    set_norm_variant(one[0], L, dt, B);
     finish_norm_plan(one[0], L, B);
     demote_small_full(one, &L, B);
     const NormPlan np = one[0];
@@ -942,7 +951,7 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
                 L.kind = BK_EMBEDDING;
                 NormPlan np{};
                 np.path = Path::Embed;
-                set_norm_variant(np, L, dt);
+                set_norm_variant(np, L, dt, B);
                 npart = std::max(npart, np.npart);
             }
             return align_up((size_t)(B * npart) * sizeof(float));
@@ -952,7 +961,7 @@ size_t bk_workspace_size(bk_op op, bk_dtype dt, int64_t B, int64_t T, int64_t d,
             L.kind = BK_LINEAR;
             NormPlan np{};
             np.path = Path::Inst;
-            set_norm_variant(np, L, dt);     // NULL pointers count as aligned
+            set_norm_variant(np, L, dt, B);  // NULL pointers count as aligned
             finish_norm_plan(np, L, B);
             return std::max(small, norm_ws_bytes(np, B));
         }

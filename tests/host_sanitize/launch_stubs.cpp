@@ -93,6 +93,11 @@ hipError_t launch_gemm(const GemmArgs& a, int n_wg, bool, bool inst, GemmVariant
         const GemmGeom geo = gemm_geom(v, L.d, L.p);
         need(L.tm == geo.tm && L.tn == geo.tn, "gemm tiles");
         const int64_t tiles = (int64_t)L.tm * L.tn;
+        if (inst && v == GemmVariant::GradDL) {
+            // one workgroup per (sample, tile), never split, no clip weights
+            need(L.ksplit <= 1 && a.C == nullptr && (int64_t)a.B * L.T < ((int64_t)1 << 31) && L.T >= 64,
+                 "LDS-DMA instantiated norm");
+        }
         if (inst) {
             const int64_t parts = L.ksplit > 1 ? tiles * (geo.tile_elems / kSplitRedWG) : tiles;
             in_ws(a.part, L.part_off, (int64_t)a.B * parts, 4, "inst partials");

@@ -17,7 +17,7 @@ import workloads as wl
 pytestmark = pytest.mark.gpu
 
 NORM_TOL = {torch.float32: 1e-5, torch.bfloat16: 2e-2}
-from tolerances import NORM_GUARD  # noqa: E402
+from tolerances import NORM_GUARD, GRAD_GUARD_EXACT  # noqa: E402
 GRAD_TOL = {torch.float32: 1e-4, torch.bfloat16: 2e-2}
 DEV = "cuda"
 
@@ -611,6 +611,40 @@ def test_private_grad_mixopt_matches_oracle(bk, dtype):
 # Layers with few output tiles and a long contraction (convolutions at image
 # scale, skinny adapters) cut each tile's K range into slices whose partial
 # tiles are added in order by a second kernel.
+@pytest.mark.parametrize("B,T,d,p", [
+    (32, 200, 296, 264),      # 2 x 2 tiles, ragged d and p; T = 6 stages + 8 rows (short last stage)
+    (128, 256, 256, 256),     # exactly 128 (sample, tile) workgroups
+    (127, 256, 256, 256),     # one fewer: the wide kernel
+    (16, 1024, 768, 768)])    # the long-sequence stack's instantiated layer
+def test_inst_norm_on_dma_kernel(bk, B, T, d, p):
+    """bf16 instantiated norms of layers with at least 128 (sample, 256 x 256
+    tile) pairs run on the LDS-DMA kernel: norms against the definition, the
+    kept per-sample gradients (BK-MixOpt) against the oracle's, the grouped
+    call bitwise equal to the single-layer one, and a zero sample exactly 0."""
+    a, g = _pair(B, T, d, p, torch.bfloat16, seed=B + T + d, g_scale=1e-2)
+    a[1].zero_()
+    ref = oracle.linear_norm_sq(a, g)
+    ad, gd = a.to(DEV), g.to(DEV)
+    one = bk.bk_inst_norm(ad, gd)
+    assert _rel(one.cpu().numpy(), ref) <= NORM_GUARD
+    assert one[1].item() == 0.0
+    specs = [{"kind": bk.BK_LINEAR, "x": ad, "g": gd, "G": torch.empty(d, p, device=DEV)}]
+    arr = bk.make_layers(specs)
+    assert not bk.bk_use_ghost(T, d, p)
+    grouped = torch.empty(1, B, device=DEV)
+    bk.bk_layer_norms(arr, 1, bk.BK_BF16, B, grouped)
+    torch.cuda.synchronize()
+    assert torch.equal(grouped[0], one)
+    if B * d * p <= (1 << 27):
+        norm, P = bk.bk_per_sample_grads(ad, gd)
+        assert torch.equal(norm, one)
+        ref_P = oracle.per_sample_grads(a, g)
+        P = P.cpu().numpy()
+        for i in range(B):
+            assert _frob(P[i], ref_P[i]) <= GRAD_GUARD_EXACT, i
+        assert not P[1].any()
+
+
 @pytest.mark.parametrize("B,T,d,p", [
     (2, 2048, 152, 64),      # one 256 x 128 tile per sample, 8 slices
     (3, 1000, 96, 200),      # ragged T, one tile, 4 slices
