@@ -1038,16 +1038,16 @@ struct StagePos {
 // instructions of the stage three ahead among the first eight), and every
 // phase ends at a workgroup barrier.  Waves 4-7 run one phase behind waves
 // 0-3, so that on every SIMD one wave issues MFMAs while the other reads.
+// The buffer refilled during the MFMA phase of stage s, (s + 3) mod 4, was
+// last read in the memory phases of stage s - 1, which both halves have
+// passed; a stage's buffer is complete once every wave has waited for its
+// DMA of it before the barrier that precedes the first reads of it.
 //
 // INST (per-sample gradient instantiation, App. B.4.1): workgroup = (sample,
 // tile), its stages those of the one sample, no weights (every other stage
 // loads zeros); the epilogue sums the squares of the tile's d x p entries
 // into one norm partial per (sample, tile) and, when L.G is set (BK-MixOpt),
 // stores the tile of the sample's gradient into L.G + sample d p.
-// The buffer refilled during the MFMA phase of stage s, (s + 3) mod 4, was
-// last read in the memory phases of stage s - 1, which both halves have
-// passed; a stage's buffer is complete once every wave has waited for its
-// DMA of it before the barrier that precedes the first reads of it.
 // ---------------------------------------------------------------------------
 constexpr int kDOp = kDKS * kDRow;               // one operand of one stage
 constexpr int kDStage = 2 * kDOp;
