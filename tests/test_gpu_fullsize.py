@@ -55,7 +55,7 @@ def _frob(x, ref):
 class Stack:
     """Device inputs and outputs of one workload, laid out as bench.py lays them."""
 
-    def __init__(self, bk, w):
+    def __init__(self, bk, w, time_rule=False, mixopt=False):
         self.bk, self.w = bk, w
         B, n = w.B, len(w.layers)
         self.raw = [wl.draw_layer(w, l, device=DEV) for l in range(n)]
@@ -77,10 +77,15 @@ class Stack:
         # the per-sample gamma / bias sums pass from the norm phase to the
         # gradient phase through these buffers: the Stack keeps them alive
         self.Ps = [torch.empty(B, L.p, device=DEV) if L.kind == "norm" else None for L in w.layers]
+        if mixopt:   # BK-MixOpt: the layers that instantiate keep their per-sample gradients
+            rule = bk.bk_use_ghost_time if time_rule else bk.bk_use_ghost
+            self.Ps = [torch.empty(B, L.d, L.p, device=DEV) if L.kind in ("linear", "conv") and
+                       not rule(L.T, L.d, L.p) else P for L, P in zip(w.layers, self.Ps)]
         self.Pbs = [torch.empty(B, L.p, device=DEV) if L.bias else None for L in w.layers]
         kinds = {"embed": bk.BK_EMBEDDING, "norm": bk.BK_NORM_AFFINE}
         self.arr = bk.make_layers([{"kind": kinds.get(L.kind, bk.BK_LINEAR), "x": x, "g": g, "G": G,
-                                    "V": L.d, "P": P, "bias": L.bias, "Gb": Gb, "Pb": Pb}
+                                    "V": L.d, "P": P, "bias": L.bias, "Gb": Gb, "Pb": Pb,
+                                    "time_rule": time_rule, "mixopt": mixopt}
                                    for L, (x, g), G, P, Gb, Pb in
                                    zip(w.layers, self.ins, self.Gs, self.Ps, self.Gbs, self.Pbs)])
         self.mode = bk.BK_CLIP_ABADI if w.clip == "abadi" else bk.BK_CLIP_AUTO
@@ -303,4 +308,36 @@ def test_gpt2_full_accumulate_doubles(bk):
         assert torch.equal(st.Gs[l], 2 * G1[l]), l
         assert torch.equal(st.Gbs[l], 2 * Gb1[l]), l
     del st, G1, Gb1
+    torch.cuda.empty_cache()
+
+
+def test_long_stack_time_rule_mixopt(bk):
+    """The long-sequence stack (36 layers, T = 1024, B = 16) with the decision
+    by time and BK-MixOpt: every layer is instantiated on the LDS-DMA kernel
+    and keeps its per-sample gradients, and each clipped gradient is their
+    weighted sum.  Norms, totals and clip factors against the oracle's;
+    sampled entries of every G against the oracle with the oracle's C."""
+    w = wl.get(3)
+    n, B = len(w.layers), w.B
+    assert not any(bk.bk_use_ghost_time(L.T, L.d, L.p) for L in w.layers)
+    st = Stack(bk, w, time_rule=True, mixopt=True)
+    norms, C, tot = st.private_grad(0.0)
+    rng = np.random.default_rng(33)
+    pos = {l: (_pick(rng, L.d), _pick(rng, L.p)) for l, L in enumerate(w.layers)}
+    got = {l: _take(st.Gs[l], *pos[l]) for l in range(n)}
+    ref_norms = np.zeros((n, B))
+    keep = {}
+    for l, L in enumerate(w.layers):
+        x, g = _oracle_inputs(w, l, st.raw[l])
+        ref_norms[l] = _oracle_norm(L, x, g)
+        assert _rel(norms[l], ref_norms[l]) <= NORM_GUARD, l
+        keep[l] = (x[:, :, pos[l][0]], g[:, :, pos[l][1]])
+        del x, g
+    ref_tot = oracle.aggregate(ref_norms)
+    ref_C = oracle.clip_factors(ref_tot, w.clip, w.R, w.gamma)
+    assert _rel(tot, ref_tot) <= NORM_GUARD and _rel(C, ref_C) <= NORM_GUARD
+    for l in range(n):
+        ref = oracle.weighted_grad(*keep[l], ref_C)
+        assert _frob(got[l], ref) <= GRAD_GUARD_EXACT, l
+    del st
     torch.cuda.empty_cache()
