@@ -1,10 +1,12 @@
 """Build libbk.so (the HIP kernels and the C ABI of include/bk.h) for gfx950.
 
-    python paper_2210_00038_amd/build.py
+    python paper_2210_00038_amd/build.py [--ceiling]
 
 Every source is compiled by hipcc into an object in ``_build/`` (in parallel),
 then linked into ``paper_2210_00038_amd/libbk.so``.  Packed-fp32 instruction
-selection is switched off for all device code.
+selection is switched off for all device code.  ``--ceiling`` also builds
+``_build/gemm_loop``, the standalone microbenchmark of the clipped-gradient
+GEMM's inner loop (csrc/ceiling/gemm_loop.hip).
 """
 from __future__ import annotations
 
@@ -61,6 +63,21 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_ceiling(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    exe = os.path.join(BUILD, "gemm_loop")
+    flags = [f for f in FLAGS if f != "-fPIC"]
+    cmd = [hipcc(), *flags, "-x", "hip", os.path.join(CSRC, "ceiling", "gemm_loop.hip"), "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compiling the GEMM-loop microbenchmark failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {exe}")
+    return exe
+
+
 if __name__ == "__main__":
     build(verbose=True)
+    if "--ceiling" in sys.argv[1:]:
+        build_ceiling(verbose=True)
     sys.exit(0)
