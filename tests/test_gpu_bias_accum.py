@@ -203,3 +203,32 @@ def test_bias_sums_formed_in_the_ghost_pass(bk, dtype, T, d, p):
         assert _frob(bufs.Pb[l].cpu().numpy(), oracle.bias_sums(ins[l][1])) <= TOL[dtype], l
         assert _frob(bufs.Gb[l].cpu().numpy(), ref["Gb"][l]) <= TOL[dtype], l
         assert _frob(bufs.G[l].cpu().numpy(), ref["G"][l]) <= TOL[dtype], l
+
+
+def test_mixopt_accumulate_on_dma_instantiation(bk):
+    """BK-MixOpt with gradient accumulation on a layer whose instantiated norm
+    runs on the LDS-DMA kernel (bf16, 32 samples x 4 tiles of 256 x 256): the
+    per-sample gradients it keeps give each physical batch's clipped
+    gradient, added over two physical batches; against the oracle's logical
+    batch, with the kept gradients those of the last batch."""
+    from tolerances import GRAD_GUARD_EXACT, NORM_GUARD
+    layers = [_L("linear", 384, 512, 512, mixopt=True),   # 2T^2 >= pd: instantiated
+              _L("linear", 64, 128, 128)]                  # ghost
+    assert not bk.bk_use_ghost(384, 512, 512) and bk.bk_use_ghost(64, 128, 128)
+    B, nb, seed = 32, 2, 5
+    gen = torch.Generator().manual_seed(77)
+    batches = [_draw(layers, B, torch.bfloat16, gen) for _ in range(nb)]
+    bufs = _Bufs(bk, layers, B)
+    Cs = []
+    for b in range(nb):
+        _, C = _run(bk, layers, batches[b], bufs, B, torch.bfloat16, bk.BK_CLIP_AUTO, 1.0, 0.01, 0.0, seed, b > 0)
+        Cs.append(C)
+    ref = oracle.logical_batch(layers, batches, "auto", 1.0, 0.01, 0.0, seed)
+    for b in range(nb):
+        assert _rel(Cs[b], ref["C"][b]) <= NORM_GUARD, b
+    for l in range(len(layers)):
+        assert _frob(bufs.G[l].cpu().numpy(), ref["G"][l]) <= GRAD_GUARD_EXACT, l
+    P = bufs.P[0].cpu().numpy()
+    ref_P = oracle.per_sample_grads(*batches[-1][0])
+    for i in range(0, B, 7):
+        assert _frob(P[i], ref_P[i]) <= GRAD_GUARD_EXACT, i
